@@ -1,0 +1,232 @@
+/*
+ * gts.h -- C ABI of libgts: exact path-based TreeShap for AMD Instinct MI355X
+ * (gfx950), after Mitchell, Frank & Holmes, "GPUTreeShap: Massively Parallel
+ * Exact Calculation of SHAP Scores for Tree Ensembles" (arXiv 2010.13972).
+ *
+ * Pipeline (Section 3, steps 1-4):
+ *   gts_extract_paths   host   ensemble -> merged unique root-to-leaf paths
+ *   gts_pack_paths      host   paths -> bins of <= 64 path elements
+ *   gts_model_layout    host   packed paths -> one device-ready byte blob
+ *   gts_shap            device SHAP values              phi[rows][G][M+1]
+ *   gts_shap_interactions device SHAP interaction values phi[rows][G][M+1][M+1]
+ *
+ * Conventions shared by every call:
+ *   - All memory is owned by the caller.  The library allocates nothing on the
+ *     device, keeps no state between calls and never frees caller memory.
+ *   - Every call returns a gts_status; on failure gts_last_error() returns a
+ *     message for the calling thread (valid until that thread's next call).
+ *   - A split sends x to the left child iff x < threshold; a path element
+ *     holds the half-open range [lower, upper) (Section 3.1).
+ *   - Feature values must be finite.  A NaN makes every range test false
+ *     (the element-wise test of the paper's kernel listing), which is not the
+ *     tree's own routing; missing values are not supported.
+ *   - M = number of features, G = number of output groups (classes).
+ */
+#ifndef GTS_H
+#define GTS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gts_status {
+  GTS_OK = 0,
+  GTS_EINVAL = 1,    /* bad argument or malformed ensemble / layout */
+  GTS_EPATHLEN = 2,  /* a merged path is longer than the bin capacity (<= 64) */
+  GTS_EBUFSIZE = 3,  /* output capacity too small; required sizes were written */
+  GTS_ENOMEM = 4,    /* host allocation failed */
+  GTS_EDEVICE = 5    /* a HIP call or kernel launch failed */
+} gts_status;
+
+typedef enum gts_dtype { GTS_F32 = 0, GTS_F64 = 1 } gts_dtype;
+
+/* Bin-packing heuristics of Section 3.3 / Table 1. */
+typedef enum gts_pack_alg {
+  GTS_PACK_BFD = 0,  /* Best-Fit-Decreasing (the paper's choice, Section 4.1) */
+  GTS_PACK_FFD = 1,  /* First-Fit-Decreasing */
+  GTS_PACK_NF = 2,   /* Next-Fit, paths in their input order */
+  GTS_PACK_NONE = 3  /* one path per bin (the "none" baseline of Table 5) */
+} gts_pack_alg;
+
+/*
+ * A tree ensemble as flat node lists: per node the lists {v, a, b, t, r, d}
+ * of Section 2.1 (leaf value, left child, right child, threshold, cover,
+ * feature).  Tree k owns nodes [tree_node_offsets[k], tree_node_offsets[k+1]);
+ * child indices are local to the tree, the root is local index 0, and a leaf
+ * has left == right == -1.  feature/threshold are ignored on leaves, value on
+ * internal nodes.  cover must be finite and >= 0; a ratio with a zero-cover
+ * parent is taken as 0.  tree_group[k] in [0, G) is the output the tree adds
+ * to.  All pointers are host pointers.
+ */
+typedef struct gts_ensemble {
+  int32_t num_features;              /* M >= 1 */
+  int32_t num_groups;                /* G >= 1 */
+  int64_t num_trees;                 /* T >= 0 */
+  int64_t num_nodes;                 /* tree_node_offsets[T] */
+  const int64_t *tree_node_offsets;  /* [T+1], non-decreasing, starts at 0 */
+  const int32_t *tree_group;         /* [T] */
+  const int32_t *left;               /* [num_nodes] */
+  const int32_t *right;              /* [num_nodes] */
+  const int32_t *feature;            /* [num_nodes] */
+  const float *threshold;            /* [num_nodes] */
+  const double *cover;               /* [num_nodes] */
+  const double *value;               /* [num_nodes] */
+} gts_ensemble;
+
+/*
+ * One element of a unique path: the fields of the paper's PathElement
+ * (Listing 1) plus the output group of the path's tree.  The first element of
+ * every path is its root (feature_idx -1, range (-inf, +inf), zero_fraction 1);
+ * v is the path's leaf value on every element.  40 bytes, naturally aligned.
+ */
+typedef struct gts_path_element {
+  int64_t path_idx;       /* unique path index */
+  int32_t feature_idx;    /* split feature, -1 for the root element */
+  int32_t group;          /* output group of the path's tree */
+  float lower;            /* feature range [lower, upper) */
+  float upper;
+  double zero_fraction;   /* product of cover ratios along the path */
+  double v;               /* leaf value at the end of the path */
+} gts_path_element;
+
+/*
+ * Device-ready model produced by gts_model_layout.  The fields describe the
+ * byte blob the caller copies to the device; treat them as read-only.
+ */
+typedef struct gts_model {
+  uint32_t magic;
+  int32_t dtype;           /* gts_dtype of zero fractions, leaf values, phi */
+  int32_t num_features;    /* M */
+  int32_t num_groups;      /* G */
+  int32_t max_path_len;    /* longest path, root included */
+  int32_t reserved0;
+  int64_t num_elements;
+  int64_t num_paths;
+  int64_t num_bins;
+  int64_t bytes;           /* size of the blob */
+  int64_t off[16];         /* byte offsets of the blob's arrays */
+} gts_model;
+
+/*
+ * gts_extract_paths -- Sections 3.1 and 3.2 (extract paths, remove duplicate
+ * features).
+ *
+ * Walks every tree (trees in input order, leaves in depth-first preorder with
+ * the left child first) and emits one path per leaf: its root element, then
+ * one element per distinct split feature in ascending feature order.  A left
+ * turn at threshold t bounds the range above by t, a right turn below by t;
+ * repeated features intersect their ranges and multiply their zero fractions
+ * (child cover / parent cover) in root-to-leaf order.
+ *
+ * out       host array of `capacity` elements, or NULL to query sizes only.
+ * num_elements, num_paths  (out) totals; always written on GTS_OK and
+ *           GTS_EBUFSIZE.
+ * bias      (out, may be NULL) host double[G]: per group the sum over its
+ *           paths, in path order, of v times the product of the path's zero
+ *           fractions -- the expected model output f of the empty feature set
+ *           (the bias term phi_0 of Eq. 1).
+ * Errors: GTS_EINVAL for out-of-range children, a node reached twice (cycle
+ * or shared child), feature outside [0, M), group outside [0, G), negative or
+ * non-finite cover, NaN threshold; GTS_EBUFSIZE if capacity is too small.
+ */
+gts_status gts_extract_paths(const gts_ensemble *ens, gts_path_element *out,
+                             int64_t capacity, int64_t *num_elements,
+                             int64_t *num_paths, double *bias);
+
+/*
+ * gts_pack_paths -- Section 3.3 (bin packing for work allocation).
+ *
+ * Items are paths (contiguous runs starting at a root element, as produced by
+ * gts_extract_paths) of size = path length; bins hold `bin_capacity` lanes
+ * (<= 64, one lane per path element on a wave64).  Each output group is packed
+ * on its own, groups ascending, bins numbered in opening order.
+ *   BFD: items by non-increasing size (ties: lower path position first); each
+ *        goes to the feasible bin with the smallest residual (ties: lower bin).
+ *   FFD: same order; the lowest-numbered feasible bin.
+ *   NF:  input order; the current bin if it fits, else a new bin.
+ *   NONE: one path per bin, input order.
+ * A bin may be filled exactly to capacity.  Within a bin, paths are laid out
+ * in placement order.
+ *
+ * packed       host array [num_elements]: the elements regrouped bin by bin.
+ * bin_offsets  host array [offsets_capacity]; receives num_bins+1 element
+ *              offsets into `packed`.  May be NULL with offsets_capacity 0 to
+ *              query num_bins (packed is then not written).
+ * Errors: GTS_EPATHLEN if a path is longer than bin_capacity;
+ * GTS_EINVAL for capacity outside [1, 64], an unknown alg, or input that is
+ * not a sequence of rooted paths; GTS_EBUFSIZE when offsets_capacity <
+ * num_bins + 1 (num_bins is written).
+ */
+gts_status gts_pack_paths(const gts_path_element *elems, int64_t num_elements,
+                          int32_t bin_capacity, int32_t alg,
+                          gts_path_element *packed, int64_t *bin_offsets,
+                          int64_t offsets_capacity, int64_t *num_bins);
+
+/*
+ * gts_model_layout -- marshal packed paths into the blob the device kernels
+ * read (structure-of-arrays, every array 256-byte aligned).
+ *
+ * packed, bin_offsets, num_bins: the output of gts_pack_paths (bins must not
+ *           mix groups).  bias: host double[G] from gts_extract_paths.
+ * dtype     GTS_F32 or GTS_F64: precision of zero fractions, leaf values and
+ *           of the whole SHAP recurrence and accumulation.
+ * model     (out) descriptor; model->bytes is the blob size.
+ * host_blob host buffer of blob_capacity bytes, or NULL to size only.
+ * Errors: GTS_EINVAL for inconsistent input, GTS_EPATHLEN for a path longer
+ * than 64, GTS_EBUFSIZE if blob_capacity < model->bytes.
+ */
+gts_status gts_model_layout(const gts_path_element *packed, int64_t num_elements,
+                            const int64_t *bin_offsets, int64_t num_bins,
+                            int32_t num_features, int32_t num_groups,
+                            const double *bias, int32_t dtype, gts_model *model,
+                            void *host_blob, int64_t blob_capacity);
+
+/*
+ * gts_shap -- SHAP values, Eq. (2), by the per-path permutation-weight
+ * recurrence of Algorithm 1 (EXTEND over a path's elements, then UNWIND of
+ * each element and a sum; Section 3.4, Algorithms 2-3).
+ *
+ * model    host descriptor from gts_model_layout.
+ * d_model  device copy of the blob.
+ * d_X      device float[rows][ld_x], row-major, ld_x >= M.
+ * d_phi    device array [rows][G][M+1] of the model dtype.  Overwritten:
+ *          phi[r][g][i] for i < M is feature i's SHAP value for output g;
+ *          phi[r][g][M] is the bias.
+ * stream   hipStream_t (NULL = default stream).  The call only enqueues work
+ *          and returns; results are ready when the stream reaches them.
+ * rows == 0 is a no-op.  Errors: GTS_EINVAL for NULL pointers, a descriptor
+ * that is not from gts_model_layout, rows < 0, ld_x < M; GTS_EDEVICE if a
+ * launch fails.
+ */
+gts_status gts_shap(const gts_model *model, const void *d_model,
+                    const float *d_X, int64_t rows, int64_t ld_x, void *d_phi,
+                    void *stream);
+
+/*
+ * gts_shap_interactions -- SHAP interaction values, Eq. (3)-(6), computed per
+ * path by conditioning on each of its features in turn (Sections 2.2 and
+ * 3.5): only features on a path interact through it.
+ *
+ * d_phi    device array [rows][G][M+1][M+1] of the model dtype, overwritten:
+ *          [i][j] (i != j < M) the interaction of features i and j, [i][i]
+ *          from Eq. (6), [M][M] the bias, the rest of row and column M zero.
+ * Other arguments and errors as gts_shap.
+ */
+gts_status gts_shap_interactions(const gts_model *model, const void *d_model,
+                                 const float *d_X, int64_t rows, int64_t ld_x,
+                                 void *d_phi, void *stream);
+
+/* Message describing the calling thread's most recent failure ("" if none). */
+const char *gts_last_error(void);
+
+/* Library version string. */
+const char *gts_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GTS_H */

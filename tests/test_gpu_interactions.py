@@ -1,0 +1,87 @@
+"""gts_shap_interactions on the GPU against the fp64 CPU oracle
+(SHAP interaction values, Eq. 3-6).
+
+Small cases compare every element with brute-force enumeration and with the
+oracle's conditioning route (Section 2.2); the full-size workload (the
+covtype-shaped model, 1000 rows) compares sampled rows and checks, on every
+row, symmetry, row sums equal to gts_shap's values and the bias entry.
+"""
+import numpy as np
+import pytest
+
+from paper_2010_13972_amd import gts, synth
+from parity import assert_parity, sum_tolerance
+from test_gpu_shap import chain_tree, sample_rows, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    return torch
+
+
+def run(torch, ens, X, dtype, both=False):
+    model = gts.prepare(ens, dtype)
+    Xd = torch.from_numpy(np.ascontiguousarray(X, np.float32)).cuda()
+    inter = gts.shap_interactions(model, Xd)
+    phi = gts.shap(model, Xd) if both else None
+    torch.cuda.synchronize()
+    inter = inter.cpu().numpy().astype(np.float64)
+    return (inter, phi.cpu().numpy().astype(np.float64)) if both else inter
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_tiny_ensemble_vs_brute_force(torch, orc, dtype):
+    w = synth.workload("tiny", rows=64)
+    say("interactions tiny", dtype)
+    got = run(torch, w.ensemble, w.X, dtype)
+    assert_parity(got, orc.brute_interactions(w.ensemble, w.X), dtype, 2, "tiny vs Eq. 3-6")
+    assert_parity(got, orc.interactions(w.ensemble, w.X), dtype, 2, "tiny vs conditioning")
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_random_edge_case_ensembles(torch, orc, seed, dtype):
+    w = synth.random_workload(seed, num_trees=10, max_depth=7, M=6, num_groups=2, n_bg=40,
+                              rows=21 + 17 * seed)
+    say("interactions random", seed, dtype)
+    got = run(torch, w.ensemble, w.X, dtype)
+    assert_parity(got, orc.interactions(w.ensemble, w.X), dtype, 2, f"random{seed}")
+
+
+@pytest.mark.parametrize("depth", [2, 8, 9, 13, 20])
+def test_long_paths(torch, orc, depth):
+    """Around the unrolled-variant boundary (8 features) and beyond."""
+    rng = np.random.default_rng(100 + depth)
+    M = 24
+    ens = synth.ensemble_from_lists([chain_tree(depth, M, rng), chain_tree(depth // 2 + 1, M, rng)],
+                                    M=M)
+    X = rng.uniform(0.4, 0.8, size=(40, M)).astype(np.float32)
+    say("interactions long", depth)
+    for dtype in ("f64", "f32"):
+        got = run(torch, ens, X, dtype)
+        assert_parity(got, orc.interactions(ens, X), dtype, 2, f"depth={depth}")
+
+
+def test_full_size_workload(torch, orc):
+    w = synth.workload("interactions")
+    M = w.ensemble.num_features
+    say("interactions full size", w.X.shape)
+    inter, phi = run(torch, w.ensemble, w.X, "f32", both=True)
+    rows = sample_rows(w.X.shape[0], k=8)
+    want = orc.interactions(w.ensemble, w.X[rows])
+    assert_parity(inter[rows], want, "f32", 2, "covtype-shaped model, sampled rows")
+    # every row: symmetric, rows sum to the SHAP values, bias at [M, M]
+    scale = np.abs(inter)
+    sym_err = np.abs(inter - np.swapaxes(inter, -1, -2))
+    sym_tol = 1e-3 * scale + 1e-5 * scale.sum(axis=(-2, -1), keepdims=True)
+    assert np.all(sym_err <= 2 * sym_tol)
+    row_sum = inter[..., :M, :].sum(-1)
+    bound = sum_tolerance(scale[..., :M, :], "f32") + 1e-3 * np.abs(phi[..., :M]) \
+        + 1e-5 * np.abs(phi).sum(-1, keepdims=True)
+    assert np.all(np.abs(row_sum - phi[..., :M]) <= bound)
+    assert np.allclose(inter[..., M, M], phi[..., M], rtol=1e-6, atol=1e-7)
+    assert np.all(inter[..., M, :M] == 0) and np.all(inter[..., :M, M] == 0)

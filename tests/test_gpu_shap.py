@@ -1,0 +1,158 @@
+"""gts_shap on the GPU against the fp64 CPU oracle (SHAP values, Eq. 2).
+
+Small cases compare every output element; the full-size workloads run in the
+benchmark's launch configuration and compare sampled rows with the oracle's
+Algorithm 1 plus, for every row, local accuracy (Eq. 1: the explanation sums
+to the model output).
+"""
+import numpy as np
+import pytest
+
+from paper_2010_13972_amd import gts, synth
+from parity import assert_parity, sum_tolerance
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    return torch
+
+
+def run_shap(torch, ens, X, dtype, ld_pad=0):
+    model = gts.prepare(ens, dtype)
+    Xd = torch.zeros((X.shape[0], X.shape[1] + ld_pad), dtype=torch.float32, device="cuda")
+    Xd[:, :X.shape[1]] = torch.from_numpy(np.ascontiguousarray(X, np.float32))
+    phi = gts.shap(model, Xd)
+    torch.cuda.synchronize()
+    return phi.cpu().numpy().astype(np.float64)
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+# --------------------------------------------------------------------------
+# small inputs: every element
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_tiny_ensemble_all_rows_vs_brute_force(torch, orc, dtype):
+    w = synth.workload("tiny")
+    say("tiny", dtype, w.X.shape)
+    got = run_shap(torch, w.ensemble, w.X, dtype)
+    want = orc.brute_shap(w.ensemble, w.X)
+    assert_parity(got, want, dtype, what="tiny vs Eq. 2")
+    assert_parity(got, orc.treeshap(w.ensemble, w.X), dtype, what="tiny vs Algorithm 1")
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_random_edge_case_ensembles(torch, orc, seed, dtype):
+    """Repeated features, ties x == t, zero-cover nodes, three output groups,
+    ragged row counts."""
+    w = synth.random_workload(seed, num_trees=12, max_depth=7, M=6, num_groups=3,
+                              n_bg=40, rows=37 + 29 * seed)
+    say("random", seed, dtype, w.X.shape)
+    got = run_shap(torch, w.ensemble, w.X, dtype)
+    assert_parity(got, orc.treeshap(w.ensemble, w.X), dtype, what=f"random{seed}")
+
+
+@pytest.mark.parametrize("rows", [1, 2, 63, 64, 65, 130])
+def test_ragged_row_counts_and_strided_X(torch, orc, rows):
+    w = synth.workload("tiny")
+    X = np.concatenate([w.X] * 2)[:rows]
+    say("ragged", rows)
+    got = run_shap(torch, w.ensemble, X, "f64", ld_pad=3)
+    assert_parity(got, orc.treeshap(w.ensemble, X), "f64", what=f"rows={rows}")
+
+
+def test_zero_rows_is_a_no_op(torch):
+    w = synth.workload("tiny")
+    model = gts.prepare(w.ensemble, "f32")
+    X = torch.zeros((0, 8), dtype=torch.float32, device="cuda")
+    out = gts.shap(model, X)
+    torch.cuda.synchronize()
+    assert tuple(out.shape) == (0, 1, 9)
+
+
+def chain_tree(depth, M, rng):
+    """A spine of `depth` splits on distinct features (the left child
+    continues the spine), so the deepest path has `depth` features."""
+    res = []
+    cover = 1000.0
+    for d in range(depth):
+        base = len(res)
+        res.append((base + 2, base + 1, d % M, np.float32(0.5 + 0.01 * d), cover, 0.0))
+        cl = max(1.0, float(int(cover * 0.8)))
+        res.append((-1, -1, -1, 0.0, cover - cl, float(rng.normal())))
+        cover = cl
+    res.append((-1, -1, -1, 0.0, cover, float(rng.normal())))
+    return res
+
+
+@pytest.mark.parametrize("depth", [1, 15, 16, 17, 31, 63])
+def test_long_paths(torch, orc, depth):
+    """Path lengths around the unrolled-variant boundary and the wave64
+    maximum (63 features + root = 64 elements)."""
+    rng = np.random.default_rng(depth)
+    M = 63
+    trees = [chain_tree(depth, M, rng), chain_tree(max(1, depth // 2), M, rng)]
+    ens = synth.ensemble_from_lists(trees, M=M)
+    X = rng.uniform(0.4, 1.2, size=(70, M)).astype(np.float32)
+    say("long paths", depth)
+    for dtype in ("f64", "f32"):
+        got = run_shap(torch, ens, X, dtype)
+        assert_parity(got, orc.treeshap(ens, X), dtype, what=f"depth={depth}")
+
+
+def test_special_models(torch, orc):
+    """Single-leaf trees (bias only), stumps, and a path whose feature is
+    repeated at every level (merged into one element)."""
+    leaf = [(-1, -1, -1, 0.0, 10.0, 2.5)]
+    stump = [(1, 2, 1, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 3.0, -1.0), (-1, -1, -1, 0, 7.0, 4.0)]
+    dup = [(1, 2, 0, 0.8, 16, 0), (3, 4, 0, 0.6, 12, 0), (-1, -1, -1, 0, 4, 1.0),
+           (5, 6, 0, 0.3, 7, 0), (-1, -1, -1, 0, 5, 2.0), (-1, -1, -1, 0, 3, 3.0),
+           (-1, -1, -1, 0, 4, 4.0)]
+    ens = synth.ensemble_from_lists([leaf, stump, dup, leaf], M=3)
+    X = np.random.default_rng(0).uniform(0, 1, size=(50, 3)).astype(np.float32)
+    X[:5, 0] = [0.3, 0.6, 0.8, 0.0, 1.0]  # exact ties with thresholds
+    for dtype in ("f64", "f32"):
+        got = run_shap(torch, ens, X, dtype)
+        want = orc.treeshap(ens, X)
+        assert_parity(got, want, dtype, what="special models")
+        assert np.all(got[:, 0, 2] == 0.0)  # feature 2 never used
+
+
+# --------------------------------------------------------------------------
+# full-size workloads: sampled rows against Algorithm 1, all rows against Eq. 1
+# --------------------------------------------------------------------------
+
+def sample_rows(n, k=24, seed=0):
+    rng = np.random.default_rng(seed)
+    rows = set(range(min(4, n))) | set(range(max(0, n - 4), n))
+    rows |= set(rng.choice(n, size=min(k, n), replace=False).tolist())
+    return np.array(sorted(rows))
+
+
+FULL = [("covtype_med", "f32"), ("deep", "f32"), ("deep", "f64"), ("wide", "f32"),
+        ("tiny", "f64")]
+
+
+@pytest.mark.parametrize("name,dtype", FULL, ids=[f"{n}-{d}" for n, d in FULL])
+def test_full_size_workloads(torch, orc, name, dtype):
+    w = synth.workload(name)
+    say("full size", name, dtype, w.X.shape, "paths", int((w.ensemble.left < 0).sum()))
+    got = run_shap(torch, w.ensemble, w.X, dtype)
+    rows = sample_rows(w.X.shape[0])
+    want = orc.treeshap(w.ensemble, w.X[rows])
+    assert_parity(got[rows], want, dtype, what=f"{name} sampled rows")
+    # Eq. 1 on every row: sum_i phi_i + phi_0 = f(x)
+    f = orc.predict(w.ensemble, w.X)
+    err = np.abs(got.sum(-1) - f)
+    # bound: the element-wise tolerance summed over the block, with the
+    # oracle's block magnitude estimated by the kernel's own output
+    bound = sum_tolerance(np.abs(got), dtype)
+    assert np.all(err <= bound), float((err / bound).max())

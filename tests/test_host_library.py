@@ -1,0 +1,286 @@
+"""libgts host calls against the oracle, on the CPU.
+
+Extraction (Sections 3.1-3.2), the bias and Best-Fit-Decreasing packing
+(Section 3.3) must match the oracle's independent implementations bit for
+bit.  Also: every symbol of include/gts.h is exported, and malformed input
+is rejected with the documented status.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2010_13972_amd import gts, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "gts.h")).read()
+    names = set(re.findall(r"^\S.*?\b(gts_\w+)\(", header, flags=re.M))
+    assert {"gts_extract_paths", "gts_pack_paths", "gts_model_layout", "gts_shap",
+            "gts_shap_interactions", "gts_last_error", "gts_version"} <= names
+    L = gts.lib()
+    for n in sorted(names):
+        assert hasattr(L, n), f"libgts.so does not export {n}"
+    assert "gfx950" in gts.version()
+
+
+def _as_oracle_fields(el):
+    return (el["path_idx"], el["feature_idx"], el["group"], el["lower"], el["upper"],
+            el["zero_fraction"], el["v"])
+
+
+def _assert_bitwise(a, b):
+    a = np.asarray(a)
+    b = np.asarray(b)
+    assert a.shape == b.shape
+    assert a.tobytes() == b.tobytes()
+
+
+EXTRACT_CASES = ["tiny", "covtype_med", "wide", "random0", "random1", "random2", "random3"]
+
+
+def _workload(name):
+    if name.startswith("random"):
+        s = int(name[6:])
+        return synth.random_workload(s, num_trees=6, max_depth=7, M=5, num_groups=3,
+                                     n_bg=40, rows=4)
+    return synth.workload(name)
+
+
+@pytest.mark.parametrize("name", EXTRACT_CASES)
+def test_extract_paths_bitwise_equal_to_oracle(orc, name):
+    w = _workload(name)
+    el, npaths, bias = gts.extract_paths(w.ensemble)
+    oel, onpaths, obias = orc.extract_paths(w.ensemble)
+    assert npaths == onpaths
+    for a, b in zip(_as_oracle_fields(el), _as_oracle_fields(oel)):
+        _assert_bitwise(a, b)
+    _assert_bitwise(bias, obias)
+
+
+@pytest.mark.slow
+def test_extract_and_pack_deep_ensemble(orc):
+    w = synth.workload("deep")
+    el, npaths, bias = gts.extract_paths(w.ensemble)
+    oel, onpaths, obias = orc.extract_paths(w.ensemble)
+    for a, b in zip(_as_oracle_fields(el), _as_oracle_fields(oel)):
+        _assert_bitwise(a, b)
+    _assert_bitwise(bias, obias)
+    _check_pack_against_oracle(orc, el, 64)
+
+
+def _paths_of(el):
+    roots = np.flatnonzero(el["feature_idx"] == -1)
+    sizes = np.diff(np.append(roots, len(el)))
+    return roots, sizes, el["group"][roots]
+
+
+def _check_pack_against_oracle(orc, el, cap):
+    packed, offs = gts.pack_paths(el, cap, "bfd")
+    roots, sizes, groups = _paths_of(el)
+    bin_of, lane_of, k = orc.pack_bfd(sizes, groups, cap)
+    assert len(offs) == k + 1
+    # rebuild the oracle's packed element order and compare raw bytes
+    order = np.lexsort((lane_of, bin_of))
+    want_idx = np.concatenate([np.arange(roots[p], roots[p] + sizes[p]) for p in order])
+    _assert_bitwise(packed, el[want_idx])
+    fill = np.bincount(bin_of, weights=sizes, minlength=k).astype(np.int64)
+    _assert_bitwise(offs, np.concatenate([[0], np.cumsum(fill)]))
+
+
+@pytest.mark.parametrize("name", EXTRACT_CASES)
+@pytest.mark.parametrize("cap", [64, 32, 17])
+def test_pack_paths_bitwise_equal_to_oracle_bfd(orc, name, cap):
+    w = _workload(name)
+    el, _, _ = gts.extract_paths(w.ensemble)
+    if int(np.max(_paths_of(el)[1])) > cap:
+        with pytest.raises(gts.GtsError) as e:
+            gts.pack_paths(el, cap, "bfd")
+        assert e.value.status == gts.GTS_EPATHLEN
+        return
+    _check_pack_against_oracle(orc, el, cap)
+
+
+def test_pack_golden_instances(orc):
+    """The hand-worked BFD instances, run through the library."""
+    import json
+    fx = json.load(open(os.path.join(ROOT, "tests", "golden", "bin_packing.json")))
+    for case in fx["cases"]:
+        el = _synthetic_elements(case["sizes"], case["groups"])
+        packed, offs = gts.pack_paths(el, case["capacity"], "bfd")
+        assert len(offs) - 1 == case["num_bins"]
+        roots = np.flatnonzero(el["feature_idx"] == -1)
+        for p, (b, lane) in enumerate(zip(case["bin_of"], case["lane_of"])):
+            pos = offs[b] + lane
+            assert packed["path_idx"][pos] == p and packed["feature_idx"][pos] == -1
+            assert roots[p] >= 0
+
+
+def _synthetic_elements(sizes, groups):
+    rows = []
+    for p, (s, g) in enumerate(zip(sizes, groups)):
+        rows.append((p, -1, g, -np.inf, np.inf, 1.0, 0.5))
+        for k in range(s - 1):
+            rows.append((p, k, g, 0.0, 1.0, 0.5, 0.5))
+    return np.array(rows, dtype=gts.PATH_ELEMENT)
+
+
+@pytest.mark.parametrize("alg", ["bfd", "ffd", "nf", "none"])
+def test_pack_invariants_all_algorithms(alg):
+    rng = np.random.default_rng(5)
+    sizes = rng.integers(1, 65, size=500)
+    groups = np.sort(rng.integers(0, 3, size=500))
+    el = _synthetic_elements(sizes, groups)
+    packed, offs = gts.pack_paths(el, 64, alg)
+    assert offs[0] == 0 and offs[-1] == len(el)
+    fills = np.diff(offs)
+    assert np.all((fills >= 1) & (fills <= 64))
+    assert sorted(packed["path_idx"].tolist()) == sorted(el["path_idx"].tolist())
+    for b in range(len(offs) - 1):
+        seg = packed[offs[b]:offs[b + 1]]
+        assert seg["feature_idx"][0] == -1
+        assert len(set(seg["group"].tolist())) == 1
+    k = len(offs) - 1
+    assert k >= int(np.ceil(sizes.sum() / 64))
+    if alg == "none":
+        assert k == len(sizes)
+
+
+def test_model_layout_roundtrip():
+    w = synth.workload("wide")
+    el, npaths, bias = gts.extract_paths(w.ensemble)
+    packed, offs = gts.pack_paths(el, 64, "bfd")
+    for dtype, ft in (("f32", np.float32), ("f64", np.float64)):
+        desc, blob = gts.model_layout(packed, offs, 784, 10, bias, dtype)
+        assert desc.num_paths == npaths and desc.num_bins == len(offs) - 1
+        assert desc.bytes == len(blob) and all(o % 256 == 0 for o in desc.off[:11])
+        feat = np.frombuffer(blob, np.int32, len(packed), desc.off[0])
+        assert np.array_equal(feat, packed["feature_idx"])
+        z = np.frombuffer(blob, ft, len(packed), desc.off[3])
+        assert np.array_equal(z, packed["zero_fraction"].astype(ft))
+        first = np.frombuffer(blob, np.int32, npaths, desc.off[4])
+        plen = np.frombuffer(blob, np.int32, npaths, desc.off[5])
+        gp = np.frombuffer(blob, np.int32, 11, desc.off[7])
+        assert gp[0] == 0 and gp[-1] == npaths
+        for g in range(10):
+            seg = plen[gp[g]:gp[g + 1]]
+            assert np.all(np.diff(seg) <= 0)             # non-increasing length
+            assert np.all(packed["group"][first[gp[g]:gp[g + 1]]] == g)
+        assert sorted(first.tolist()) == np.flatnonzero(packed["feature_idx"] == -1).tolist()
+
+
+# ----------------------------------------------------------------------------
+# error paths (forced from the host)
+# ----------------------------------------------------------------------------
+
+def _bad(ens_mod, **kw):
+    import copy
+    e = copy.deepcopy(ens_mod)
+    for k, v in kw.items():
+        setattr(e, k, v)
+    return e
+
+
+def test_extract_rejects_malformed_ensembles():
+    base = synth.workload("tiny").ensemble
+    left = base.left.copy()
+    left[0] = 99                                        # child out of range
+    cases = [_bad(base, left=left)]
+    left2 = base.left.copy()
+    left2[1] = 0                                        # cycle back to the root
+    cases.append(_bad(base, left=left2))
+    feat = base.feature.copy()
+    feat[0] = 8                                         # feature >= M
+    cases.append(_bad(base, feature=feat))
+    grp = base.tree_group.copy()
+    grp[3] = 1                                          # group >= G
+    cases.append(_bad(base, tree_group=grp))
+    cov = base.cover.copy()
+    cov[2] = -1.0                                       # negative cover
+    cases.append(_bad(base, cover=cov))
+    thr = base.threshold.copy()
+    thr[0] = np.nan
+    cases.append(_bad(base, threshold=thr))
+    for e in cases:
+        with pytest.raises(gts.GtsError) as exc:
+            gts.extract_paths(e)
+        assert exc.value.status == gts.GTS_EINVAL
+
+
+def test_extract_capacity_and_null_arguments():
+    w = synth.workload("tiny")
+    s, keep = gts._ensemble_struct(w.ensemble)
+    n = ctypes.c_int64(0)
+    npaths = ctypes.c_int64(0)
+    L = gts.lib()
+    assert L.gts_extract_paths(ctypes.byref(s), None, 0, ctypes.byref(n), ctypes.byref(npaths),
+                               None) == gts.GTS_OK
+    small = np.zeros(5, gts.PATH_ELEMENT)
+    st = L.gts_extract_paths(ctypes.byref(s), small.ctypes.data_as(ctypes.c_void_p), 5,
+                             ctypes.byref(n), ctypes.byref(npaths), None)
+    assert st == gts.GTS_EBUFSIZE and n.value == 284 and npaths.value == 80
+    assert L.gts_extract_paths(None, None, 0, ctypes.byref(n), ctypes.byref(npaths),
+                               None) == gts.GTS_EINVAL
+    assert L.gts_extract_paths(ctypes.byref(s), None, 0, None, None, None) == gts.GTS_EINVAL
+
+
+def test_pack_errors():
+    el = _synthetic_elements([3, 65 - 1, 2], [0, 0, 0])
+    with pytest.raises(gts.GtsError) as e:
+        gts.pack_paths(el, 32, "bfd")
+    assert e.value.status == gts.GTS_EPATHLEN
+    with pytest.raises(gts.GtsError) as e:
+        gts.pack_paths(el, 65, "bfd")
+    assert e.value.status == gts.GTS_EINVAL
+    bad = el.copy()
+    bad["feature_idx"][0] = 2                           # does not start at a root
+    with pytest.raises(gts.GtsError) as e:
+        gts.pack_paths(bad, 64, "bfd")
+    assert e.value.status == gts.GTS_EINVAL
+    L = gts.lib()
+    k = ctypes.c_int64(0)
+    offs = np.zeros(1, np.int64)
+    packed = np.zeros(len(el), gts.PATH_ELEMENT)
+    st = L.gts_pack_paths(el.ctypes.data_as(ctypes.c_void_p), len(el), 64, 0,
+                          packed.ctypes.data_as(ctypes.c_void_p),
+                          offs.ctypes.data_as(ctypes.c_void_p), 1, ctypes.byref(k))
+    assert st == gts.GTS_EBUFSIZE and k.value == 2
+    assert L.gts_pack_paths(el.ctypes.data_as(ctypes.c_void_p), len(el), 64, 9, None, None, 0,
+                            ctypes.byref(k)) == gts.GTS_EINVAL
+
+
+def test_layout_errors():
+    w = synth.workload("tiny")
+    el, _, bias = gts.extract_paths(w.ensemble)
+    packed, offs = gts.pack_paths(el, 64, "bfd")
+    with pytest.raises(gts.GtsError):
+        gts.model_layout(packed, offs, 4, 1, bias, "f32")       # feature >= M
+    bad = offs.copy()
+    bad[1] += 1                                                 # bin not on a root
+    with pytest.raises(gts.GtsError):
+        gts.model_layout(packed, bad, 8, 1, bias, "f32")
+    with pytest.raises(KeyError):
+        gts.model_layout(packed, offs, 8, 1, bias, "f16")
+
+
+def test_device_calls_reject_bad_arguments_without_touching_the_gpu():
+    """Argument checks happen before any HIP call."""
+    w = synth.workload("tiny")
+    el, _, bias = gts.extract_paths(w.ensemble)
+    packed, offs = gts.pack_paths(el, 64, "bfd")
+    desc, blob = gts.model_layout(packed, offs, 8, 1, bias, "f64")
+    L = gts.lib()
+    vp = ctypes.c_void_p
+    for fn in (L.gts_shap, L.gts_shap_interactions):
+        assert fn(None, vp(1), vp(1), 4, 8, vp(1), None) == gts.GTS_EINVAL
+        assert fn(ctypes.byref(desc), vp(1), vp(1), -1, 8, vp(1), None) == gts.GTS_EINVAL
+        assert fn(ctypes.byref(desc), vp(1), vp(1), 4, 7, vp(1), None) == gts.GTS_EINVAL
+        assert fn(ctypes.byref(desc), None, vp(1), 4, 8, vp(1), None) == gts.GTS_EINVAL
+        assert fn(ctypes.byref(desc), vp(1), vp(1), 0, 8, vp(1), None) == gts.GTS_OK  # no-op
+        forged = gts.ModelDesc.from_buffer_copy(desc)
+        forged.magic = 0
+        assert fn(ctypes.byref(forged), vp(1), vp(1), 4, 8, vp(1), None) == gts.GTS_EINVAL
