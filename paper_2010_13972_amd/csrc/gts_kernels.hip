@@ -175,39 +175,44 @@ __device__ __forceinline__ void shap_round(const DevModel<T>& d, int p, bool act
   }
 }
 
-// Paths longer than the unrolled variants: same arithmetic, runtime loops.
+// Paths longer than the unrolled variants: same arithmetic with runtime loops,
+// always in fp64.  Dividing the weight polynomial from its top coefficient
+// down cancels more and more as paths grow; in fp32 the error passes the
+// parity bound beyond about 20 features, in fp64 it stays far inside it for
+// the longest path a wave64 holds (63 features).  FP64 FMAs run at the same
+// rate as unpacked FP32 ones on gfx950.
 template <typename T>
 __device__ void shap_round_dyn(const DevModel<T>& d, int p, bool active,
                                const float* __restrict__ xrow, T* __restrict__ prow) {
   const int first = d.path_first[p] + 1;
   const int q = d.path_len[p] - 1;
-  const T v = d.path_v[p];
-  T E[kMaxPathLen];
-  T z[kMaxPathLen];
-  T D[kMaxPathLen];
+  const double v = (double)d.path_v[p];
+  double E[kMaxPathLen];
+  double z[kMaxPathLen];
+  double D[kMaxPathLen];
   uint64_t obits = 0;
-  E[0] = T(1);
+  E[0] = 1.0;
   for (int l = 1; l <= q; ++l) {
     const int e = first + l - 1;
     const float x = xrow[d.feat[e]];
     const bool ol = (d.lower[e] <= x) && (x < d.upper[e]);
-    const T zl = d.zero[e];
+    const double zl = (double)d.zero[e];
     z[l - 1] = zl;
     obits |= (uint64_t)ol << (l - 1);
-    E[l] = ol ? E[l - 1] : T(0);
-    for (int k = l - 1; k >= 1; --k) E[k] = fma(zl, E[k], ol ? E[k - 1] : T(0));
+    E[l] = ol ? E[l - 1] : 0.0;
+    for (int k = l - 1; k >= 1; --k) E[k] = fma(zl, E[k], ol ? E[k - 1] : 0.0);
     E[0] = zl * E[0];
   }
-  T t_all = T(0);
-  for (int k = 0; k < q; ++k) t_all = fma(T(shapley_weight(q, k)), E[k], t_all);
+  double t_all = 0.0;
+  for (int k = 0; k < q; ++k) t_all = fma(shapley_weight(q, k), E[k], t_all);
   for (int i = 0; i < q; ++i) {
     D[q - 1] = E[q];
     for (int k = q - 1; k >= 1; --k) D[k - 1] = fma(-z[i], D[k], E[k]);
-    T s = T(0);
-    for (int k = 0; k < q; ++k) s = fma(T(shapley_weight(q, k)), D[k], s);
+    double s = 0.0;
+    for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
     const bool oi = (obits >> i) & 1u;
-    const T phi = oi ? v * (T(1) - z[i]) * s : -v * t_all;
-    if (active) atomicAdd(&prow[d.feat[first + i]], phi);
+    const double phi = oi ? v * (1.0 - z[i]) * s : -v * t_all;
+    if (active) atomicAdd(&prow[d.feat[first + i]], (T)phi);
   }
 }
 
@@ -293,69 +298,70 @@ __device__ __forceinline__ void inter_round(const DevModel<T>& d, int p, bool ac
     if (active && f[c] >= 0) atomicAdd(&prow[f[c] * stride + f[c]], diag[c]);
 }
 
+// Long paths: runtime loops, always in fp64 (see shap_round_dyn).
 template <typename T>
 __device__ void inter_round_dyn(const DevModel<T>& d, int p, bool active,
                                 const float* __restrict__ xrow, T* __restrict__ prow, int stride) {
   const int first = d.path_first[p] + 1;
   const int q = d.path_len[p] - 1;
-  const T v = d.path_v[p];
-  T E[kMaxPathLen];
-  T z[kMaxPathLen];
-  T D[kMaxPathLen];
-  T DD[kMaxPathLen];
-  T tp[kMaxPathLen];
-  T diag[kMaxPathLen];
+  const double v = (double)d.path_v[p];
+  double E[kMaxPathLen];
+  double z[kMaxPathLen];
+  double D[kMaxPathLen];
+  double DD[kMaxPathLen];
+  double tp[kMaxPathLen];
+  double diag[kMaxPathLen];
   uint64_t obits = 0;
-  E[0] = T(1);
+  E[0] = 1.0;
   for (int l = 1; l <= q; ++l) {
     const int e = first + l - 1;
     const float x = xrow[d.feat[e]];
     const bool ol = (d.lower[e] <= x) && (x < d.upper[e]);
-    const T zl = d.zero[e];
+    const double zl = (double)d.zero[e];
     z[l - 1] = zl;
     obits |= (uint64_t)ol << (l - 1);
-    E[l] = ol ? E[l - 1] : T(0);
-    for (int k = l - 1; k >= 1; --k) E[k] = fma(zl, E[k], ol ? E[k - 1] : T(0));
+    E[l] = ol ? E[l - 1] : 0.0;
+    for (int k = l - 1; k >= 1; --k) E[k] = fma(zl, E[k], ol ? E[k - 1] : 0.0);
     E[0] = zl * E[0];
   }
-  T t_all = T(0), t_pair = T(0);
-  for (int k = 0; k < q; ++k) t_all = fma(T(shapley_weight(q, k)), E[k], t_all);
-  for (int k = 0; k < q - 1; ++k) t_pair = fma(T(shapley_weight(q - 1, k)), E[k], t_pair);
-  const T half_v = T(0.5) * v;
+  double t_all = 0.0, t_pair = 0.0;
+  for (int k = 0; k < q; ++k) t_all = fma(shapley_weight(q, k), E[k], t_all);
+  for (int k = 0; k < q - 1; ++k) t_pair = fma(shapley_weight(q - 1, k), E[k], t_pair);
+  const double half_v = 0.5 * v;
   for (int c = 0; c < q; ++c) {
     D[q - 1] = E[q];
     for (int k = q - 1; k >= 1; --k) D[k - 1] = fma(-z[c], D[k], E[k]);
-    T s = T(0), acc = T(0);
-    for (int k = 0; k < q; ++k) s = fma(T(shapley_weight(q, k)), D[k], s);
-    for (int k = 0; k < q - 1; ++k) acc = fma(T(shapley_weight(q - 1, k)), D[k], acc);
+    double s = 0.0, acc = 0.0;
+    for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
+    for (int k = 0; k < q - 1; ++k) acc = fma(shapley_weight(q - 1, k), D[k], acc);
     const bool oc = (obits >> c) & 1u;
-    diag[c] = oc ? v * (T(1) - z[c]) * s : -v * t_all;
+    diag[c] = oc ? v * (1.0 - z[c]) * s : -v * t_all;
     tp[c] = acc;
     const int fc = d.feat[first + c];
     for (int i = 0; i < c; ++i) {
       DD[q - 2] = D[q - 1];
       for (int k = q - 2; k >= 1; --k) DD[k - 1] = fma(-z[i], DD[k], D[k]);
-      T s11 = T(0);
-      for (int k = 0; k < q - 1; ++k) s11 = fma(T(shapley_weight(q - 1, k)), DD[k], s11);
+      double s11 = 0.0;
+      for (int k = 0; k < q - 1; ++k) s11 = fma(shapley_weight(q - 1, k), DD[k], s11);
       const bool oi = (obits >> i) & 1u;
-      T delta;
-      if (oi && oc) delta = half_v * (T(1) - z[i]) * (T(1) - z[c]) * s11;
-      else if (oi) delta = -half_v * (T(1) - z[i]) * tp[i];
-      else if (oc) delta = -half_v * (T(1) - z[c]) * tp[c];
+      double delta;
+      if (oi && oc) delta = half_v * (1.0 - z[i]) * (1.0 - z[c]) * s11;
+      else if (oi) delta = -half_v * (1.0 - z[i]) * tp[i];
+      else if (oc) delta = -half_v * (1.0 - z[c]) * tp[c];
       else delta = half_v * t_pair;
       diag[c] -= delta;
       diag[i] -= delta;
       const int fi = d.feat[first + i];
       if (active) {
-        atomicAdd(&prow[fi * stride + fc], delta);
-        atomicAdd(&prow[fc * stride + fi], delta);
+        atomicAdd(&prow[fi * stride + fc], (T)delta);
+        atomicAdd(&prow[fc * stride + fi], (T)delta);
       }
     }
   }
   for (int c = 0; c < q; ++c)
     if (active) {
       const int fc = d.feat[first + c];
-      atomicAdd(&prow[fc * stride + fc], diag[c]);
+      atomicAdd(&prow[fc * stride + fc], (T)diag[c]);
     }
 }
 
