@@ -475,10 +475,6 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
     sizes[kLower] = 4 * num_elements;
     sizes[kUpper] = 4 * num_elements;
     sizes[kZero] = (int64_t)ts * num_elements;
-    sizes[kPathFirst] = 4 * P;
-    sizes[kPathLen] = 4 * P;
-    sizes[kPathV] = (int64_t)ts * P;
-    sizes[kGroupPaths] = 4 * (G + 1);
     sizes[kBinStart] = 4 * (num_bins + 1);
     sizes[kGroupBins] = 4 * (G + 1);
     sizes[kBias] = (int64_t)ts * G;
@@ -515,43 +511,23 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
       lower[i] = packed[i].lower;
       upper[i] = packed[i].upper;
     }
-    // row-lane order: by group, then by non-increasing length, then position
-    std::vector<int64_t> order((size_t)P);
-    for (int64_t i = 0; i < P; ++i) order[(size_t)i] = i;
-    std::stable_sort(order.begin(), order.end(), [&](int64_t a, int64_t b) {
-      const PathRef &x = paths[(size_t)a], &y = paths[(size_t)b];
-      if (x.group != y.group) return x.group < y.group;
-      return x.size > y.size;
-    });
-    int32_t* pfirst = reinterpret_cast<int32_t*>(blob + m.off[kPathFirst]);
-    int32_t* plen = reinterpret_cast<int32_t*>(blob + m.off[kPathLen]);
-    int32_t* gpaths = reinterpret_cast<int32_t*>(blob + m.off[kGroupPaths]);
     int32_t* bstart = reinterpret_cast<int32_t*>(blob + m.off[kBinStart]);
     int32_t* gbins = reinterpret_cast<int32_t*>(blob + m.off[kGroupBins]);
-    for (int64_t k = 0; k < P; ++k) {
-      pfirst[k] = (int32_t)paths[(size_t)order[(size_t)k]].first;
-      plen[k] = paths[(size_t)order[(size_t)k]].size;
-    }
-    for (int64_t g = 0; g <= G; ++g) gpaths[g] = 0;
-    for (int64_t k = 0; k < P; ++k) gpaths[paths[(size_t)k].group + 1] += 1;
-    for (int64_t g = 0; g < G; ++g) gpaths[g + 1] += gpaths[g];
     for (int64_t b = 0; b <= num_bins; ++b) bstart[b] = (int32_t)bin_offsets[b];
     for (int64_t g = 0; g <= G; ++g) gbins[g] = 0;
     for (int64_t b = 0; b < num_bins; ++b) gbins[bin_group[(size_t)b] + 1] += 1;
     for (int64_t g = 0; g < G; ++g) gbins[g + 1] += gbins[g];
     if (dtype == GTS_F64) {
       double* z = reinterpret_cast<double*>(blob + m.off[kZero]);
-      double* v = reinterpret_cast<double*>(blob + m.off[kPathV]);
       double* bb = reinterpret_cast<double*>(blob + m.off[kBias]);
-      for (int64_t i = 0; i < num_elements; ++i) z[i] = packed[i].zero_fraction;
-      for (int64_t k = 0; k < P; ++k) v[k] = packed[paths[(size_t)order[(size_t)k]].first].v;
+      for (int64_t i = 0; i < num_elements; ++i)
+        z[i] = packed[i].feature_idx == -1 ? packed[i].v : packed[i].zero_fraction;
       for (int64_t g = 0; g < G; ++g) bb[g] = bias[g];
     } else {
       float* z = reinterpret_cast<float*>(blob + m.off[kZero]);
-      float* v = reinterpret_cast<float*>(blob + m.off[kPathV]);
       float* bb = reinterpret_cast<float*>(blob + m.off[kBias]);
-      for (int64_t i = 0; i < num_elements; ++i) z[i] = (float)packed[i].zero_fraction;
-      for (int64_t k = 0; k < P; ++k) v[k] = (float)packed[paths[(size_t)order[(size_t)k]].first].v;
+      for (int64_t i = 0; i < num_elements; ++i)
+        z[i] = (float)(packed[i].feature_idx == -1 ? packed[i].v : packed[i].zero_fraction);
       for (int64_t g = 0; g < G; ++g) bb[g] = (float)bias[g];
     }
     return GTS_OK;

@@ -9,22 +9,20 @@
 namespace gts {
 
 // Arrays of the device blob, indices into gts_model::off.  Elements are in
-// bin order (the order gts_pack_paths produced); per-path arrays are in
-// "row-lane order": grouped by output group, then by non-increasing path
-// length, so consecutive paths have equal or similar lengths.
+// bin order, the order gts_pack_paths produced: each bin is at most 64
+// consecutive elements (one wave64 loads it with one element per lane), bins
+// never mix output groups and are ordered by group.  A path is a root element
+// followed by its feature elements; the root's zero-fraction slot holds the
+// path's leaf value v (a root's own zero fraction is always 1 and unused).
 enum BlobArray : int {
   kFeat = 0,       // int32[num_elements]   split feature, -1 on root elements
   kLower = 1,      // float[num_elements]   range [lower, upper)
   kUpper = 2,      // float[num_elements]
-  kZero = 3,       // T[num_elements]       zero fraction
-  kPathFirst = 4,  // int32[num_paths]      element index of the path's root
-  kPathLen = 5,    // int32[num_paths]      path length, root included
-  kPathV = 6,      // T[num_paths]          leaf value
-  kGroupPaths = 7, // int32[G+1]            path range of each group
-  kBinStart = 8,   // int32[num_bins+1]     element range of each bin
-  kGroupBins = 9,  // int32[G+1]            bin range of each group
-  kBias = 10,      // T[G]                  expected value per group
-  kBlobArrays = 11
+  kZero = 3,       // T[num_elements]       zero fraction (leaf value on roots)
+  kBinStart = 4,   // int32[num_bins+1]     element range of each bin
+  kGroupBins = 5,  // int32[G+1]            bin range of each group
+  kBias = 6,       // T[G]                  expected value per group
+  kBlobArrays = 7
 };
 
 constexpr uint32_t kModelMagic = 0x31535447u;  // "GTS1"

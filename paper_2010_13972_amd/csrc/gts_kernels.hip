@@ -1,32 +1,42 @@
 // Device half of libgts for gfx950 (CDNA4, wave64): SHAP values and SHAP
 // interaction values of merged tree paths.
 //
-// Mapping ("row-lane").  A lane owns one (row, path) pair and runs the whole
-// per-path dynamic programme of Algorithm 1 in its registers; a wave holds RW
-// rows x (64/RW) paths.  Paths are visited in groups of equal length (the
-// model layout sorts them), so the trip counts are compile-time constants and
-// a wave never diverges on path length.  With RW == 64 every lane of a wave
-// shares one path, whose elements are then read with scalar loads.
+// Work units.  The model arrives packed into bins of at most 64 path
+// elements (Section 3.3, Best-Fit-Decreasing).  A wave takes one bin at a
+// time and loads it with one element per lane -- the element-per-thread layout
+// of the paper's kernel -- prefetching the next bin while it computes.  A
+// ballot over "is a root element" marks where each path starts.
 //
-// Arithmetic.  EXTEND (Algorithm 1) keeps permutation weights w_k that are
-// the polynomial coefficients E_k of prod_k (z_k + o_k t) scaled by
-// k!(l-k)!/(l+1)!.  The kernels keep E_k itself: adding an element is then
-// E_k <- z E_k + o E_{k-1} (one multiply-add), and the scale factors move
-// into the final sum as the Shapley weights c_k = k!(q-1-k)!/q!.  UNWIND of
-// element i (o_i = 1) divides the polynomial by (z_i + t) from the top
-// coefficient down, as Algorithm 1's o != 0 branch does; for o_i = 0 the
-// contribution reduces to -v * sum_k c_k E_k, the same for every such
-// element, so no division by a zero fraction ever happens.
+// Lanes.  Unlike the paper's kernel, a lane does not own a path element: it
+// owns a (row, path) pair and runs the whole per-path dynamic programme of
+// Algorithm 1 in its registers.  A wave covers RW rows x (64/RW) paths.  With
+// RW == 64 all lanes share one path, whose elements are broadcast from the
+// bin's lanes with v_readlane into scalar registers; with fewer rows per wave
+// each lane pulls its own path's elements with ds_bpermute.  Trip counts are
+// compile-time constants (one variant per path length up to 16 features), so
+// a wave never diverges on path length.  This does the q^2 work of a path once
+// per row instead of spreading it over q lanes that then need q shuffles each.
 //
-// Accumulation.  A workgroup owns a tile of RW rows for one output group and
-// a slice of that group's paths; contributions go to a phi tile in LDS with
-// LDS atomics and the tile is written (or atomically added, when the path
-// list is split across workgroups) to HBM once.
+// Arithmetic.  EXTEND keeps permutation weights w_k, which are the
+// coefficients E_k of prod_k (z_k + o_k t) scaled by k!(l-k)!/(l+1)!.  The
+// kernels keep E_k: adding an element is E_k <- z E_k + o E_{k-1} (one
+// multiply-add), and the scale factors reappear in the final sums as the
+// Shapley weights c_k = k!(q-1-k)!/q!.  UNWIND of an element with o = 1
+// divides the polynomial by (z + t) from the top coefficient down, like
+// Algorithm 1's o != 0 branch; for o = 0 the contribution reduces to
+// -v * sum_k c_k E_k, shared by every such element, so no division by a zero
+// fraction is ever needed.
+//
+// Accumulation.  A workgroup owns a tile of RW rows of one output group and a
+// slice of that group's bins.  Contributions go to a phi tile in LDS (an
+// atomic add built from compare-and-swap); the tile is written to HBM once
+// (atomically added when several workgroups share the row tile).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
-#include <cstdio>
 #include <mutex>
+#include <numeric>
 #include <vector>
 
 #include "gts_internal.h"
@@ -34,8 +44,6 @@
 namespace gts {
 namespace {
 
-constexpr int kWaves = 4;              // waves per workgroup
-constexpr int kBlock = 64 * kWaves;    // threads per workgroup
 constexpr int kMaxUnrolledShap = 16;   // longest path (features) with unrolled code
 constexpr int kMaxUnrolledInter = 8;
 
@@ -44,11 +52,9 @@ struct DevModel {
   const int32_t* __restrict__ feat;
   const float* __restrict__ lower;
   const float* __restrict__ upper;
-  const T* __restrict__ zero;
-  const int32_t* __restrict__ path_first;
-  const int32_t* __restrict__ path_len;
-  const T* __restrict__ path_v;
-  const int32_t* __restrict__ group_paths;
+  const T* __restrict__ zero;         // zero fraction; leaf value on root elements
+  const int32_t* __restrict__ bin_start;
+  const int32_t* __restrict__ group_bins;
   const T* __restrict__ bias;
   int32_t M;
   int32_t G;
@@ -62,58 +68,153 @@ DevModel<T> dev_model(const gts_model* m, const void* blob) {
   d.lower = reinterpret_cast<const float*>(b + m->off[kLower]);
   d.upper = reinterpret_cast<const float*>(b + m->off[kUpper]);
   d.zero = reinterpret_cast<const T*>(b + m->off[kZero]);
-  d.path_first = reinterpret_cast<const int32_t*>(b + m->off[kPathFirst]);
-  d.path_len = reinterpret_cast<const int32_t*>(b + m->off[kPathLen]);
-  d.path_v = reinterpret_cast<const T*>(b + m->off[kPathV]);
-  d.group_paths = reinterpret_cast<const int32_t*>(b + m->off[kGroupPaths]);
+  d.bin_start = reinterpret_cast<const int32_t*>(b + m->off[kBinStart]);
+  d.group_bins = reinterpret_cast<const int32_t*>(b + m->off[kGroupBins]);
   d.bias = reinterpret_cast<const T*>(b + m->off[kBias]);
   d.M = m->num_features;
   d.G = m->num_groups;
   return d;
 }
 
-// Shapley weight of a coalition of size k among the other n-1 players.
-__host__ __device__ constexpr double shapley_weight(int n, int k) {
-  double w = 1.0;
-  // k! (n-1-k)! / n!  =  1 / (n * C(n-1, k))
-  double c = 1.0;
-  for (int i = 1; i <= k; ++i) c = c * (double)(n - i) / (double)i;
-  w = 1.0 / ((double)n * c);
-  return w;
-}
-
 struct Launch {
   int64_t rows;
   int64_t ld;
-  int32_t row_tiles;
-  int32_t splits;   // path-list slices per group
-  int32_t sx;       // LDS row stride of the X tile (floats)
-  int32_t sp;       // LDS row stride of the phi tile (elements)
-  int32_t width;    // phi entries per (row, group): M+1 or (M+1)^2
+  int32_t tiles;     // row tiles
+  int32_t splits;    // bin slices per group
+  int32_t sx;        // LDS row stride of the X tile (floats)
+  int32_t sp;        // LDS row stride of the phi tile (elements)
+  int32_t width;     // phi entries per (row, group): M+1 or (M+1)^2
   int32_t accumulate;  // 1: atomically add the tile to phi (phi pre-zeroed)
 };
 
+// Shapley weight of a coalition of size k among the other n-1 players:
+// k! (n-1-k)! / n!  =  1 / (n * C(n-1, k)).
+__host__ __device__ constexpr double shapley_weight(int n, int k) {
+  double c = 1.0;
+  for (int i = 1; i <= k; ++i) c = c * (double)(n - i) / (double)i;
+  return 1.0 / ((double)n * c);
+}
+
 // ---------------------------------------------------------------------------
-// element fetch: x value test and zero fraction of the lane's path elements
+// cross-lane moves
 // ---------------------------------------------------------------------------
 
+__device__ __forceinline__ int rl(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+__device__ __forceinline__ float rl(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+__device__ __forceinline__ double rl(double v, int lane) {
+  const unsigned long long u = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)(u & 0xffffffffu), lane);
+  const int hi = __builtin_amdgcn_readlane((int)(u >> 32), lane);
+  return __longlong_as_double(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+// ds_bpermute: value of lane `lane` (taken modulo the wave size)
+__device__ __forceinline__ int bp(int v, int lane) {
+  return __builtin_amdgcn_ds_bpermute((lane & 63) << 2, v);
+}
+__device__ __forceinline__ float bp(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_ds_bpermute((lane & 63) << 2, __float_as_int(v)));
+}
+__device__ __forceinline__ double bp(double v, int lane) {
+  const unsigned long long u = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_ds_bpermute((lane & 63) << 2, (int)(u & 0xffffffffu));
+  const int hi = __builtin_amdgcn_ds_bpermute((lane & 63) << 2, (int)(u >> 32));
+  return __longlong_as_double(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+
+// Add to a phi-tile entry in LDS.  A compare-and-swap loop on the bit
+// pattern: gfx950 executes the LDS float add atomic (ds_add_f32) one lane at
+// a time, about 190 cycles per wave64 instruction, while the integer
+// compare-and-swap runs at the rate of a plain read-modify-write; without a
+// conflict the loop runs once.
+__device__ __forceinline__ void lds_add(float* p, float v) {
+  unsigned* q = reinterpret_cast<unsigned*>(p);
+  unsigned old = *q, assumed;
+  do {
+    assumed = old;
+    old = atomicCAS(q, assumed, __float_as_uint(__uint_as_float(assumed) + v));
+  } while (old != assumed);
+}
+__device__ __forceinline__ void lds_add(double* p, double v) {
+  unsigned long long* q = reinterpret_cast<unsigned long long*>(p);
+  unsigned long long old = *q, assumed;
+  do {
+    assumed = old;
+    old = atomicCAS(q, assumed,
+                    (unsigned long long)__double_as_longlong(__longlong_as_double((long long)assumed) + v));
+  } while (old != assumed);
+}
+
+// One bin, one element per lane.
+template <typename T>
+struct Bin {
+  int feat;   // -1 root, -2 past the end of the bin
+  float lo, hi;
+  T z;        // zero fraction, or the leaf value on a root
+  int len;    // elements in the bin (uniform)
+};
+
+template <typename T>
+__device__ __forceinline__ Bin<T> load_bin(const DevModel<T>& d, int bi, int lane) {
+  Bin<T> b;
+  const int e0 = d.bin_start[bi];
+  b.len = d.bin_start[bi + 1] - e0;
+  if (lane < b.len) {
+    const int e = e0 + lane;
+    b.feat = d.feat[e];
+    b.lo = d.lower[e];
+    b.hi = d.upper[e];
+    b.z = d.zero[e];
+  } else {
+    b.feat = -2;
+    b.lo = 0.0f;
+    b.hi = 0.0f;
+    b.z = T(0);
+  }
+  return b;
+}
+
+// Element k (0-based among the path's features) of the path starting at
+// bin lane s.  UNIFORM: s is the same for the whole wave (v_readlane);
+// otherwise s is per lane (ds_bpermute, executed by every lane).
+template <typename T, bool UNIFORM>
+struct Fetch {
+  const Bin<T>& b;
+  int s;
+  __device__ __forceinline__ int feat(int k) const {
+    return UNIFORM ? rl(b.feat, s + 1 + k) : bp(b.feat, s + 1 + k);
+  }
+  __device__ __forceinline__ float lo(int k) const {
+    return UNIFORM ? rl(b.lo, s + 1 + k) : bp(b.lo, s + 1 + k);
+  }
+  __device__ __forceinline__ float hi(int k) const {
+    return UNIFORM ? rl(b.hi, s + 1 + k) : bp(b.hi, s + 1 + k);
+  }
+  __device__ __forceinline__ T z(int k) const {
+    return UNIFORM ? rl(b.z, s + 1 + k) : bp(b.z, s + 1 + k);
+  }
+  __device__ __forceinline__ T v() const { return UNIFORM ? rl(b.z, s) : bp(b.z, s); }
+};
+
+// Feature, presence test o_k = [lower <= x < upper] and zero fraction of
+// the first Q elements.  Elements k >= q are padding: present with
+// probability 1 and absent with probability 1 (z = o = 1), which changes no
+// other element's Shapley value; f = -1 marks them unwritten.
 template <typename T, int Q, bool UNIFORM>
-__device__ __forceinline__ void load_elements(const DevModel<T>& d, int first, int q,
-                                              const float* __restrict__ xrow, int (&f)[Q],
-                                              bool (&o)[Q], T (&z)[Q]) {
+__device__ __forceinline__ void load_path(const Fetch<T, UNIFORM>& fe, int q,
+                                          const float* __restrict__ xrow, int (&f)[Q],
+                                          bool (&o)[Q], T (&z)[Q]) {
 #pragma unroll
   for (int k = 0; k < Q; ++k) {
-    if (UNIFORM || k < q) {
-      const int e = first + k;
-      f[k] = d.feat[e];
-      const float x = xrow[f[k]];
-      o[k] = (d.lower[e] <= x) && (x < d.upper[e]);
-      z[k] = d.zero[e];
-    } else {  // padding element: present with probability 1, changes nothing
-      f[k] = -1;
-      o[k] = true;
-      z[k] = T(1);
-    }
+    const int fk = fe.feat(k);
+    const float lo = fe.lo(k), hi = fe.hi(k);
+    const T zk = fe.z(k);
+    const bool real = UNIFORM || k < q;
+    const float x = xrow[real ? fk : 0];
+    f[k] = real ? fk : -1;
+    o[k] = real ? (lo <= x) && (x < hi) : true;
+    z[k] = real ? zk : T(1);
   }
 }
 
@@ -134,7 +235,7 @@ __device__ __forceinline__ void extend_all(const bool (&o)[Q], const T (&z)[Q], 
   }
 }
 
-// D = E / (zi + t) for a degree-Q polynomial E with E_Q known; D has Q terms.
+// D = E / (zi + t) for a degree-Q polynomial E; D has Q terms.
 template <typename T, int Q>
 __device__ __forceinline__ void unwind_one(const T (&E)[Q + 1], T zi, T (&D)[Q]) {
   D[Q - 1] = E[Q];
@@ -143,22 +244,15 @@ __device__ __forceinline__ void unwind_one(const T (&E)[Q + 1], T zi, T (&D)[Q])
 }
 
 // ---------------------------------------------------------------------------
-// SHAP values of one (row, path) per lane, Q features per path
+// per-lane path arithmetic
 // ---------------------------------------------------------------------------
 
-template <typename T, int Q, bool UNIFORM>
-__device__ __forceinline__ void shap_round(const DevModel<T>& d, int p, bool active,
-                                           const float* __restrict__ xrow, T* __restrict__ prow) {
-  const int first = d.path_first[p] + 1;
-  const int q = UNIFORM ? Q : d.path_len[p] - 1;
-  const T v = d.path_v[p];
-  int f[Q];
-  bool o[Q];
-  T z[Q];
-  load_elements<T, Q, UNIFORM>(d, first, q, xrow, f, o, z);
+// SHAP values: phi[f_i] += v (o_i - z_i) * sum_k c_k D^i_k
+template <typename T, int Q>
+__device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
+                                          T v, bool active, T* __restrict__ prow) {
   T E[Q + 1];
   extend_all<T, Q>(o, z, E);
-  // shared contribution of every element with o = 0
   T t_all = T(0);
 #pragma unroll
   for (int k = 0; k < Q; ++k) t_all = fma(T(shapley_weight(Q, k)), E[k], t_all);
@@ -171,74 +265,21 @@ __device__ __forceinline__ void shap_round(const DevModel<T>& d, int p, bool act
 #pragma unroll
     for (int k = 0; k < Q; ++k) s = fma(T(shapley_weight(Q, k)), D[k], s);
     const T phi = o[i] ? v * (T(1) - z[i]) * s : neg_vt;
-    if (active && f[i] >= 0) atomicAdd(&prow[f[i]], phi);
+    if (active && f[i] >= 0) lds_add(&prow[f[i]], phi);
   }
 }
 
-// Paths longer than the unrolled variants: same arithmetic with runtime loops,
-// always in fp64.  Dividing the weight polynomial from its top coefficient
-// down cancels more and more as paths grow; in fp32 the error passes the
-// parity bound beyond about 20 features, in fp64 it stays far inside it for
-// the longest path a wave64 holds (63 features).  FP64 FMAs run at the same
-// rate as unpacked FP32 ones on gfx950.
-template <typename T>
-__device__ void shap_round_dyn(const DevModel<T>& d, int p, bool active,
-                               const float* __restrict__ xrow, T* __restrict__ prow) {
-  const int first = d.path_first[p] + 1;
-  const int q = d.path_len[p] - 1;
-  const double v = (double)d.path_v[p];
-  double E[kMaxPathLen];
-  double z[kMaxPathLen];
-  double D[kMaxPathLen];
-  uint64_t obits = 0;
-  E[0] = 1.0;
-  for (int l = 1; l <= q; ++l) {
-    const int e = first + l - 1;
-    const float x = xrow[d.feat[e]];
-    const bool ol = (d.lower[e] <= x) && (x < d.upper[e]);
-    const double zl = (double)d.zero[e];
-    z[l - 1] = zl;
-    obits |= (uint64_t)ol << (l - 1);
-    E[l] = ol ? E[l - 1] : 0.0;
-    for (int k = l - 1; k >= 1; --k) E[k] = fma(zl, E[k], ol ? E[k - 1] : 0.0);
-    E[0] = zl * E[0];
-  }
-  double t_all = 0.0;
-  for (int k = 0; k < q; ++k) t_all = fma(shapley_weight(q, k), E[k], t_all);
-  for (int i = 0; i < q; ++i) {
-    D[q - 1] = E[q];
-    for (int k = q - 1; k >= 1; --k) D[k - 1] = fma(-z[i], D[k], E[k]);
-    double s = 0.0;
-    for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
-    const bool oi = (obits >> i) & 1u;
-    const double phi = oi ? v * (1.0 - z[i]) * s : -v * t_all;
-    if (active) atomicAdd(&prow[d.feat[first + i]], (T)phi);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// SHAP interaction values of one (row, path) per lane
-// ---------------------------------------------------------------------------
-// For elements i != c of a path with value v the interaction through this
-// path is Delta_ic = v/2 (o_i - z_i)(o_c - z_c) S_ic, where S_ic is the
-// Shapley-weighted sum over the path without i and c (weights for q-1
-// players).  By cases on (o_i, o_c):
+// Interaction values.  For elements i != c the interaction through this path
+// is Delta_ic = v/2 (o_i - z_i)(o_c - z_c) S_ic, S_ic the Shapley-weighted sum
+// over the path without i and c (weights for q-1 players).  By cases on
+// (o_i, o_c):
 //   (1,1): S_ic from E / ((z_i + t)(z_c + t))
-//   (1,0): (o_c - z_c) S_ic = -sum_k c'_k D^i_k           (D^i = E / (z_i + t))
+//   (1,0): (o_c - z_c) S_ic = -sum_k c'_k D^i_k         (D^i = E / (z_i + t))
 //   (0,0): (o_i - z_i)(o_c - z_c) S_ic = sum_k c'_k E_k
-// phi_ii = phi_i - sum_{c != i} Delta_ic (Eq. 6).
-
-template <typename T, int Q, bool UNIFORM>
-__device__ __forceinline__ void inter_round(const DevModel<T>& d, int p, bool active,
-                                            const float* __restrict__ xrow, T* __restrict__ prow,
-                                            int stride) {
-  const int first = d.path_first[p] + 1;
-  const int q = UNIFORM ? Q : d.path_len[p] - 1;
-  const T v = d.path_v[p];
-  int f[Q];
-  bool o[Q];
-  T z[Q];
-  load_elements<T, Q, UNIFORM>(d, first, q, xrow, f, o, z);
+// and phi_ii = phi_i - sum_{c != i} Delta_ic (Eq. 6).
+template <typename T, int Q>
+__device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
+                                           T v, bool active, T* __restrict__ prow, int stride) {
   T E[Q + 1];
   extend_all<T, Q>(o, z, E);
   T t_all = T(0);
@@ -260,26 +301,22 @@ __device__ __forceinline__ void inter_round(const DevModel<T>& d, int p, bool ac
 #pragma unroll
     for (int k = 0; k < Q; ++k) s = fma(T(shapley_weight(Q, k)), D[k], s);
     diag[c] = o[c] ? v * (T(1) - z[c]) * s : -v * t_all;
+    tp[c] = T(0);
     if constexpr (Q >= 2) {
-      T acc = T(0);
 #pragma unroll
-      for (int k = 0; k < Q - 1; ++k) acc = fma(T(shapley_weight(Q - 1, k)), D[k], acc);
-      tp[c] = acc;
-    } else {
-      tp[c] = T(0);
+      for (int k = 0; k < Q - 1; ++k) tp[c] = fma(T(shapley_weight(Q - 1, k)), D[k], tp[c]);
     }
 #pragma unroll
     for (int i = 0; i < c; ++i) {
-      // (1,1): divide D^c by (z_i + t) -> Q-1 terms, weighted sum
-      T DD[Q];
+      T s11 = T(0);
       if constexpr (Q >= 2) {
+        T DD[Q];
         DD[Q - 2] = D[Q - 1];
 #pragma unroll
         for (int k = Q - 2; k >= 1; --k) DD[k - 1] = fma(-z[i], DD[k], D[k]);
-      }
-      T s11 = T(0);
 #pragma unroll
-      for (int k = 0; k < Q - 1; ++k) s11 = fma(T(shapley_weight(Q - 1, k)), DD[k], s11);
+        for (int k = 0; k < Q - 1; ++k) s11 = fma(T(shapley_weight(Q - 1, k)), DD[k], s11);
+      }
       T delta;
       if (o[i] && o[c]) delta = half_v * (T(1) - z[i]) * (T(1) - z[c]) * s11;
       else if (o[i]) delta = -half_v * (T(1) - z[i]) * tp[i];
@@ -288,169 +325,251 @@ __device__ __forceinline__ void inter_round(const DevModel<T>& d, int p, bool ac
       diag[c] -= delta;
       diag[i] -= delta;
       if (active && f[i] >= 0 && f[c] >= 0) {
-        atomicAdd(&prow[f[i] * stride + f[c]], delta);
-        atomicAdd(&prow[f[c] * stride + f[i]], delta);
+        lds_add(&prow[f[i] * stride + f[c]], delta);
+        lds_add(&prow[f[c] * stride + f[i]], delta);
       }
     }
   }
 #pragma unroll
   for (int c = 0; c < Q; ++c)
-    if (active && f[c] >= 0) atomicAdd(&prow[f[c] * stride + f[c]], diag[c]);
+    if (active && f[c] >= 0) lds_add(&prow[f[c] * stride + f[c]], diag[c]);
 }
 
-// Long paths: runtime loops, always in fp64 (see shap_round_dyn).
-template <typename T>
-__device__ void inter_round_dyn(const DevModel<T>& d, int p, bool active,
-                                const float* __restrict__ xrow, T* __restrict__ prow, int stride) {
-  const int first = d.path_first[p] + 1;
-  const int q = d.path_len[p] - 1;
-  const double v = (double)d.path_v[p];
+// Paths longer than the unrolled variants: the same arithmetic with runtime
+// loops, always in fp64.  Dividing the weight polynomial from its top
+// coefficient down cancels more and more as paths grow; in fp32 the error
+// passes the parity bound beyond about 20 features, in fp64 it stays far
+// inside it for the longest path a wave64 holds (63 features).  FP64 FMAs run
+// at the rate of unpacked FP32 ones on gfx950.
+template <typename T, bool UNIFORM, bool INTER>
+__device__ void path_dyn(const Fetch<T, UNIFORM>& fe, int qfetch, int q, bool active,
+                         const float* __restrict__ xrow, T* __restrict__ prow, int stride) {
   double E[kMaxPathLen];
   double z[kMaxPathLen];
   double D[kMaxPathLen];
-  double DD[kMaxPathLen];
-  double tp[kMaxPathLen];
-  double diag[kMaxPathLen];
+  int f[kMaxPathLen];
   uint64_t obits = 0;
+  // fetch with a wave-uniform trip count (ds_bpermute needs every lane)
+  for (int k = 0; k < qfetch; ++k) {
+    const int fk = fe.feat(k);
+    const float lo = fe.lo(k), hi = fe.hi(k);
+    const double zk = (double)fe.z(k);
+    if (k < q) {
+      const float x = xrow[fk];
+      f[k] = fk;
+      z[k] = zk;
+      obits |= (uint64_t)((lo <= x) && (x < hi)) << k;
+    }
+  }
+  const double v = (double)fe.v();
   E[0] = 1.0;
   for (int l = 1; l <= q; ++l) {
-    const int e = first + l - 1;
-    const float x = xrow[d.feat[e]];
-    const bool ol = (d.lower[e] <= x) && (x < d.upper[e]);
-    const double zl = (double)d.zero[e];
-    z[l - 1] = zl;
-    obits |= (uint64_t)ol << (l - 1);
+    const double zl = z[l - 1];
+    const bool ol = (obits >> (l - 1)) & 1u;
     E[l] = ol ? E[l - 1] : 0.0;
     for (int k = l - 1; k >= 1; --k) E[k] = fma(zl, E[k], ol ? E[k - 1] : 0.0);
     E[0] = zl * E[0];
   }
-  double t_all = 0.0, t_pair = 0.0;
+  double t_all = 0.0;
   for (int k = 0; k < q; ++k) t_all = fma(shapley_weight(q, k), E[k], t_all);
-  for (int k = 0; k < q - 1; ++k) t_pair = fma(shapley_weight(q - 1, k), E[k], t_pair);
-  const double half_v = 0.5 * v;
-  for (int c = 0; c < q; ++c) {
-    D[q - 1] = E[q];
-    for (int k = q - 1; k >= 1; --k) D[k - 1] = fma(-z[c], D[k], E[k]);
-    double s = 0.0, acc = 0.0;
-    for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
-    for (int k = 0; k < q - 1; ++k) acc = fma(shapley_weight(q - 1, k), D[k], acc);
-    const bool oc = (obits >> c) & 1u;
-    diag[c] = oc ? v * (1.0 - z[c]) * s : -v * t_all;
-    tp[c] = acc;
-    const int fc = d.feat[first + c];
-    for (int i = 0; i < c; ++i) {
-      DD[q - 2] = D[q - 1];
-      for (int k = q - 2; k >= 1; --k) DD[k - 1] = fma(-z[i], DD[k], D[k]);
-      double s11 = 0.0;
-      for (int k = 0; k < q - 1; ++k) s11 = fma(shapley_weight(q - 1, k), DD[k], s11);
+  if constexpr (!INTER) {
+    for (int i = 0; i < q; ++i) {
+      D[q - 1] = E[q];
+      for (int k = q - 1; k >= 1; --k) D[k - 1] = fma(-z[i], D[k], E[k]);
+      double s = 0.0;
+      for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
       const bool oi = (obits >> i) & 1u;
-      double delta;
-      if (oi && oc) delta = half_v * (1.0 - z[i]) * (1.0 - z[c]) * s11;
-      else if (oi) delta = -half_v * (1.0 - z[i]) * tp[i];
-      else if (oc) delta = -half_v * (1.0 - z[c]) * tp[c];
-      else delta = half_v * t_pair;
-      diag[c] -= delta;
-      diag[i] -= delta;
-      const int fi = d.feat[first + i];
-      if (active) {
-        atomicAdd(&prow[fi * stride + fc], (T)delta);
-        atomicAdd(&prow[fc * stride + fi], (T)delta);
+      const double phi = oi ? v * (1.0 - z[i]) * s : -v * t_all;
+      if (active) lds_add(&prow[f[i]], (T)phi);
+    }
+  } else {
+    double DD[kMaxPathLen];
+    double tp[kMaxPathLen];
+    double diag[kMaxPathLen];
+    double t_pair = 0.0;
+    for (int k = 0; k < q - 1; ++k) t_pair = fma(shapley_weight(q - 1, k), E[k], t_pair);
+    const double half_v = 0.5 * v;
+    for (int c = 0; c < q; ++c) {
+      D[q - 1] = E[q];
+      for (int k = q - 1; k >= 1; --k) D[k - 1] = fma(-z[c], D[k], E[k]);
+      double s = 0.0, acc = 0.0;
+      for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
+      for (int k = 0; k < q - 1; ++k) acc = fma(shapley_weight(q - 1, k), D[k], acc);
+      const bool oc = (obits >> c) & 1u;
+      diag[c] = oc ? v * (1.0 - z[c]) * s : -v * t_all;
+      tp[c] = acc;
+      for (int i = 0; i < c; ++i) {
+        DD[q - 2] = D[q - 1];
+        for (int k = q - 2; k >= 1; --k) DD[k - 1] = fma(-z[i], DD[k], D[k]);
+        double s11 = 0.0;
+        for (int k = 0; k < q - 1; ++k) s11 = fma(shapley_weight(q - 1, k), DD[k], s11);
+        const bool oi = (obits >> i) & 1u;
+        double delta;
+        if (oi && oc) delta = half_v * (1.0 - z[i]) * (1.0 - z[c]) * s11;
+        else if (oi) delta = -half_v * (1.0 - z[i]) * tp[i];
+        else if (oc) delta = -half_v * (1.0 - z[c]) * tp[c];
+        else delta = half_v * t_pair;
+        diag[c] -= delta;
+        diag[i] -= delta;
+        if (active) {
+          lds_add(&prow[f[i] * stride + f[c]], (T)delta);
+          lds_add(&prow[f[c] * stride + f[i]], (T)delta);
+        }
       }
     }
+    for (int c = 0; c < q; ++c)
+      if (active) lds_add(&prow[f[c] * stride + f[c]], (T)diag[c]);
   }
-  for (int c = 0; c < q; ++c)
-    if (active) {
-      const int fc = d.feat[first + c];
-      atomicAdd(&prow[fc * stride + fc], (T)diag[c]);
-    }
 }
 
-// ---------------------------------------------------------------------------
-// workgroup driver
-// ---------------------------------------------------------------------------
+template <typename T, int Q, bool UNIFORM, bool INTER>
+__device__ __forceinline__ void path_fixed(const Fetch<T, UNIFORM>& fe, int q, bool active,
+                                           const float* __restrict__ xrow, T* __restrict__ prow,
+                                           int stride) {
+  int f[Q];
+  bool o[Q];
+  T z[Q];
+  load_path<T, Q, UNIFORM>(fe, q, xrow, f, o, z);
+  const T v = fe.v();
+  if constexpr (INTER) inter_math<T, Q>(f, o, z, v, active, prow, stride);
+  else shap_math<T, Q>(f, o, z, v, active, prow);
+}
 
-template <typename T, int RW, bool INTER>
-__device__ __forceinline__ void dispatch_round(int Q, const DevModel<T>& d, int p, bool active,
-                                               const float* xrow, T* prow) {
-  constexpr bool U = (RW == 64);
+// Q = features of the longest path in the wave's current set (uniform)
+template <typename T, bool UNIFORM, bool INTER>
+__device__ __forceinline__ void dispatch(int Q, const Fetch<T, UNIFORM>& fe, int q, bool active,
+                                         const float* xrow, T* prow, int stride) {
+  static_assert(kMaxUnrolledShap == 16 && kMaxUnrolledInter == 8, "update the case lists");
   if constexpr (INTER) {
     switch (Q) {
-#define GTS_CASE(n) case n: inter_round<T, n, U>(d, p, active, xrow, prow, d.M + 1); break;
+#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, true>(fe, q, active, xrow, prow, stride); break;
       GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
       GTS_CASE(7) GTS_CASE(8)
 #undef GTS_CASE
-      default: inter_round_dyn<T>(d, p, active, xrow, prow, d.M + 1); break;
+      default: path_dyn<T, UNIFORM, true>(fe, Q, q, active, xrow, prow, stride); break;
     }
   } else {
     switch (Q) {
-#define GTS_CASE(n) case n: shap_round<T, n, U>(d, p, active, xrow, prow); break;
+#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, false>(fe, q, active, xrow, prow, stride); break;
       GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
       GTS_CASE(7) GTS_CASE(8) GTS_CASE(9) GTS_CASE(10) GTS_CASE(11) GTS_CASE(12)
       GTS_CASE(13) GTS_CASE(14) GTS_CASE(15) GTS_CASE(16)
 #undef GTS_CASE
-      default: shap_round_dyn<T>(d, p, active, xrow, prow); break;
+      default: path_dyn<T, UNIFORM, false>(fe, Q, q, active, xrow, prow, stride); break;
     }
   }
 }
 
-// One workgroup: rows [tile*RW, tile*RW + RW) of output group g, paths of
-// slice s of that group.  blockIdx.x = (tile * G + g) * S + s, so with S a
-// multiple of 8 each XCD (blocks are dealt round-robin to the 8 XCDs) reads
-// only its own slices of the path list.
+// All paths of one bin.  RW == 64: one path at a time for the whole wave.
+// RW < 64: rounds of up to P = 64/RW paths, lane (j, r) = (path j, row r).
 template <typename T, int RW, bool INTER>
-__global__ __launch_bounds__(kBlock) void rowlane_kernel(DevModel<T> d, const float* __restrict__ X,
-                                                        T* __restrict__ phi, Launch L) {
+__device__ __forceinline__ void process_bin(const Bin<T>& b, int lane, const float* xrow,
+                                            T* prow, int stride) {
+  uint64_t roots = __ballot(b.feat == -1);
+  if constexpr (RW == 64) {
+    while (roots) {
+      const int s = __builtin_ctzll(roots);
+      roots &= roots - 1;
+      const int e = roots ? __builtin_ctzll(roots) : b.len;
+      const int q = e - s - 1;
+      if (q > 0) dispatch<T, true, INTER>(q, Fetch<T, true>{b, s}, q, true, xrow, prow, stride);
+    }
+  } else {
+    constexpr int P = 64 / RW;
+    const int j = lane / RW;
+    while (roots) {
+      int my_s = 0, my_q = -1, qmax = 0;
+#pragma unroll
+      for (int jj = 0; jj < P; ++jj) {
+        if (roots) {
+          const int s = __builtin_ctzll(roots);
+          roots &= roots - 1;
+          const int e = roots ? __builtin_ctzll(roots) : b.len;
+          const int q = e - s - 1;
+          qmax = q > qmax ? q : qmax;
+          if (j == jj) {
+            my_s = s;
+            my_q = q;
+          }
+        }
+      }
+      const bool active = my_q > 0;
+      if (my_q < 0) my_q = 0;
+      if (qmax > 0)
+        dispatch<T, false, INTER>(qmax, Fetch<T, false>{b, my_s}, my_q, active, xrow, prow, stride);
+    }
+  }
+}
+
+// One workgroup: rows [tile*RW, tile*RW + RW) of output group g, bins of
+// slice s of that group.  Workgroups are dealt to the 8 XCDs round-robin; when
+// the (group, slice) units divide evenly among the XCDs, consecutive
+// workgroups on an XCD take the same unit for successive row tiles, so each
+// XCD's L2 holds only its own part of the model.
+template <typename T, int RW, bool INTER, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const float* __restrict__ X,
+                                                         T* __restrict__ phi, Launch L) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int P = 64 / RW;  // paths per wave round
+  constexpr int kThreads = 64 * WAVES;
   const int M = d.M;
   const int G = d.G;
+  const int U = G * L.splits;
   const int64_t b = blockIdx.x;
-  const int s = (int)(b % L.splits);
-  const int64_t tg = b / L.splits;
-  const int g = (int)(tg % G);
-  const int64_t tile = tg / G;
+  int64_t tile;
+  int u;
+  if (U % 8 == 0) {
+    const int64_t local = b >> 3;
+    tile = local % L.tiles;
+    u = (int)(b & 7) + 8 * (int)(local / L.tiles);
+  } else {
+    tile = b / U;
+    u = (int)(b % U);
+  }
+  const int g = u / L.splits;
+  const int s = u - g * L.splits;
   const int64_t r0 = tile * RW;
 
   float* xs = reinterpret_cast<float*>(smem);
   T* ps = reinterpret_cast<T*>(smem + (size_t)RW * L.sx * sizeof(float));
 
   // stage the X tile (coalesced along each row) and clear the phi tile
-  for (int i = threadIdx.x; i < RW * M; i += kBlock) {
+  for (int i = threadIdx.x; i < RW * M; i += kThreads) {
     const int r = i / M, c = i - r * M;
     const int64_t row = r0 + r;
     xs[r * L.sx + c] = row < L.rows ? X[row * L.ld + c] : 0.0f;
   }
-  for (int i = threadIdx.x; i < RW * L.sp; i += kBlock) ps[i] = T(0);
+  for (int i = threadIdx.x; i < RW * L.sp; i += kThreads) ps[i] = T(0);
   __syncthreads();
 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int r = lane % RW;
-  const int j = lane / RW;
-  const int g0 = d.group_paths[g], g1 = d.group_paths[g + 1];
-  const int n = g1 - g0;
-  int chunk = (n + L.splits - 1) / L.splits;
-  chunk = (chunk + P - 1) / P * P;
-  const int a = g0 + min(n, s * chunk);
-  const int e = g0 + min(n, (s + 1) * chunk);
-  const int rounds = (e - a + P - 1) / P;
+  const int gb0 = d.group_bins[g], gb1 = d.group_bins[g + 1];
+  const int nb = gb1 - gb0;
+  const int chunk = (nb + L.splits - 1) / L.splits;
+  const int b_lo = gb0 + min(nb, s * chunk);
+  const int b_hi = gb0 + min(nb, (s + 1) * chunk);
   const float* xrow = xs + r * L.sx;
   T* prow = ps + r * L.sp;
-  for (int rd = wave; rd < rounds; rd += kWaves) {
-    const int lead = __builtin_amdgcn_readfirstlane(a + rd * P);
-    const int Q = __builtin_amdgcn_readfirstlane(d.path_len[lead]) - 1;
-    int p = lead + j;
-    const bool active = p < e;
-    if (!active) p = lead;
-    if (RW == 64) p = __builtin_amdgcn_readfirstlane(p);
-    if (Q > 0) dispatch_round<T, RW, INTER>(Q, d, p, active, xrow, prow);
+  const int stride = M + 1;
+
+  int bi = b_lo + wave;
+  if (bi < b_hi) {
+    Bin<T> cur = load_bin(d, bi, lane);
+    for (; bi < b_hi; bi += WAVES) {
+      Bin<T> nxt;
+      const int bn = bi + WAVES;
+      if (bn < b_hi) nxt = load_bin(d, bn, lane);
+      process_bin<T, RW, INTER>(cur, lane, xrow, prow, stride);
+      cur = nxt;
+    }
   }
   __syncthreads();
 
   // write the tile: phi[row][g][.]; the bias goes to the last entry
   const T bias = d.bias[g];
   const int W = L.width;
-  for (int i = threadIdx.x; i < RW * W; i += kBlock) {
+  for (int i = threadIdx.x; i < RW * W; i += kThreads) {
     const int rr = i / W, c = i - rr * W;
     const int64_t row = r0 + rr;
     if (row >= L.rows) continue;
@@ -472,27 +591,39 @@ __global__ void fill_zero(T* __restrict__ p, int64_t n) {
 // host-side launch
 // ---------------------------------------------------------------------------
 
-int device_cus() {
-  static std::mutex mu;
-  static std::vector<int> cus;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 256;
-  std::lock_guard<std::mutex> lock(mu);
-  if ((int)cus.size() <= dev) cus.resize(dev + 1, 0);
-  if (cus[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    cus[dev] = n;
-  }
-  return cus[dev];
-}
+struct DeviceInfo {
+  int cus = 256;
+  int lds_per_block = 64 * 1024;
+};
 
-constexpr int64_t kLdsBudget = 64 * 1024;
+DeviceInfo device_info() {
+  static std::mutex mu;
+  static std::vector<DeviceInfo> cache;
+  static std::vector<char> have;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return DeviceInfo{};
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)cache.size() <= dev) {
+    cache.resize(dev + 1);
+    have.resize(dev + 1, 0);
+  }
+  if (!have[dev]) {
+    DeviceInfo info;
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      info.cus = n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
+        n > 0)
+      info.lds_per_block = n;
+    cache[dev] = info;
+    have[dev] = 1;
+  }
+  return cache[dev];
+}
 
 inline int odd_at_least(int n) { return n | 1; }
 
-template <typename T, int RW, bool INTER>
+template <typename T, int RW, bool INTER, int WAVES>
 gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64_t rows,
                      int64_t ld, void* phi, hipStream_t stream, int splits, int32_t sx, int32_t sp,
                      int32_t width, size_t lds) {
@@ -500,27 +631,25 @@ gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64
   Launch L;
   L.rows = rows;
   L.ld = ld;
-  L.row_tiles = (int32_t)((rows + RW - 1) / RW);
+  L.tiles = (int32_t)((rows + RW - 1) / RW);
   L.splits = splits;
   L.sx = sx;
   L.sp = sp;
   L.width = width;
   L.accumulate = splits > 1 ? 1 : 0;
-  const int64_t total = (int64_t)rows * m->num_groups * width;
+  const int64_t total = rows * (int64_t)m->num_groups * width;
   if (L.accumulate) {
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 65536);
     hipLaunchKernelGGL(fill_zero<T>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        static_cast<T*>(phi), total);
   }
-  const int64_t grid = (int64_t)L.row_tiles * m->num_groups * splits;
+  const int64_t grid = (int64_t)L.tiles * m->num_groups * splits;
   if (grid > 0x7fffffffLL) return fail(GTS_EINVAL, "problem too large for one launch");
-  auto kern = rowlane_kernel<T, RW, INTER>;
-  if (lds > 48 * 1024) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-      return fail(GTS_EDEVICE, "cannot raise the LDS limit to %zu bytes", lds);
-  }
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kBlock), lds, stream, d, X,
+  auto kern = shap_kernel<T, RW, INTER, WAVES>;
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return fail(GTS_EDEVICE, "cannot set the LDS size of the kernel to %zu bytes", lds);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * WAVES), lds, stream, d, X,
                      static_cast<T*>(phi), L);
   const hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
@@ -530,38 +659,63 @@ gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64
 template <typename T, bool INTER>
 gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t rows, int64_t ld,
                   void* phi, hipStream_t stream) {
+  const DeviceInfo dev = device_info();
   const int M = m->num_features;
   const int G = m->num_groups;
-  const int32_t width = INTER ? (M + 1) * (M + 1) : (M + 1);
+  const int64_t width64 = INTER ? (int64_t)(M + 1) * (M + 1) : (int64_t)(M + 1);
+  if (width64 > (1 << 30)) return fail(GTS_EINVAL, "M = %d is too large", M);
+  const int32_t width = (int32_t)width64;
   const int32_t sx = odd_at_least(M);
   const int32_t sp = odd_at_least(width);
-  // largest row tile whose X and phi tiles fit the LDS budget
+  // Row tile: the largest RW whose X and phi tiles fit in 64 KB (several
+  // workgroups per CU, 4 waves each).  If that leaves fewer than 8 rows per
+  // wave (more than 8 paths per round, while a bin holds about 64/L paths),
+  // use up to the whole LDS of a workgroup for 8 rows, with 8 waves.
+  auto need = [&](int rw) { return (size_t)rw * ((size_t)sx * sizeof(float) + (size_t)sp * sizeof(T)); };
   int RW = 0;
-  size_t lds = 0;
-  for (int cand : {64, 32, 16, 8, 4}) {
-    const size_t need = (size_t)cand * ((size_t)sx * sizeof(float) + (size_t)sp * sizeof(T));
-    if ((int64_t)need <= kLdsBudget) { RW = cand; lds = need; break; }
+  int waves = 4;
+  for (int cand : {64, 32, 16, 8}) {
+    if (need(cand) <= 64 * 1024) {
+      RW = cand;
+      break;
+    }
   }
-  if (RW == 0)
-    return fail(GTS_EINVAL, "M = %d is too large for an LDS tile of 4 rows", M);
-  // enough workgroups to give every CU several; slices a multiple of 8 (XCDs)
+  if (RW == 0 && (int64_t)need(8) <= dev.lds_per_block) {
+    RW = 8;
+    waves = 8;
+  }
+  if (RW == 0 && (int64_t)need(4) <= dev.lds_per_block) {
+    RW = 4;
+    waves = need(4) > 64 * 1024 ? 8 : 4;
+  }
+  if (RW == 0) return fail(GTS_EINVAL, "M = %d needs more LDS than a workgroup has", M);
+  const size_t lds = need(RW);
+  // enough workgroups to give every CU several; (group, slice) units a
+  // multiple of the 8 XCDs when the bin list is split
   const int64_t tiles = (rows + RW - 1) / RW;
   const int64_t base = tiles * G;
-  const int64_t target = 8LL * device_cus();
+  const int64_t target = 8LL * dev.cus;
+  const int64_t bins_per_group = std::max<int64_t>(1, m->num_bins / G);
   int splits = 1;
   if (base < target) {
-    const int64_t max_paths = std::max<int64_t>(1, m->num_paths / G);
-    splits = (int)std::min<int64_t>((target + base - 1) / base, max_paths / (64 / RW) + 1);
-    splits = std::max(1, splits);
-    if (splits > 1) splits = (splits + 7) / 8 * 8;
+    int64_t want = (target + base - 1) / base;
+    const int64_t step = 8 / std::gcd(G, 8);
+    want = (want + step - 1) / step * step;
+    splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
   }
+#define GTS_LAUNCH(rw)                                                                       \
+  return waves == 8 ? launch_rw<T, rw, INTER, 8>(m, blob, X, rows, ld, phi, stream, splits, sx, \
+                                                 sp, width, lds)                                \
+                    : launch_rw<T, rw, INTER, 4>(m, blob, X, rows, ld, phi, stream, splits, sx, \
+                                                 sp, width, lds)
   switch (RW) {
-    case 64: return launch_rw<T, 64, INTER>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, width, lds);
-    case 32: return launch_rw<T, 32, INTER>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, width, lds);
-    case 16: return launch_rw<T, 16, INTER>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, width, lds);
-    case 8: return launch_rw<T, 8, INTER>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, width, lds);
-    default: return launch_rw<T, 4, INTER>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, width, lds);
+    case 64: GTS_LAUNCH(64);
+    case 32: GTS_LAUNCH(32);
+    case 16: GTS_LAUNCH(16);
+    case 8: GTS_LAUNCH(8);
+    default: GTS_LAUNCH(4);
   }
+#undef GTS_LAUNCH
 }
 
 gts_status entry(const gts_model* model, const void* d_model, const float* d_X, int64_t rows,

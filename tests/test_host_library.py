@@ -151,26 +151,34 @@ def test_pack_invariants_all_algorithms(alg):
 
 
 def test_model_layout_roundtrip():
+    """The blob holds the packed elements in bin order (roots carry the leaf
+    value in their zero-fraction slot), bin offsets and per-group bin ranges."""
     w = synth.workload("wide")
     el, npaths, bias = gts.extract_paths(w.ensemble)
     packed, offs = gts.pack_paths(el, 64, "bfd")
+    roots = packed["feature_idx"] == -1
     for dtype, ft in (("f32", np.float32), ("f64", np.float64)):
         desc, blob = gts.model_layout(packed, offs, 784, 10, bias, dtype)
         assert desc.num_paths == npaths and desc.num_bins == len(offs) - 1
-        assert desc.bytes == len(blob) and all(o % 256 == 0 for o in desc.off[:11])
-        feat = np.frombuffer(blob, np.int32, len(packed), desc.off[0])
+        assert desc.bytes == len(blob) and all(o % 256 == 0 for o in desc.off[:7])
+        assert desc.max_path_len == 9
+        n = len(packed)
+        feat = np.frombuffer(blob, np.int32, n, desc.off[0])
         assert np.array_equal(feat, packed["feature_idx"])
-        z = np.frombuffer(blob, ft, len(packed), desc.off[3])
-        assert np.array_equal(z, packed["zero_fraction"].astype(ft))
-        first = np.frombuffer(blob, np.int32, npaths, desc.off[4])
-        plen = np.frombuffer(blob, np.int32, npaths, desc.off[5])
-        gp = np.frombuffer(blob, np.int32, 11, desc.off[7])
-        assert gp[0] == 0 and gp[-1] == npaths
+        lo = np.frombuffer(blob, np.float32, n, desc.off[1])
+        hi = np.frombuffer(blob, np.float32, n, desc.off[2])
+        assert np.array_equal(lo, packed["lower"]) and np.array_equal(hi, packed["upper"])
+        z = np.frombuffer(blob, ft, n, desc.off[3])
+        want = np.where(roots, packed["v"], packed["zero_fraction"]).astype(ft)
+        assert np.array_equal(z, want)
+        bstart = np.frombuffer(blob, np.int32, len(offs), desc.off[4])
+        assert np.array_equal(bstart, offs)
+        gb = np.frombuffer(blob, np.int32, 11, desc.off[5])
+        assert gb[0] == 0 and gb[-1] == len(offs) - 1
         for g in range(10):
-            seg = plen[gp[g]:gp[g + 1]]
-            assert np.all(np.diff(seg) <= 0)             # non-increasing length
-            assert np.all(packed["group"][first[gp[g]:gp[g + 1]]] == g)
-        assert sorted(first.tolist()) == np.flatnonzero(packed["feature_idx"] == -1).tolist()
+            seg = packed[offs[gb[g]]:offs[gb[g + 1]]]
+            assert np.all(seg["group"] == g)
+        assert np.array_equal(np.frombuffer(blob, ft, 10, desc.off[6]), bias.astype(ft))
 
 
 # ----------------------------------------------------------------------------
