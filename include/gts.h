@@ -7,6 +7,7 @@
  *   gts_extract_paths   host   ensemble -> merged unique root-to-leaf paths
  *   gts_pack_paths      host   paths -> bins of <= 64 path elements
  *   gts_model_layout    host   packed paths -> one device-ready byte blob
+ *   gts_prepare_model   host   the three steps above in one pass
  *   gts_shap            device SHAP values              phi[rows][G][M+1]
  *   gts_shap_interactions device SHAP interaction values phi[rows][G][M+1][M+1]
  *
@@ -174,7 +175,9 @@ gts_status gts_pack_paths(const gts_path_element *elems, int64_t num_elements,
  * dtype     GTS_F32 or GTS_F64: precision of zero fractions, leaf values and
  *           of the whole SHAP recurrence and accumulation.
  * model     (out) descriptor; model->bytes is the blob size.
- * host_blob host buffer of blob_capacity bytes, or NULL to size only.
+ * host_blob host buffer of blob_capacity bytes, or NULL to size only (the
+ *           input is then only counted; it is validated when the blob is
+ *           written).
  * Errors: GTS_EINVAL for inconsistent input, GTS_EPATHLEN for a path longer
  * than 64, GTS_EBUFSIZE if blob_capacity < model->bytes.
  */
@@ -183,6 +186,24 @@ gts_status gts_model_layout(const gts_path_element *packed, int64_t num_elements
                             int32_t num_features, int32_t num_groups,
                             const double *bias, int32_t dtype, gts_model *model,
                             void *host_blob, int64_t blob_capacity);
+
+/*
+ * gts_prepare_model -- Sections 3.1-3.3 in one host pass: extract and merge
+ * the paths of `ens`, pack them (bin_capacity, alg as gts_pack_paths) and
+ * write the device blob, without materialising the intermediate
+ * path-element lists; trees are walked on several host threads.  The blob
+ * and descriptor are byte for byte those of
+ * gts_model_layout(gts_pack_paths(gts_extract_paths(ens))).
+ *
+ * host_blob host buffer of blob_capacity bytes, or NULL to size only (then
+ *           model->bytes gives the size).  bias (out, may be NULL) double[G].
+ * Errors: as gts_extract_paths for a malformed ensemble; GTS_EPATHLEN if a
+ * merged path is longer than bin_capacity; GTS_EBUFSIZE if blob_capacity <
+ * model->bytes (model is written).
+ */
+gts_status gts_prepare_model(const gts_ensemble *ens, int32_t bin_capacity, int32_t alg,
+                             int32_t dtype, gts_model *model, void *host_blob,
+                             int64_t blob_capacity, double *bias);
 
 /*
  * gts_shap -- SHAP values, Eq. (2), by the per-path permutation-weight

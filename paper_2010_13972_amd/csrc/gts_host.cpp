@@ -3,6 +3,7 @@
 // layout.  Compiled without floating-point contraction so that the extracted
 // zero fractions and the bias are reproducible bit for bit.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -10,6 +11,7 @@
 #include <functional>
 #include <limits>
 #include <new>
+#include <thread>
 #include <vector>
 
 #include "gts_internal.h"
@@ -42,6 +44,10 @@ gts_status check_model(const gts_model* m) {
 }
 
 namespace {
+
+// ---------------------------------------------------------------------------
+// path extraction
+// ---------------------------------------------------------------------------
 
 // One split on the way from the root to a leaf.
 struct Split {
@@ -80,57 +86,133 @@ gts_status validate_ensemble(const gts_ensemble* e) {
   return GTS_OK;
 }
 
-// Depth-first walk of one tree (left child first).  Calls leaf(node, splits,
-// count) at every leaf.  Rejects bad children, revisits and bad node data.
-template <typename LeafFn>
-gts_status walk_tree(const gts_ensemble* e, int64_t t, std::vector<Split>& path,
-                     std::vector<unsigned char>& seen, LeafFn&& leaf) {
-  const int64_t base = e->tree_node_offsets[t];
-  const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
-  seen.assign((size_t)n, 0);
-  struct Frame { int32_t node; int32_t depth; Split into; };
+// Reusable per-thread buffers for walking trees.
+struct Walker {
+  struct Frame {
+    int32_t node;
+    int32_t depth;
+    Split into;  // the split that leads to `node`
+  };
   std::vector<Frame> stack;
-  stack.push_back(Frame{0, 0, Split{}});
-  while (!stack.empty()) {
-    const Frame fr = stack.back();
-    stack.pop_back();
-    const int32_t node = fr.node;
-    if (seen[(size_t)node])
-      return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
-                  (long long)t, node);
-    seen[(size_t)node] = 1;
-    path.resize((size_t)fr.depth);
-    if (fr.depth > 0) path[(size_t)fr.depth - 1] = fr.into;
-    const int64_t gi = base + node;
-    const double r = e->cover[gi];
-    if (!(r >= 0.0) || !std::isfinite(r))
-      return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
-                  (long long)t, node);
-    const int32_t a = e->left[gi], b = e->right[gi];
-    if (a < 0 && b < 0) {
-      if (!std::isfinite(e->value[gi]))
-        return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
-      gts_status st = leaf(node, path);
-      if (st != GTS_OK) return st;
-      continue;
+  std::vector<Split> path;    // splits from the root to the current node
+  std::vector<Split> merged;  // the current leaf's merged elements
+  std::vector<unsigned char> seen;
+
+  // Section 3.2: order the leaf's splits by feature (insertion sort is stable,
+  // so repeats stay in root-to-leaf order), then fold repeats into one
+  // element: intersect the ranges, multiply the zero fractions.
+  size_t merge(size_t depth) {
+    merged.resize(depth);
+    Split* s = merged.data();
+    for (size_t i = 0; i < depth; ++i) {
+      const Split key = path[i];
+      size_t j = i;
+      while (j > 0 && s[j - 1].feature > key.feature) {
+        s[j] = s[j - 1];
+        --j;
+      }
+      s[j] = key;
     }
-    if (a < 0 || b < 0 || a >= n || b >= n)
-      return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
-                  node);
-    const int32_t d = e->feature[gi];
-    if (d < 0 || d >= e->num_features)
-      return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)", (long long)t,
-                  node, d, e->num_features);
-    const float th = e->threshold[gi];
-    if (std::isnan(th))
-      return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
-    const double ra = e->cover[base + a], rb = e->cover[base + b];
-    const float inf = std::numeric_limits<float>::infinity();
-    // right child pushed first so the left child (x < t) is visited first
-    stack.push_back(Frame{b, fr.depth + 1, Split{d, th, inf, cover_ratio(rb, r)}});
-    stack.push_back(Frame{a, fr.depth + 1, Split{d, -inf, th, cover_ratio(ra, r)}});
+    size_t m = 0;
+    for (size_t i = 0; i < depth; ++i) {
+      if (m > 0 && s[m - 1].feature == s[i].feature) {
+        Split& acc = s[m - 1];
+        if (s[i].lower > acc.lower) acc.lower = s[i].lower;
+        if (s[i].upper < acc.upper) acc.upper = s[i].upper;
+        acc.zero_fraction = acc.zero_fraction * s[i].zero_fraction;
+      } else {
+        s[m] = s[i];
+        s[m].zero_fraction = 1.0 * s[i].zero_fraction;
+        ++m;
+      }
+    }
+    return m;
   }
-  return GTS_OK;
+
+  // Depth-first walk of tree t, left child (x < t) first.  Calls
+  // leaf(node, m) with `merged[0..m)` holding the leaf's merged elements.
+  template <typename LeafFn>
+  gts_status walk(const gts_ensemble* e, int64_t t, LeafFn&& leaf) {
+    const int64_t base = e->tree_node_offsets[t];
+    const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
+    seen.assign((size_t)n, 0);
+    stack.clear();
+    stack.push_back(Frame{0, 0, Split{}});
+    const float inf = std::numeric_limits<float>::infinity();
+    while (!stack.empty()) {
+      const Frame fr = stack.back();
+      stack.pop_back();
+      const int32_t node = fr.node;
+      if (seen[(size_t)node])
+        return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
+                    (long long)t, node);
+      seen[(size_t)node] = 1;
+      if (path.size() < (size_t)fr.depth) path.resize((size_t)fr.depth);
+      if (fr.depth > 0) path[(size_t)fr.depth - 1] = fr.into;
+      const int64_t gi = base + node;
+      const double r = e->cover[gi];
+      if (!(r >= 0.0) || !std::isfinite(r))
+        return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
+                    (long long)t, node);
+      const int32_t a = e->left[gi], b = e->right[gi];
+      if (a < 0 && b < 0) {
+        if (!std::isfinite(e->value[gi]))
+          return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
+        leaf(node, merge((size_t)fr.depth));
+        continue;
+      }
+      if (a < 0 || b < 0 || a >= n || b >= n)
+        return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
+                    node);
+      const int32_t d = e->feature[gi];
+      if (d < 0 || d >= e->num_features)
+        return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)", (long long)t,
+                    node, d, e->num_features);
+      const float th = e->threshold[gi];
+      if (std::isnan(th))
+        return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
+      const double ra = e->cover[base + a], rb = e->cover[base + b];
+      // the right child is pushed first so that the left child is visited first
+      stack.push_back(Frame{b, fr.depth + 1, Split{d, th, inf, cover_ratio(rb, r)}});
+      stack.push_back(Frame{a, fr.depth + 1, Split{d, -inf, th, cover_ratio(ra, r)}});
+    }
+    return GTS_OK;
+  }
+};
+
+// Runs fn(t, walker) for every tree on up to `threads` threads (dynamic
+// chunks of trees); returns the per-tree statuses.
+template <typename Fn>
+void for_each_tree(int64_t T, int threads, std::vector<gts_status>& status, Fn&& fn) {
+  status.assign((size_t)T, GTS_OK);
+  if (threads <= 1) {
+    Walker w;
+    for (int64_t t = 0; t < T; ++t) status[(size_t)t] = fn(t, w);
+    return;
+  }
+  std::atomic<int64_t> next{0};
+  constexpr int64_t kChunk = 8;
+  auto worker = [&]() {
+    Walker w;
+    for (;;) {
+      const int64_t a = next.fetch_add(kChunk);
+      if (a >= T) break;
+      const int64_t b = std::min(T, a + kChunk);
+      for (int64_t t = a; t < b; ++t) status[(size_t)t] = fn(t, w);
+    }
+  };
+  std::vector<std::thread> pool;
+  pool.reserve((size_t)threads - 1);
+  for (int i = 1; i < threads; ++i) pool.emplace_back(worker);
+  worker();
+  for (auto& th : pool) th.join();
+}
+
+int host_threads(int64_t work_items) {
+  unsigned hw = std::thread::hardware_concurrency();
+  if (hw == 0) hw = 1;
+  const int64_t by_work = (work_items + 31) / 32;  // at least ~32 trees per thread
+  return (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)hw, 16, by_work}));
 }
 
 }  // namespace
@@ -155,71 +237,88 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
   gts_status st = validate_ensemble(ens);
   if (st != GTS_OK) return st;
   try {
-    if (bias)
-      for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = 0.0;
-    int64_t n = 0, paths = 0;
-    std::vector<Split> path, sorted;
-    std::vector<unsigned char> seen;
-    for (int64_t t = 0; t < ens->num_trees; ++t) {
-      const int64_t base = ens->tree_node_offsets[t];
-      const int32_t group = ens->tree_group[t];
-      st = walk_tree(ens, t, path, seen, [&](int32_t leaf, const std::vector<Split>& sp) {
-        const double v = ens->value[base + leaf];
-        // Section 3.2: order by feature (stable: repeats stay root-to-leaf),
-        // then combine consecutive repeats into one element.
-        sorted.assign(sp.begin(), sp.end());
-        std::stable_sort(sorted.begin(), sorted.end(),
-                         [](const Split& x, const Split& y) { return x.feature < y.feature; });
-        size_t m = 0;
-        for (size_t i = 0; i < sorted.size(); ++i) {
-          if (m > 0 && sorted[m - 1].feature == sorted[i].feature) {
-            Split& acc = sorted[m - 1];
-            if (sorted[i].lower > acc.lower) acc.lower = sorted[i].lower;
-            if (sorted[i].upper < acc.upper) acc.upper = sorted[i].upper;
-            acc.zero_fraction = acc.zero_fraction * sorted[i].zero_fraction;
-          } else {
-            sorted[m] = sorted[i];
-            sorted[m].zero_fraction = 1.0 * sorted[i].zero_fraction;
-            ++m;
-          }
-        }
-        sorted.resize(m);
-        if (bias) {
-          double prod = 1.0;
-          for (size_t i = 0; i < m; ++i) prod = prod * sorted[i].zero_fraction;
-          bias[group] += v * prod;
-        }
-        const float inf = std::numeric_limits<float>::infinity();
-        for (size_t i = 0; i <= m; ++i) {
-          if (n < capacity) {
-            gts_path_element& el = out[n];
-            el.path_idx = paths;
-            el.group = group;
-            el.v = v;
-            if (i == 0) {
-              el.feature_idx = -1;
-              el.lower = -inf;
-              el.upper = inf;
-              el.zero_fraction = 1.0;
-            } else {
-              el.feature_idx = sorted[i - 1].feature;
-              el.lower = sorted[i - 1].lower;
-              el.upper = sorted[i - 1].upper;
-              el.zero_fraction = sorted[i - 1].zero_fraction;
-            }
-          }
-          ++n;
-        }
-        ++paths;
-        return GTS_OK;
+    const int64_t T = ens->num_trees;
+    const int threads = host_threads(T);
+    // pass 1: elements and paths per tree
+    std::vector<int64_t> tree_elems((size_t)T + 1, 0), tree_paths((size_t)T + 1, 0);
+    std::vector<gts_status> status;
+    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+      int64_t ne = 0, np = 0;
+      gts_status s = w.walk(ens, t, [&](int32_t, size_t m) {
+        ne += (int64_t)m + 1;
+        ++np;
       });
-      if (st != GTS_OK) return st;
+      tree_elems[(size_t)t + 1] = ne;
+      tree_paths[(size_t)t + 1] = np;
+      return s;
+    });
+    for (int64_t t = 0; t < T; ++t) {
+      if (status[(size_t)t] != GTS_OK) {
+        // re-walk the first bad tree here so the message is this thread's
+        Walker w;
+        return w.walk(ens, t, [](int32_t, size_t) {});
+      }
     }
+    for (int64_t t = 0; t < T; ++t) {
+      tree_elems[(size_t)t + 1] += tree_elems[(size_t)t];
+      tree_paths[(size_t)t + 1] += tree_paths[(size_t)t];
+    }
+    const int64_t n = tree_elems[(size_t)T], paths = tree_paths[(size_t)T];
     *num_elements = n;
     *num_paths = paths;
-    if (n > capacity && out != nullptr)
+    if (bias)
+      for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = 0.0;
+    if (out == nullptr && bias == nullptr) return GTS_OK;
+    if (out != nullptr && n > capacity)
       return fail(GTS_EBUFSIZE, "capacity %lld < %lld elements", (long long)capacity,
                   (long long)n);
+    // pass 2: write the elements; keep each path's bias term v * prod(z)
+    std::vector<double> term(bias ? (size_t)paths : 0);
+    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+      const int64_t base = ens->tree_node_offsets[t];
+      const int32_t group = ens->tree_group[t];
+      int64_t k = tree_elems[(size_t)t];
+      int64_t p = tree_paths[(size_t)t];
+      const float inf = std::numeric_limits<float>::infinity();
+      return w.walk(ens, t, [&](int32_t leaf, size_t m) {
+        const double v = ens->value[base + leaf];
+        if (bias) {
+          double prod = 1.0;
+          for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
+          term[(size_t)p] = v * prod;
+        }
+        if (out) {
+          gts_path_element* el = out + k;
+          el[0].path_idx = p;
+          el[0].feature_idx = -1;
+          el[0].group = group;
+          el[0].lower = -inf;
+          el[0].upper = inf;
+          el[0].zero_fraction = 1.0;
+          el[0].v = v;
+          for (size_t i = 0; i < m; ++i) {
+            const Split& s = w.merged[i];
+            el[i + 1].path_idx = p;
+            el[i + 1].feature_idx = s.feature;
+            el[i + 1].group = group;
+            el[i + 1].lower = s.lower;
+            el[i + 1].upper = s.upper;
+            el[i + 1].zero_fraction = s.zero_fraction;
+            el[i + 1].v = v;
+          }
+        }
+        k += (int64_t)m + 1;
+        ++p;
+      });
+    });
+    if (bias) {
+      // sum in path order, like a single pass over the ensemble would
+      int64_t p = 0;
+      for (int64_t t = 0; t < T; ++t) {
+        const int32_t g = ens->tree_group[t];
+        for (; p < tree_paths[(size_t)t + 1]; ++p) bias[g] += term[(size_t)p];
+      }
+    }
     return GTS_OK;
   } catch (const std::bad_alloc&) {
     return fail(GTS_ENOMEM, "host allocation failed");
@@ -230,6 +329,10 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
 
 namespace gts {
 namespace {
+
+// ---------------------------------------------------------------------------
+// bin packing
+// ---------------------------------------------------------------------------
 
 struct PathRef {
   int64_t first;  // element index of the root
@@ -245,31 +348,31 @@ gts_status parse_paths(const gts_path_element* el, int64_t n, std::vector<PathRe
   if (el == nullptr) return fail(GTS_EINVAL, "elements pointer is NULL");
   if (el[0].feature_idx != -1)
     return fail(GTS_EINVAL, "element 0 is not a root element (feature_idx -1)");
+  int64_t first = 0;
   for (int64_t i = 0; i < n; ++i) {
     const gts_path_element& e = el[i];
     if (e.feature_idx == -1) {
-      if (!paths.empty() && paths.back().size > max_len)
-        return fail(GTS_EPATHLEN, "path at element %lld has length %d > %d",
-                    (long long)paths.back().first, paths.back().size, max_len);
-      paths.push_back(PathRef{i, 1, e.group});
+      if (i > 0)
+        paths.push_back(PathRef{first, (int32_t)std::min<int64_t>(i - first, INT32_MAX), el[first].group});
+      first = i;
       if (num_groups > 0 && (e.group < 0 || e.group >= num_groups))
         return fail(GTS_EINVAL, "element %lld: group %d outside [0, %d)", (long long)i,
                     e.group, num_groups);
       continue;
     }
-    PathRef& p = paths.back();
-    const gts_path_element& root = el[p.first];
+    const gts_path_element& root = el[first];
     if (e.feature_idx < -1 || (num_features > 0 && e.feature_idx >= num_features))
       return fail(GTS_EINVAL, "element %lld: feature %d out of range", (long long)i,
                   e.feature_idx);
     if (e.path_idx != root.path_idx || e.group != root.group)
       return fail(GTS_EINVAL, "element %lld does not belong to the path started at %lld",
-                  (long long)i, (long long)p.first);
-    ++p.size;
+                  (long long)i, (long long)first);
   }
-  if (paths.back().size > max_len)
-    return fail(GTS_EPATHLEN, "path at element %lld has length %d > %d",
-                (long long)paths.back().first, paths.back().size, max_len);
+  paths.push_back(PathRef{first, (int32_t)std::min<int64_t>(n - first, INT32_MAX), el[first].group});
+  for (const PathRef& p : paths)
+    if (p.size > max_len)
+      return fail(GTS_EPATHLEN, "path at element %lld has length %d > %d", (long long)p.first,
+                  p.size, max_len);
   return GTS_OK;
 }
 
@@ -307,6 +410,203 @@ struct FirstFitTree {
   }
 };
 
+// The outcome of packing: bin of every path, the placement order, the first
+// element of every path in the packed sequence and the bins' element ranges.
+struct Packing {
+  std::vector<int64_t> order;        // paths in placement order
+  std::vector<int64_t> bin_of;       // per path
+  std::vector<int64_t> dest;         // per path: packed element offset
+  std::vector<int64_t> bin_offsets;  // [K+1]
+  std::vector<int32_t> bin_group;    // [K]
+  int64_t K = 0;
+};
+
+// Section 3.3 on paths given by size and group (path order = input order).
+// Processing order: by group; then (BFD, FFD) non-increasing size; ties by
+// position -- a counting sort over (group rank, size) keys.
+void assign_bins(const int32_t* size, const int32_t* group, int64_t P, int32_t cap, int32_t alg,
+                 Packing& pk, bool layout) {
+  const bool decreasing = (alg == GTS_PACK_BFD || alg == GTS_PACK_FFD);
+  std::vector<int32_t> groups;
+  groups.reserve(16);
+  for (int64_t i = 0; i < P; ++i)
+    if (groups.empty() || groups.back() != group[i]) groups.push_back(group[i]);
+  std::sort(groups.begin(), groups.end());
+  groups.erase(std::unique(groups.begin(), groups.end()), groups.end());
+  const int64_t nsize = decreasing ? (int64_t)cap + 1 : 1;
+  std::vector<int64_t> count(groups.size() * (size_t)nsize + 1, 0);
+  std::vector<int32_t> key((size_t)P);
+  for (int64_t i = 0; i < P; ++i) {
+    const int64_t g = std::lower_bound(groups.begin(), groups.end(), group[i]) - groups.begin();
+    key[(size_t)i] = (int32_t)(g * nsize + (decreasing ? cap - size[i] : 0));
+    ++count[(size_t)key[(size_t)i] + 1];
+  }
+  for (size_t k = 1; k < count.size(); ++k) count[k] += count[k - 1];
+  std::vector<int64_t>& order = pk.order;
+  order.resize((size_t)P);
+  for (int64_t i = 0; i < P; ++i) order[(size_t)count[(size_t)key[(size_t)i]]++] = i;
+
+  std::vector<int64_t>& bin_of = pk.bin_of;
+  bin_of.resize((size_t)P);
+  std::vector<int32_t> resid;
+  std::vector<BinHeap> by_resid((size_t)cap + 1);
+  int64_t K = 0;
+  size_t i = 0;
+  while (i < order.size()) {
+    const int32_t g = group[order[i]];
+    size_t j = i;
+    while (j < order.size() && group[order[j]] == g) ++j;
+    const int64_t first_bin = K;
+    if (alg == GTS_PACK_BFD) {
+      for (BinHeap& h : by_resid) h.clear();
+      for (size_t k = i; k < j; ++k) {
+        const int32_t s = size[order[k]];
+        int64_t b = -1;
+        int32_t r = s;
+        for (; r <= cap; ++r)
+          if (!by_resid[(size_t)r].empty()) {
+            b = heap_pop(by_resid[(size_t)r]);
+            break;
+          }
+        if (b < 0) {
+          b = K++;
+          r = cap;
+        }
+        const int32_t left = r - s;
+        if (left > 0) heap_push(by_resid[(size_t)left], b);
+        bin_of[(size_t)order[k]] = b;
+      }
+    } else if (alg == GTS_PACK_FFD) {
+      FirstFitTree tree((int64_t)(j - i));
+      int64_t opened = 0;
+      resid.assign((size_t)(j - i), 0);
+      for (size_t k = i; k < j; ++k) {
+        const int32_t s = size[order[k]];
+        int64_t local = tree.leftmost_at_least(s);
+        if (local < 0) {
+          local = opened++;
+          resid[(size_t)local] = cap;
+        }
+        resid[(size_t)local] -= s;
+        tree.set(local, resid[(size_t)local]);
+        bin_of[(size_t)order[k]] = first_bin + local;
+      }
+      K = first_bin + opened;
+    } else if (alg == GTS_PACK_NF) {
+      int32_t r = 0;
+      for (size_t k = i; k < j; ++k) {
+        const int32_t s = size[order[k]];
+        if (K == first_bin || r < s) {
+          ++K;
+          r = cap;
+        }
+        r -= s;
+        bin_of[(size_t)order[k]] = K - 1;
+      }
+    } else {
+      for (size_t k = i; k < j; ++k) bin_of[(size_t)order[k]] = K++;
+    }
+    i = j;
+  }
+  pk.K = K;
+  if (!layout) return;
+  // bins in order; inside a bin, paths in placement order
+  std::vector<int64_t>& off = pk.bin_offsets;
+  off.assign((size_t)K + 1, 0);
+  pk.bin_group.assign((size_t)K, 0);
+  for (int64_t p = 0; p < P; ++p) {
+    off[(size_t)bin_of[(size_t)p] + 1] += size[p];
+    pk.bin_group[(size_t)bin_of[(size_t)p]] = group[p];
+  }
+  for (int64_t b = 0; b < K; ++b) off[(size_t)b + 1] += off[(size_t)b];
+  std::vector<int64_t> cursor(off.begin(), off.end() - 1);
+  pk.dest.resize((size_t)P);
+  for (size_t k = 0; k < order.size(); ++k) {
+    const int64_t p = order[k];
+    const int64_t b = bin_of[(size_t)p];
+    pk.dest[(size_t)p] = cursor[(size_t)b];
+    cursor[(size_t)b] += size[p];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// device layout
+// ---------------------------------------------------------------------------
+
+struct BlobPlan {
+  gts_model m;
+  int64_t sizes[kBlobArrays];
+};
+
+BlobPlan plan_blob(int64_t n, int64_t P, int64_t K, int32_t M, int32_t G, int32_t dtype,
+                   int32_t maxlen) {
+  BlobPlan bp;
+  const size_t ts = dtype == GTS_F64 ? sizeof(double) : sizeof(float);
+  bp.sizes[kFeat] = 4 * n;
+  bp.sizes[kLower] = 4 * n;
+  bp.sizes[kUpper] = 4 * n;
+  bp.sizes[kZero] = (int64_t)ts * n;
+  bp.sizes[kBinStart] = 4 * (K + 1);
+  bp.sizes[kGroupBins] = 4 * ((int64_t)G + 1);
+  bp.sizes[kBias] = (int64_t)ts * G;
+  gts_model& m = bp.m;
+  std::memset(&m, 0, sizeof(m));
+  m.magic = kModelMagic;
+  m.dtype = dtype;
+  m.num_features = M;
+  m.num_groups = G;
+  m.num_elements = n;
+  m.num_paths = P;
+  m.num_bins = K;
+  m.max_path_len = std::min<int32_t>(maxlen, kMaxPathLen + 1);
+  int64_t cur = 0;
+  for (int k = 0; k < kBlobArrays; ++k) {
+    m.off[k] = cur;
+    cur += (bp.sizes[k] + kBlobAlign - 1) / kBlobAlign * kBlobAlign;
+  }
+  m.bytes = cur > 0 ? cur : kBlobAlign;
+  return bp;
+}
+
+// Zero the alignment padding after each array (the arrays themselves are
+// written in full), so equal models give byte-identical blobs.
+void zero_padding(const BlobPlan& bp, char* blob) {
+  for (int k = 0; k < kBlobArrays; ++k) {
+    const int64_t a = bp.m.off[k] + bp.sizes[k];
+    const int64_t b = (k + 1 < kBlobArrays) ? bp.m.off[k + 1] : bp.m.bytes;
+    if (b > a) std::memset(blob + a, 0, (size_t)(b - a));
+  }
+}
+
+// The parts of the blob that depend only on the packing and the bias.
+void write_bins_and_bias(const BlobPlan& bp, char* blob, const int64_t* bin_offsets,
+                         const int32_t* bin_group, const double* bias) {
+  const gts_model& m = bp.m;
+  int32_t* bstart = reinterpret_cast<int32_t*>(blob + m.off[kBinStart]);
+  int32_t* gbins = reinterpret_cast<int32_t*>(blob + m.off[kGroupBins]);
+  for (int64_t b = 0; b <= m.num_bins; ++b) bstart[b] = (int32_t)bin_offsets[b];
+  for (int64_t g = 0; g <= m.num_groups; ++g) gbins[g] = 0;
+  for (int64_t b = 0; b < m.num_bins; ++b) gbins[bin_group[b] + 1] += 1;
+  for (int64_t g = 0; g < m.num_groups; ++g) gbins[g + 1] += gbins[g];
+  if (m.dtype == GTS_F64) {
+    double* bb = reinterpret_cast<double*>(blob + m.off[kBias]);
+    for (int64_t g = 0; g < m.num_groups; ++g) bb[g] = bias[g];
+  } else {
+    float* bb = reinterpret_cast<float*>(blob + m.off[kBias]);
+    for (int64_t g = 0; g < m.num_groups; ++g) bb[g] = (float)bias[g];
+  }
+}
+
+// One element of the blob: the root's zero-fraction slot holds v.
+inline void put_element(const gts_model& m, char* blob, int64_t i, int32_t feat, float lo,
+                        float hi, double z_or_v) {
+  reinterpret_cast<int32_t*>(blob + m.off[kFeat])[i] = feat;
+  reinterpret_cast<float*>(blob + m.off[kLower])[i] = lo;
+  reinterpret_cast<float*>(blob + m.off[kUpper])[i] = hi;
+  if (m.dtype == GTS_F64) reinterpret_cast<double*>(blob + m.off[kZero])[i] = z_or_v;
+  else reinterpret_cast<float*>(blob + m.off[kZero])[i] = (float)z_or_v;
+}
+
 }  // namespace
 }  // namespace gts
 
@@ -330,91 +630,23 @@ extern "C" gts_status gts_pack_paths(const gts_path_element* elems, int64_t num_
     gts_status st = parse_paths(elems, num_elements, paths, bin_capacity, 0, 0);
     if (st != GTS_OK) return st;
     const int64_t P = (int64_t)paths.size();
-    // processing order: by group, then per algorithm
-    std::vector<int64_t> order((size_t)P);
-    for (int64_t i = 0; i < P; ++i) order[(size_t)i] = i;
-    const bool decreasing = (alg == GTS_PACK_BFD || alg == GTS_PACK_FFD);
-    std::stable_sort(order.begin(), order.end(), [&](int64_t a, int64_t b) {
-      const PathRef &x = paths[(size_t)a], &y = paths[(size_t)b];
-      if (x.group != y.group) return x.group < y.group;
-      if (decreasing && x.size != y.size) return x.size > y.size;
-      return a < b;
-    });
-    std::vector<int64_t> bin_of((size_t)P);
-    std::vector<int32_t> resid;
-    int64_t K = 0;
-    size_t i = 0;
-    while (i < order.size()) {
-      const int32_t g = paths[(size_t)order[i]].group;
-      size_t j = i;
-      while (j < order.size() && paths[(size_t)order[j]].group == g) ++j;
-      const int64_t first_bin = K;
-      if (alg == GTS_PACK_BFD) {
-        std::vector<BinHeap> by_resid((size_t)bin_capacity + 1);
-        for (size_t k = i; k < j; ++k) {
-          const int32_t s = paths[(size_t)order[k]].size;
-          int64_t b = -1;
-          int32_t r = s;
-          for (; r <= bin_capacity; ++r)
-            if (!by_resid[(size_t)r].empty()) { b = heap_pop(by_resid[(size_t)r]); break; }
-          if (b < 0) {
-            b = K++;
-            r = bin_capacity;
-          }
-          const int32_t left = r - s;
-          if (left > 0) heap_push(by_resid[(size_t)left], b);
-          bin_of[(size_t)order[k]] = b;
-        }
-      } else if (alg == GTS_PACK_FFD) {
-        FirstFitTree tree((int64_t)(j - i));
-        int64_t opened = 0;
-        for (size_t k = i; k < j; ++k) {
-          const int32_t s = paths[(size_t)order[k]].size;
-          int64_t local = tree.leftmost_at_least(s);
-          if (local < 0) {
-            local = opened++;
-            resid.resize((size_t)(first_bin + opened));
-            resid[(size_t)(first_bin + local)] = bin_capacity;
-          }
-          const int64_t b = first_bin + local;
-          resid[(size_t)b] -= s;
-          tree.set(local, resid[(size_t)b]);
-          bin_of[(size_t)order[k]] = b;
-        }
-        K = first_bin + opened;
-      } else if (alg == GTS_PACK_NF) {
-        int32_t r = 0;
-        for (size_t k = i; k < j; ++k) {
-          const int32_t s = paths[(size_t)order[k]].size;
-          if (K == first_bin || r < s) {
-            ++K;
-            r = bin_capacity;
-          }
-          r -= s;
-          bin_of[(size_t)order[k]] = K - 1;
-        }
-      } else {
-        for (size_t k = i; k < j; ++k) bin_of[(size_t)order[k]] = K++;
-      }
-      i = j;
+    std::vector<int32_t> size((size_t)P), group((size_t)P);
+    for (int64_t p = 0; p < P; ++p) {
+      size[(size_t)p] = paths[(size_t)p].size;
+      group[(size_t)p] = paths[(size_t)p].group;
     }
-    *num_bins = K;
-    if (offsets_capacity == 0) return GTS_OK;
-    if (offsets_capacity < K + 1)
+    Packing pk;
+    const bool want = offsets_capacity > 0;
+    assign_bins(size.data(), group.data(), P, bin_capacity, alg, pk, want);
+    *num_bins = pk.K;
+    if (!want) return GTS_OK;
+    if (offsets_capacity < pk.K + 1)
       return fail(GTS_EBUFSIZE, "offsets_capacity %lld < num_bins + 1 = %lld",
-                  (long long)offsets_capacity, (long long)(K + 1));
-    // lay bins out in order; inside a bin, paths in placement order
-    std::vector<int64_t> count((size_t)K + 1, 0);
-    for (int64_t p = 0; p < P; ++p) count[(size_t)bin_of[(size_t)p] + 1] += paths[(size_t)p].size;
-    for (int64_t b = 0; b < K; ++b) count[(size_t)b + 1] += count[(size_t)b];
-    for (int64_t b = 0; b <= K; ++b) bin_offsets[b] = count[(size_t)b];
-    std::vector<int64_t> cursor(count.begin(), count.end() - 1);
-    for (size_t k = 0; k < order.size(); ++k) {
-      const PathRef& p = paths[(size_t)order[k]];
-      const int64_t b = bin_of[(size_t)order[k]];
-      std::memcpy(packed + cursor[(size_t)b], elems + p.first, sizeof(gts_path_element) * (size_t)p.size);
-      cursor[(size_t)b] += p.size;
-    }
+                  (long long)offsets_capacity, (long long)(pk.K + 1));
+    for (int64_t b = 0; b <= pk.K; ++b) bin_offsets[b] = pk.bin_offsets[(size_t)b];
+    for (int64_t p = 0; p < P; ++p)
+      std::memcpy(packed + pk.dest[(size_t)p], elems + paths[(size_t)p].first,
+                  sizeof(gts_path_element) * (size_t)paths[(size_t)p].size);
     return GTS_OK;
   } catch (const std::bad_alloc&) {
     return fail(GTS_ENOMEM, "host allocation failed");
@@ -436,15 +668,36 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
     return fail(GTS_EINVAL, "too many path elements for 32-bit device indices");
   if (bin_offsets == nullptr) return fail(GTS_EINVAL, "bin_offsets must not be NULL");
   if (bias == nullptr) return fail(GTS_EINVAL, "bias must not be NULL");
+  if (num_elements > 0 && packed == nullptr) return fail(GTS_EINVAL, "packed must not be NULL");
   if (blob_capacity < 0 || (blob_capacity > 0 && host_blob == nullptr))
     return fail(GTS_EINVAL, "bad host_blob / blob_capacity");
   try {
+    // sizes: only counts are needed
+    int64_t P = 0;
+    int32_t maxlen = 0;
+    {
+      int64_t last = -1;
+      for (int64_t i = 0; i < num_elements; ++i) {
+        if (packed[i].feature_idx == -1) {
+          if (last >= 0) maxlen = std::max<int32_t>(maxlen, (int32_t)std::min<int64_t>(i - last, INT32_MAX));
+          last = i;
+          ++P;
+        }
+      }
+      if (last >= 0) maxlen = std::max<int32_t>(maxlen, (int32_t)std::min<int64_t>(num_elements - last, INT32_MAX));
+    }
+    const BlobPlan bp = plan_blob(num_elements, P, num_bins, num_features, num_groups, dtype, maxlen);
+    if (host_blob == nullptr) {
+      *model = bp.m;
+      return GTS_OK;
+    }
+    // full validation before anything is written
     std::vector<PathRef> paths;
     gts_status st = parse_paths(packed, num_elements, paths, kMaxPathLen, num_groups, num_features);
     if (st != GTS_OK) return st;
     if (bin_offsets[0] != 0 || bin_offsets[num_bins] != num_elements)
       return fail(GTS_EINVAL, "bin_offsets must run from 0 to num_elements");
-    // every bin starts on a root element and holds paths of one group
+    // every bin starts on a root element and holds whole paths of one group
     std::vector<int32_t> bin_group((size_t)num_bins);
     {
       size_t p = 0;
@@ -453,82 +706,136 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
         if (e < a || e - a > kMaxPathLen)
           return fail(GTS_EINVAL, "bin %lld spans %lld elements", (long long)b, (long long)(e - a));
         if (a == e) return fail(GTS_EINVAL, "bin %lld is empty", (long long)b);
-        while (p < paths.size() && paths[p].first < a) ++p;
         if (p >= paths.size() || paths[p].first != a)
           return fail(GTS_EINVAL, "bin %lld does not start on a path root", (long long)b);
         bin_group[(size_t)b] = paths[p].group;
-        for (size_t q = p; q < paths.size() && paths[q].first < e; ++q) {
-          if (paths[q].first + paths[q].size > e)
+        for (; p < paths.size() && paths[p].first < e; ++p) {
+          if (paths[p].first + paths[p].size > e)
             return fail(GTS_EINVAL, "a path crosses the end of bin %lld", (long long)b);
-          if (paths[q].group != bin_group[(size_t)b])
+          if (paths[p].group != bin_group[(size_t)b])
             return fail(GTS_EINVAL, "bin %lld mixes output groups", (long long)b);
         }
         if (b > 0 && bin_group[(size_t)b] < bin_group[(size_t)b - 1])
           return fail(GTS_EINVAL, "bins must be ordered by group");
       }
     }
-    const int64_t P = (int64_t)paths.size();
-    const int64_t G = num_groups;
-    const size_t ts = dtype == GTS_F64 ? sizeof(double) : sizeof(float);
-    int64_t sizes[kBlobArrays];
-    sizes[kFeat] = 4 * num_elements;
-    sizes[kLower] = 4 * num_elements;
-    sizes[kUpper] = 4 * num_elements;
-    sizes[kZero] = (int64_t)ts * num_elements;
-    sizes[kBinStart] = 4 * (num_bins + 1);
-    sizes[kGroupBins] = 4 * (G + 1);
-    sizes[kBias] = (int64_t)ts * G;
-    gts_model m;
-    std::memset(&m, 0, sizeof(m));
-    m.magic = kModelMagic;
-    m.dtype = dtype;
-    m.num_features = num_features;
-    m.num_groups = num_groups;
-    m.num_elements = num_elements;
-    m.num_paths = P;
-    m.num_bins = num_bins;
-    int64_t cur = 0;
-    for (int k = 0; k < kBlobArrays; ++k) {
-      m.off[k] = cur;
-      cur += (sizes[k] + kBlobAlign - 1) / kBlobAlign * kBlobAlign;
-    }
-    m.bytes = cur > 0 ? cur : kBlobAlign;
-    int32_t maxlen = 0;
-    for (const PathRef& p : paths) maxlen = std::max(maxlen, p.size);
-    m.max_path_len = maxlen;
-    *model = m;
-    if (host_blob == nullptr) return GTS_OK;
-    if (blob_capacity < m.bytes)
+    *model = bp.m;
+    if (blob_capacity < bp.m.bytes)
       return fail(GTS_EBUFSIZE, "blob_capacity %lld < %lld bytes", (long long)blob_capacity,
-                  (long long)m.bytes);
+                  (long long)bp.m.bytes);
     char* blob = static_cast<char*>(host_blob);
-    std::memset(blob, 0, (size_t)m.bytes);
-    int32_t* feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]);
-    float* lower = reinterpret_cast<float*>(blob + m.off[kLower]);
-    float* upper = reinterpret_cast<float*>(blob + m.off[kUpper]);
+    zero_padding(bp, blob);
     for (int64_t i = 0; i < num_elements; ++i) {
-      feat[i] = packed[i].feature_idx;
-      lower[i] = packed[i].lower;
-      upper[i] = packed[i].upper;
+      const gts_path_element& e = packed[i];
+      put_element(bp.m, blob, i, e.feature_idx, e.lower, e.upper,
+                  e.feature_idx == -1 ? e.v : e.zero_fraction);
     }
-    int32_t* bstart = reinterpret_cast<int32_t*>(blob + m.off[kBinStart]);
-    int32_t* gbins = reinterpret_cast<int32_t*>(blob + m.off[kGroupBins]);
-    for (int64_t b = 0; b <= num_bins; ++b) bstart[b] = (int32_t)bin_offsets[b];
-    for (int64_t g = 0; g <= G; ++g) gbins[g] = 0;
-    for (int64_t b = 0; b < num_bins; ++b) gbins[bin_group[(size_t)b] + 1] += 1;
-    for (int64_t g = 0; g < G; ++g) gbins[g + 1] += gbins[g];
-    if (dtype == GTS_F64) {
-      double* z = reinterpret_cast<double*>(blob + m.off[kZero]);
-      double* bb = reinterpret_cast<double*>(blob + m.off[kBias]);
-      for (int64_t i = 0; i < num_elements; ++i)
-        z[i] = packed[i].feature_idx == -1 ? packed[i].v : packed[i].zero_fraction;
-      for (int64_t g = 0; g < G; ++g) bb[g] = bias[g];
-    } else {
-      float* z = reinterpret_cast<float*>(blob + m.off[kZero]);
-      float* bb = reinterpret_cast<float*>(blob + m.off[kBias]);
-      for (int64_t i = 0; i < num_elements; ++i)
-        z[i] = (float)(packed[i].feature_idx == -1 ? packed[i].v : packed[i].zero_fraction);
-      for (int64_t g = 0; g < G; ++g) bb[g] = (float)bias[g];
+    write_bins_and_bias(bp, blob, bin_offsets, bin_group.data(), bias);
+    return GTS_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(GTS_ENOMEM, "host allocation failed");
+  }
+}
+
+extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_capacity,
+                                        int32_t alg, int32_t dtype, gts_model* model,
+                                        void* host_blob, int64_t blob_capacity, double* bias) {
+  clear_error();
+  if (model == nullptr) return fail(GTS_EINVAL, "model must not be NULL");
+  if (bin_capacity < 1 || bin_capacity > kMaxPathLen)
+    return fail(GTS_EINVAL, "bin_capacity %d outside [1, %d]", bin_capacity, kMaxPathLen);
+  if (alg < GTS_PACK_BFD || alg > GTS_PACK_NONE)
+    return fail(GTS_EINVAL, "unknown packing algorithm %d", alg);
+  if (dtype != GTS_F32 && dtype != GTS_F64) return fail(GTS_EINVAL, "unknown dtype %d", dtype);
+  if (blob_capacity < 0 || (blob_capacity > 0 && host_blob == nullptr))
+    return fail(GTS_EINVAL, "bad host_blob / blob_capacity");
+  gts_status st = validate_ensemble(ens);
+  if (st != GTS_OK) return st;
+  try {
+    const int64_t T = ens->num_trees;
+    const int threads = host_threads(T);
+    // walk 1: the merged length of every path, per tree
+    std::vector<std::vector<int32_t>> tree_sizes((size_t)T);
+    std::vector<gts_status> status;
+    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+      std::vector<int32_t>& sz = tree_sizes[(size_t)t];
+      sz.clear();
+      return w.walk(ens, t, [&](int32_t, size_t m) { sz.push_back((int32_t)m + 1); });
+    });
+    for (int64_t t = 0; t < T; ++t)
+      if (status[(size_t)t] != GTS_OK) {
+        Walker w;
+        return w.walk(ens, t, [](int32_t, size_t) {});
+      }
+    std::vector<int64_t> tree_first((size_t)T + 1, 0);
+    for (int64_t t = 0; t < T; ++t)
+      tree_first[(size_t)t + 1] = tree_first[(size_t)t] + (int64_t)tree_sizes[(size_t)t].size();
+    const int64_t P = tree_first[(size_t)T];
+    std::vector<int32_t> size((size_t)P), group((size_t)P);
+    int64_t n = 0;
+    int32_t maxlen = 0;
+    for (int64_t t = 0; t < T; ++t) {
+      const std::vector<int32_t>& sz = tree_sizes[(size_t)t];
+      for (size_t k = 0; k < sz.size(); ++k) {
+        const int64_t p = tree_first[(size_t)t] + (int64_t)k;
+        size[(size_t)p] = sz[k];
+        group[(size_t)p] = ens->tree_group[t];
+        n += sz[k];
+        maxlen = std::max(maxlen, sz[k]);
+      }
+    }
+    if (maxlen > bin_capacity)
+      return fail(GTS_EPATHLEN, "a merged path has length %d > bin capacity %d", maxlen,
+                  bin_capacity);
+    if (n >= std::numeric_limits<int32_t>::max())
+      return fail(GTS_EINVAL, "too many path elements for 32-bit device indices");
+    // pack on sizes only
+    Packing pk;
+    assign_bins(size.data(), group.data(), P, bin_capacity, alg, pk, true);
+    const BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
+    *model = bp.m;
+    if (host_blob == nullptr && bias == nullptr) return GTS_OK;
+    if (host_blob != nullptr && blob_capacity < bp.m.bytes)
+      return fail(GTS_EBUFSIZE, "blob_capacity %lld < %lld bytes", (long long)blob_capacity,
+                  (long long)bp.m.bytes);
+    char* blob = static_cast<char*>(host_blob);
+    // walk 2: each path's elements straight to their packed position
+    std::vector<double> term((size_t)P);
+    const float inf = std::numeric_limits<float>::infinity();
+    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+      const int64_t base = ens->tree_node_offsets[t];
+      int64_t p = tree_first[(size_t)t];
+      return w.walk(ens, t, [&](int32_t leaf, size_t m) {
+        const double v = ens->value[base + leaf];
+        double prod = 1.0;
+        for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
+        term[(size_t)p] = v * prod;
+        if (blob) {
+          const int64_t d = pk.dest[(size_t)p];
+          put_element(bp.m, blob, d, -1, -inf, inf, v);
+          for (size_t i = 0; i < m; ++i) {
+            const Split& s = w.merged[i];
+            put_element(bp.m, blob, d + 1 + (int64_t)i, s.feature, s.lower, s.upper,
+                        s.zero_fraction);
+          }
+        }
+        ++p;
+      });
+    });
+    // bias: sum in path order, like a single pass over the ensemble would
+    std::vector<double> bsum((size_t)ens->num_groups, 0.0);
+    {
+      int64_t p = 0;
+      for (int64_t t = 0; t < T; ++t) {
+        const int32_t g = ens->tree_group[t];
+        for (; p < tree_first[(size_t)t + 1]; ++p) bsum[(size_t)g] += term[(size_t)p];
+      }
+    }
+    if (bias)
+      for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = bsum[(size_t)g];
+    if (blob) {
+      zero_padding(bp, blob);
+      write_bins_and_bias(bp, blob, pk.bin_offsets.data(), pk.bin_group.data(), bsum.data());
     }
     return GTS_OK;
   } catch (const std::bad_alloc&) {

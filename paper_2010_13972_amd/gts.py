@@ -75,6 +75,9 @@ def lib() -> ctypes.CDLL:
         L.gts_model_layout.argtypes = [vp, i64, vp, i64, i32, i32, vp, i32,
                                        ctypes.POINTER(ModelDesc), vp, i64]
         L.gts_model_layout.restype = st
+        L.gts_prepare_model.argtypes = [ctypes.POINTER(_Ensemble), i32, i32, i32,
+                                        ctypes.POINTER(ModelDesc), vp, i64, vp]
+        L.gts_prepare_model.restype = st
         for name in ("gts_shap", "gts_shap_interactions"):
             f = getattr(L, name)
             f.argtypes = [ctypes.POINTER(ModelDesc), vp, vp, i64, i64, vp, vp]
@@ -143,13 +146,13 @@ def pack_paths(elements: np.ndarray, bin_capacity: int = 64,
     elements = np.ascontiguousarray(elements, PATH_ELEMENT)
     k = ctypes.c_int64(0)
     a = PACK_ALGS[alg]
-    _check(lib().gts_pack_paths(_ptr(elements), len(elements), bin_capacity, a, None, None, 0,
-                                ctypes.byref(k)), "gts_pack_paths")
-    packed = np.zeros(len(elements), PATH_ELEMENT)
-    offs = np.zeros(k.value + 1, np.int64)
+    # one call: there are never more bins than paths
+    num_paths = int(np.count_nonzero(elements["feature_idx"] == -1))
+    packed = np.empty(len(elements), PATH_ELEMENT)
+    offs = np.empty(num_paths + 1, np.int64)
     _check(lib().gts_pack_paths(_ptr(elements), len(elements), bin_capacity, a, _ptr(packed),
                                 _ptr(offs), len(offs), ctypes.byref(k)), "gts_pack_paths")
-    return packed, offs
+    return packed, offs[:k.value + 1].copy()
 
 
 def model_layout(packed: np.ndarray, bin_offsets: np.ndarray, num_features: int,
@@ -162,7 +165,7 @@ def model_layout(packed: np.ndarray, bin_offsets: np.ndarray, num_features: int,
     args = (_ptr(packed), len(packed), _ptr(bin_offsets), len(bin_offsets) - 1, num_features,
             num_groups, _ptr(bias), DTYPES[dtype])
     _check(lib().gts_model_layout(*args, ctypes.byref(desc), None, 0), "gts_model_layout")
-    blob = np.zeros(desc.bytes, np.uint8)
+    blob = np.empty(desc.bytes, np.uint8)
     _check(lib().gts_model_layout(*args, ctypes.byref(desc), _ptr(blob), len(blob)),
            "gts_model_layout")
     return desc, blob
@@ -200,9 +203,41 @@ def upload(desc: ModelDesc, blob: np.ndarray, num_features: int, num_groups: int
                        bias)
 
 
+def prepare_blob(ens, dtype: str = "f32", bin_capacity: int = 64, alg: str = "bfd",
+                 _cache={}):
+    """gts_prepare_model: (ModelDesc, host blob, bias) straight from the
+    ensemble.  The blob size of the last model with the same node count is
+    tried first, so repeated preparation of one ensemble is a single call."""
+    s, keep = _ensemble_struct(ens)
+    desc = ModelDesc()
+    bias = np.zeros(ens.num_groups, np.float64)
+    key = (ens.num_nodes, ens.num_trees, dtype, bin_capacity, alg)
+    size = _cache.get(key, 0)
+    blob = np.empty(size, np.uint8) if size else None
+    st = lib().gts_prepare_model(ctypes.byref(s), bin_capacity, PACK_ALGS[alg], DTYPES[dtype],
+                                 ctypes.byref(desc), _ptr(blob), size, _ptr(bias))
+    if st == GTS_OK and blob is not None and desc.bytes == size:
+        return desc, blob, bias
+    if st not in (GTS_OK, GTS_EBUFSIZE):
+        _check(st, "gts_prepare_model")
+    blob = np.empty(desc.bytes, np.uint8)
+    _check(lib().gts_prepare_model(ctypes.byref(s), bin_capacity, PACK_ALGS[alg], DTYPES[dtype],
+                                   ctypes.byref(desc), _ptr(blob), len(blob), _ptr(bias)),
+           "gts_prepare_model")
+    _cache[key] = int(desc.bytes)
+    return desc, blob, bias
+
+
 def prepare(ens, dtype: str = "f32", device="cuda", bin_capacity: int = 64,
             alg: str = "bfd") -> DeviceModel:
     """Extract, pack, lay out and upload an ensemble (Section 3, steps 1-3)."""
+    desc, blob, bias = prepare_blob(ens, dtype, bin_capacity, alg)
+    return upload(desc, blob, ens.num_features, ens.num_groups, dtype, bias, device)
+
+
+def prepare_stepwise(ens, dtype: str = "f32", device="cuda", bin_capacity: int = 64,
+                     alg: str = "bfd") -> DeviceModel:
+    """The same as prepare() through the three separate host calls."""
     elements, _, bias = extract_paths(ens)
     packed, offs = pack_paths(elements, bin_capacity, alg)
     desc, blob = model_layout(packed, offs, ens.num_features, ens.num_groups, bias, dtype)

@@ -292,3 +292,36 @@ def test_device_calls_reject_bad_arguments_without_touching_the_gpu():
         forged = gts.ModelDesc.from_buffer_copy(desc)
         forged.magic = 0
         assert fn(ctypes.byref(forged), vp(1), vp(1), 4, 8, vp(1), None) == gts.GTS_EINVAL
+
+
+@pytest.mark.parametrize("name", ["tiny", "covtype_med", "wide", "random0", "random2"])
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+@pytest.mark.parametrize("alg", ["bfd", "nf"])
+def test_prepare_model_equals_the_three_step_route(name, dtype, alg):
+    """gts_prepare_model writes byte for byte the blob and descriptor of
+    gts_model_layout(gts_pack_paths(gts_extract_paths(.)))."""
+    w = _workload(name)
+    el, npaths, bias = gts.extract_paths(w.ensemble)
+    packed, offs = gts.pack_paths(el, 64, alg)
+    d1, b1 = gts.model_layout(packed, offs, w.ensemble.num_features, w.ensemble.num_groups,
+                              bias, dtype)
+    for _ in range(2):  # second call takes the cached-size fast path
+        d2, b2, bias2 = gts.prepare_blob(w.ensemble, dtype, 64, alg)
+        assert bytes(d1) == bytes(d2)
+        assert b1.tobytes() == b2.tobytes()
+        assert bias.tobytes() == bias2.tobytes()
+
+
+def test_prepare_model_errors():
+    w = synth.workload("deep")
+    with pytest.raises(gts.GtsError) as e:           # depth-16 paths do not fit 8 lanes
+        gts.prepare_blob(w.ensemble, "f32", 8, "bfd")
+    assert e.value.status == gts.GTS_EPATHLEN
+    base = synth.workload("tiny").ensemble
+    import copy
+    bad = copy.deepcopy(base)
+    bad.feature = bad.feature.copy()
+    bad.feature[0] = 99
+    with pytest.raises(gts.GtsError) as e:
+        gts.prepare_blob(bad, "f32")
+    assert e.value.status == gts.GTS_EINVAL
