@@ -416,6 +416,7 @@ struct Packing {
   std::vector<int64_t> order;        // paths in placement order
   std::vector<int64_t> bin_of;       // per path
   std::vector<int64_t> dest;         // per path: packed element offset
+  std::vector<int32_t> slot;         // per path: its position among its bin's paths
   std::vector<int64_t> bin_offsets;  // [K+1]
   std::vector<int32_t> bin_group;    // [K]
   int64_t K = 0;
@@ -520,11 +521,14 @@ void assign_bins(const int32_t* size, const int32_t* group, int64_t P, int32_t c
   }
   for (int64_t b = 0; b < K; ++b) off[(size_t)b + 1] += off[(size_t)b];
   std::vector<int64_t> cursor(off.begin(), off.end() - 1);
+  std::vector<int32_t> filled((size_t)K, 0);
   pk.dest.resize((size_t)P);
+  pk.slot.resize((size_t)P);
   for (size_t k = 0; k < order.size(); ++k) {
     const int64_t p = order[k];
     const int64_t b = bin_of[(size_t)p];
     pk.dest[(size_t)p] = cursor[(size_t)b];
+    pk.slot[(size_t)p] = filled[(size_t)b]++;
     cursor[(size_t)b] += size[p];
   }
 }
@@ -605,6 +609,99 @@ inline void put_element(const gts_model& m, char* blob, int64_t i, int32_t feat,
   reinterpret_cast<float*>(blob + m.off[kUpper])[i] = hi;
   if (m.dtype == GTS_F64) reinterpret_cast<double*>(blob + m.off[kZero])[i] = z_or_v;
   else reinterpret_cast<float*>(blob + m.off[kZero])[i] = (float)z_or_v;
+}
+
+// Device order of a path's feature elements.  The kernels may run several
+// paths of a bin side by side, one per group of lanes, stepping through their
+// elements together; paths that share a feature (often the same tree's upper
+// splits) would then update the same phi-tile entry in the same step, which
+// the kernels' compare-and-swap accumulation resolves by retrying.  SHAP
+// arithmetic does not depend on the element order, so each path's
+// feature-sorted elements are rotated: paths are taken in their order in the
+// bin, and each gets the rotation (tried from t mod q for the t-th path) that
+// puts the fewest of its features at a position where an earlier path of
+// the bin already has the same feature.
+template <typename Z>
+void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t a1,
+                std::vector<uint64_t>& used, std::vector<int32_t>& touched) {
+  Z zbuf[kMaxPathLen];
+  float lbuf[kMaxPathLen], hbuf[kMaxPathLen];
+  int32_t fbuf[kMaxPathLen];
+  int32_t t = 0;
+  int64_t a = a0;
+  while (a < a1) {
+    int64_t e = a + 1;
+    while (e < a1 && feat[e] != -1) ++e;
+    const int32_t q = (int32_t)(e - a - 1);
+    if (q > 1) {
+      const int32_t* f = feat + a + 1;
+      int32_t best = 0, best_cost = INT32_MAX;
+      for (int32_t i = 0; i < q; ++i) {
+        const int32_t rho = (t + i) % q;
+        int32_t cost = 0;
+        for (int32_t k = 0; k < q; ++k) cost += (int32_t)((used[(size_t)f[(k + rho) % q]] >> k) & 1u);
+        if (cost < best_cost) {
+          best_cost = cost;
+          best = rho;
+          if (cost == 0) break;
+        }
+      }
+      for (int32_t k = 0; k < q; ++k) {
+        const int64_t src = a + 1 + (k + best) % q;
+        fbuf[k] = feat[src];
+        lbuf[k] = lo[src];
+        hbuf[k] = hi[src];
+        zbuf[k] = zf[src];
+      }
+      for (int32_t k = 0; k < q; ++k) {
+        feat[a + 1 + k] = fbuf[k];
+        lo[a + 1 + k] = lbuf[k];
+        hi[a + 1 + k] = hbuf[k];
+        zf[a + 1 + k] = zbuf[k];
+      }
+    }
+    for (int32_t k = 0; k < q; ++k) {
+      uint64_t& m = used[(size_t)feat[a + 1 + k]];
+      if (m == 0) touched.push_back(feat[a + 1 + k]);
+      m |= 1ull << k;
+    }
+    ++t;
+    a = e;
+  }
+  for (int32_t f : touched) used[(size_t)f] = 0;
+  touched.clear();
+}
+
+// Applies rotate_bin to every bin of a written blob, bins spread over threads.
+void rotate_bins(const gts_model& m, char* blob, const int64_t* bin_offsets) {
+  int32_t* feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]);
+  float* lo = reinterpret_cast<float*>(blob + m.off[kLower]);
+  float* hi = reinterpret_cast<float*>(blob + m.off[kUpper]);
+  const int64_t K = m.num_bins;
+  const int threads = (int)std::max<int64_t>(1, std::min<int64_t>(host_threads(K / 8), 16));
+  std::atomic<int64_t> next{0};
+  auto worker = [&]() {
+    std::vector<uint64_t> used((size_t)m.num_features, 0);
+    std::vector<int32_t> touched;
+    constexpr int64_t kChunk = 64;
+    for (;;) {
+      const int64_t b0 = next.fetch_add(kChunk);
+      if (b0 >= K) break;
+      const int64_t b1 = std::min(K, b0 + kChunk);
+      for (int64_t b = b0; b < b1; ++b) {
+        if (m.dtype == GTS_F64)
+          rotate_bin(feat, lo, hi, reinterpret_cast<double*>(blob + m.off[kZero]), bin_offsets[b],
+                     bin_offsets[b + 1], used, touched);
+        else
+          rotate_bin(feat, lo, hi, reinterpret_cast<float*>(blob + m.off[kZero]), bin_offsets[b],
+                     bin_offsets[b + 1], used, touched);
+      }
+    }
+  };
+  std::vector<std::thread> pool;
+  for (int i = 1; i < threads; ++i) pool.emplace_back(worker);
+  worker();
+  for (auto& th : pool) th.join();
 }
 
 }  // namespace
@@ -730,6 +827,7 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
       put_element(bp.m, blob, i, e.feature_idx, e.lower, e.upper,
                   e.feature_idx == -1 ? e.v : e.zero_fraction);
     }
+    rotate_bins(bp.m, blob, bin_offsets);
     write_bins_and_bias(bp, blob, bin_offsets, bin_group.data(), bias);
     return GTS_OK;
   } catch (const std::bad_alloc&) {
@@ -835,6 +933,7 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = bsum[(size_t)g];
     if (blob) {
       zero_padding(bp, blob);
+      rotate_bins(bp.m, blob, pk.bin_offsets.data());
       write_bins_and_bias(bp, blob, pk.bin_offsets.data(), pk.bin_group.data(), bsum.data());
     }
     return GTS_OK;

@@ -14,6 +14,8 @@ namespace gts {
 // never mix output groups and are ordered by group.  A path is a root element
 // followed by its feature elements; the root's zero-fraction slot holds the
 // path's leaf value v (a root's own zero fraction is always 1 and unused).
+// Within a bin, each path's feature-sorted elements are stored rotated (see
+// rotate_bin in the host code); roots stay first.
 enum BlobArray : int {
   kFeat = 0,       // int32[num_elements]   split feature, -1 on root elements
   kLower = 1,      // float[num_elements]   range [lower, upper)

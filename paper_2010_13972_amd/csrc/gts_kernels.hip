@@ -95,34 +95,6 @@ __host__ __device__ constexpr double shapley_weight(int n, int k) {
   return 1.0 / ((double)n * c);
 }
 
-// ---------------------------------------------------------------------------
-// cross-lane moves
-// ---------------------------------------------------------------------------
-
-__device__ __forceinline__ int rl(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
-__device__ __forceinline__ float rl(float v, int lane) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
-}
-__device__ __forceinline__ double rl(double v, int lane) {
-  const unsigned long long u = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_readlane((int)(u & 0xffffffffu), lane);
-  const int hi = __builtin_amdgcn_readlane((int)(u >> 32), lane);
-  return __longlong_as_double(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
-}
-// ds_bpermute: value of lane `lane` (taken modulo the wave size)
-__device__ __forceinline__ int bp(int v, int lane) {
-  return __builtin_amdgcn_ds_bpermute((lane & 63) << 2, v);
-}
-__device__ __forceinline__ float bp(float v, int lane) {
-  return __int_as_float(__builtin_amdgcn_ds_bpermute((lane & 63) << 2, __float_as_int(v)));
-}
-__device__ __forceinline__ double bp(double v, int lane) {
-  const unsigned long long u = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_ds_bpermute((lane & 63) << 2, (int)(u & 0xffffffffu));
-  const int hi = __builtin_amdgcn_ds_bpermute((lane & 63) << 2, (int)(u >> 32));
-  return __longlong_as_double(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
-}
-
 // Add to a phi-tile entry in LDS.  A compare-and-swap loop on the bit
 // pattern: gfx950 executes the LDS float add atomic (ds_add_f32) one lane at
 // a time, about 190 cycles per wave64 instruction, while the integer
@@ -144,6 +116,15 @@ __device__ __forceinline__ void lds_add(double* p, double v) {
     old = atomicCAS(q, assumed,
                     (unsigned long long)__double_as_longlong(__longlong_as_double((long long)assumed) + v));
   } while (old != assumed);
+}
+
+// Accumulate into the phi tile.  EXCL: no other lane or wave can update the
+// same entry at the same time (a wave-private tile with one path per wave),
+// so a plain read-modify-write suffices.
+template <bool EXCL, typename T>
+__device__ __forceinline__ void acc_add(T* p, T v) {
+  if constexpr (EXCL) *p += v;
+  else lds_add(p, v);
 }
 
 // One bin, one element per lane.
@@ -175,26 +156,55 @@ __device__ __forceinline__ Bin<T> load_bin(const DevModel<T>& d, int bi, int lan
   return b;
 }
 
-// Element k (0-based among the path's features) of the path starting at
-// bin lane s.  UNIFORM: s is the same for the whole wave (v_readlane);
-// otherwise s is per lane (ds_bpermute, executed by every lane).
-template <typename T, bool UNIFORM>
+// One wave's copy of its current bin in LDS: element e (a lane of the bin)
+// as (feature, lower, upper, zero fraction or leaf value).  Paths start at a
+// table built from the root ballot: start[t] = bin lane of the t-th root,
+// start[#roots] = bin length.
+template <typename T>
+struct Stage {
+  int4 meta[64];   // feature, lower bits, upper bits, z bits (fp32 z only)
+  T zd[64];        // z in the model dtype
+  int start[65];
+};
+
+template <typename T>
+__device__ __forceinline__ int stage_bin(Stage<T>* st, const Bin<T>& b, int lane) {
+  st->meta[lane] = make_int4(b.feat, __float_as_int(b.lo), __float_as_int(b.hi),
+                             sizeof(T) == 4 ? __float_as_int((float)b.z) : 0);
+  st->zd[lane] = b.z;
+  const bool root = b.feat == -1;
+  const uint64_t roots = __ballot(root);
+  const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(roots >> 32),
+                                             __builtin_amdgcn_mbcnt_lo((unsigned)roots, 0u));
+  if (root) st->start[rank] = lane;
+  const int nroots = __popcll(roots);
+  if (lane == 0) st->start[nroots] = b.len;
+  // the stores above are read by other lanes of this wave only
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  return nroots;
+}
+
+// Element k (0-based among the path's features) of the path whose root is
+// at bin lane s; s is wave-uniform when one path fills the wave.
+template <typename T>
 struct Fetch {
-  const Bin<T>& b;
+  const Stage<T>* st;
   int s;
-  __device__ __forceinline__ int feat(int k) const {
-    return UNIFORM ? rl(b.feat, s + 1 + k) : bp(b.feat, s + 1 + k);
+  __device__ __forceinline__ void get(int k, int& f, float& lo, float& hi, T& z) const {
+    const int e = (s + 1 + k) & 63;
+    const int4 m = st->meta[e];
+    f = m.x;
+    lo = __int_as_float(m.y);
+    hi = __int_as_float(m.z);
+    if constexpr (sizeof(T) == 4) z = __int_as_float(m.w);
+    else z = st->zd[e];
   }
-  __device__ __forceinline__ float lo(int k) const {
-    return UNIFORM ? rl(b.lo, s + 1 + k) : bp(b.lo, s + 1 + k);
+  __device__ __forceinline__ T v() const {
+    if constexpr (sizeof(T) == 4) return __int_as_float(st->meta[s & 63].w);
+    else return st->zd[s & 63];
   }
-  __device__ __forceinline__ float hi(int k) const {
-    return UNIFORM ? rl(b.hi, s + 1 + k) : bp(b.hi, s + 1 + k);
-  }
-  __device__ __forceinline__ T z(int k) const {
-    return UNIFORM ? rl(b.z, s + 1 + k) : bp(b.z, s + 1 + k);
-  }
-  __device__ __forceinline__ T v() const { return UNIFORM ? rl(b.z, s) : bp(b.z, s); }
 };
 
 // Feature, presence test o_k = [lower <= x < upper] and zero fraction of
@@ -202,14 +212,14 @@ struct Fetch {
 // probability 1 and absent with probability 1 (z = o = 1), which changes no
 // other element's Shapley value; f = -1 marks them unwritten.
 template <typename T, int Q, bool UNIFORM>
-__device__ __forceinline__ void load_path(const Fetch<T, UNIFORM>& fe, int q,
-                                          const float* __restrict__ xrow, int (&f)[Q],
-                                          bool (&o)[Q], T (&z)[Q]) {
+__device__ __forceinline__ void load_path(const Fetch<T>& fe, int q, const float* __restrict__ xrow,
+                                          int (&f)[Q], bool (&o)[Q], T (&z)[Q]) {
 #pragma unroll
   for (int k = 0; k < Q; ++k) {
-    const int fk = fe.feat(k);
-    const float lo = fe.lo(k), hi = fe.hi(k);
-    const T zk = fe.z(k);
+    int fk;
+    float lo, hi;
+    T zk;
+    fe.get(k, fk, lo, hi, zk);
     const bool real = UNIFORM || k < q;
     const float x = xrow[real ? fk : 0];
     f[k] = real ? fk : -1;
@@ -248,7 +258,7 @@ __device__ __forceinline__ void unwind_one(const T (&E)[Q + 1], T zi, T (&D)[Q])
 // ---------------------------------------------------------------------------
 
 // SHAP values: phi[f_i] += v (o_i - z_i) * sum_k c_k D^i_k
-template <typename T, int Q>
+template <typename T, int Q, bool EXCL>
 __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
                                           T v, bool active, T* __restrict__ prow) {
   T E[Q + 1];
@@ -265,7 +275,7 @@ __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q],
 #pragma unroll
     for (int k = 0; k < Q; ++k) s = fma(T(shapley_weight(Q, k)), D[k], s);
     const T phi = o[i] ? v * (T(1) - z[i]) * s : neg_vt;
-    if (active && f[i] >= 0) lds_add(&prow[f[i]], phi);
+    if (active && f[i] >= 0) acc_add<EXCL>(&prow[f[i]], phi);
   }
 }
 
@@ -277,7 +287,7 @@ __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q],
 //   (1,0): (o_c - z_c) S_ic = -sum_k c'_k D^i_k         (D^i = E / (z_i + t))
 //   (0,0): (o_i - z_i)(o_c - z_c) S_ic = sum_k c'_k E_k
 // and phi_ii = phi_i - sum_{c != i} Delta_ic (Eq. 6).
-template <typename T, int Q>
+template <typename T, int Q, bool EXCL>
 __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
                                            T v, bool active, T* __restrict__ prow, int stride) {
   T E[Q + 1];
@@ -325,14 +335,14 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
       diag[c] -= delta;
       diag[i] -= delta;
       if (active && f[i] >= 0 && f[c] >= 0) {
-        lds_add(&prow[f[i] * stride + f[c]], delta);
-        lds_add(&prow[f[c] * stride + f[i]], delta);
+        acc_add<EXCL>(&prow[f[i] * stride + f[c]], delta);
+        acc_add<EXCL>(&prow[f[c] * stride + f[i]], delta);
       }
     }
   }
 #pragma unroll
   for (int c = 0; c < Q; ++c)
-    if (active && f[c] >= 0) lds_add(&prow[f[c] * stride + f[c]], diag[c]);
+    if (active && f[c] >= 0) acc_add<EXCL>(&prow[f[c] * stride + f[c]], diag[c]);
 }
 
 // Paths longer than the unrolled variants: the same arithmetic with runtime
@@ -341,19 +351,20 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
 // passes the parity bound beyond about 20 features, in fp64 it stays far
 // inside it for the longest path a wave64 holds (63 features).  FP64 FMAs run
 // at the rate of unpacked FP32 ones on gfx950.
-template <typename T, bool UNIFORM, bool INTER>
-__device__ void path_dyn(const Fetch<T, UNIFORM>& fe, int qfetch, int q, bool active,
+template <typename T, bool INTER, bool EXCL>
+__device__ void path_dyn(const Fetch<T>& fe, int qfetch, int q, bool active,
                          const float* __restrict__ xrow, T* __restrict__ prow, int stride) {
   double E[kMaxPathLen];
   double z[kMaxPathLen];
   double D[kMaxPathLen];
   int f[kMaxPathLen];
   uint64_t obits = 0;
-  // fetch with a wave-uniform trip count (ds_bpermute needs every lane)
   for (int k = 0; k < qfetch; ++k) {
-    const int fk = fe.feat(k);
-    const float lo = fe.lo(k), hi = fe.hi(k);
-    const double zk = (double)fe.z(k);
+    int fk;
+    float lo, hi;
+    T zt;
+    fe.get(k, fk, lo, hi, zt);
+    const double zk = (double)zt;
     if (k < q) {
       const float x = xrow[fk];
       f[k] = fk;
@@ -380,7 +391,7 @@ __device__ void path_dyn(const Fetch<T, UNIFORM>& fe, int qfetch, int q, bool ac
       for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
       const bool oi = (obits >> i) & 1u;
       const double phi = oi ? v * (1.0 - z[i]) * s : -v * t_all;
-      if (active) lds_add(&prow[f[i]], (T)phi);
+      if (active) acc_add<EXCL>(&prow[f[i]], (T)phi);
     }
   } else {
     double DD[kMaxPathLen];
@@ -412,18 +423,18 @@ __device__ void path_dyn(const Fetch<T, UNIFORM>& fe, int qfetch, int q, bool ac
         diag[c] -= delta;
         diag[i] -= delta;
         if (active) {
-          lds_add(&prow[f[i] * stride + f[c]], (T)delta);
-          lds_add(&prow[f[c] * stride + f[i]], (T)delta);
+          acc_add<EXCL>(&prow[f[i] * stride + f[c]], (T)delta);
+          acc_add<EXCL>(&prow[f[c] * stride + f[i]], (T)delta);
         }
       }
     }
     for (int c = 0; c < q; ++c)
-      if (active) lds_add(&prow[f[c] * stride + f[c]], (T)diag[c]);
+      if (active) acc_add<EXCL>(&prow[f[c] * stride + f[c]], (T)diag[c]);
   }
 }
 
-template <typename T, int Q, bool UNIFORM, bool INTER>
-__device__ __forceinline__ void path_fixed(const Fetch<T, UNIFORM>& fe, int q, bool active,
+template <typename T, int Q, bool UNIFORM, bool INTER, bool EXCL>
+__device__ __forceinline__ void path_fixed(const Fetch<T>& fe, int q, bool active,
                                            const float* __restrict__ xrow, T* __restrict__ prow,
                                            int stride) {
   int f[Q];
@@ -431,82 +442,83 @@ __device__ __forceinline__ void path_fixed(const Fetch<T, UNIFORM>& fe, int q, b
   T z[Q];
   load_path<T, Q, UNIFORM>(fe, q, xrow, f, o, z);
   const T v = fe.v();
-  if constexpr (INTER) inter_math<T, Q>(f, o, z, v, active, prow, stride);
-  else shap_math<T, Q>(f, o, z, v, active, prow);
+  if constexpr (INTER) inter_math<T, Q, EXCL>(f, o, z, v, active, prow, stride);
+  else shap_math<T, Q, EXCL>(f, o, z, v, active, prow);
 }
 
 // Q = features of the longest path in the wave's current set (uniform)
-template <typename T, bool UNIFORM, bool INTER>
-__device__ __forceinline__ void dispatch(int Q, const Fetch<T, UNIFORM>& fe, int q, bool active,
+template <typename T, bool UNIFORM, bool INTER, bool EXCL>
+__device__ __forceinline__ void dispatch(int Q, const Fetch<T>& fe, int q, bool active,
                                          const float* xrow, T* prow, int stride) {
   static_assert(kMaxUnrolledShap == 16 && kMaxUnrolledInter == 8, "update the case lists");
   if constexpr (INTER) {
     switch (Q) {
-#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, true>(fe, q, active, xrow, prow, stride); break;
+#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, true, EXCL>(fe, q, active, xrow, prow, stride); break;
       GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
       GTS_CASE(7) GTS_CASE(8)
 #undef GTS_CASE
-      default: path_dyn<T, UNIFORM, true>(fe, Q, q, active, xrow, prow, stride); break;
+      default: path_dyn<T, true, EXCL>(fe, Q, q, active, xrow, prow, stride); break;
     }
   } else {
     switch (Q) {
-#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, false>(fe, q, active, xrow, prow, stride); break;
+#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, false, EXCL>(fe, q, active, xrow, prow, stride); break;
       GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
       GTS_CASE(7) GTS_CASE(8) GTS_CASE(9) GTS_CASE(10) GTS_CASE(11) GTS_CASE(12)
       GTS_CASE(13) GTS_CASE(14) GTS_CASE(15) GTS_CASE(16)
 #undef GTS_CASE
-      default: path_dyn<T, UNIFORM, false>(fe, Q, q, active, xrow, prow, stride); break;
+      default: path_dyn<T, false, EXCL>(fe, Q, q, active, xrow, prow, stride); break;
     }
   }
+}
+
+// Largest value of v over the wave (v in [0, 64)), from six ballots.
+__device__ __forceinline__ int wave_max_small(int v) {
+  int m = 0;
+#pragma unroll
+  for (int bit = 5; bit >= 0; --bit) {
+    const int c = m | (1 << bit);
+    if (__ballot(v >= c)) m = c;
+  }
+  return m;
 }
 
 // All paths of one bin.  RW == 64: one path at a time for the whole wave.
 // RW < 64: rounds of up to P = 64/RW paths, lane (j, r) = (path j, row r).
-template <typename T, int RW, bool INTER>
-__device__ __forceinline__ void process_bin(const Bin<T>& b, int lane, const float* xrow,
-                                            T* prow, int stride) {
-  uint64_t roots = __ballot(b.feat == -1);
+template <typename T, int RW, bool INTER, bool EXCL>
+__device__ __forceinline__ void process_bin(Stage<T>* st, const Bin<T>& b, int lane,
+                                            const float* xrow, T* prow, int stride) {
+  const int nroots = stage_bin(st, b, lane);
   if constexpr (RW == 64) {
-    while (roots) {
-      const int s = __builtin_ctzll(roots);
-      roots &= roots - 1;
-      const int e = roots ? __builtin_ctzll(roots) : b.len;
-      const int q = e - s - 1;
-      if (q > 0) dispatch<T, true, INTER>(q, Fetch<T, true>{b, s}, q, true, xrow, prow, stride);
+    for (int t = 0; t < nroots; ++t) {
+      const int s = __builtin_amdgcn_readfirstlane(st->start[t]);
+      const int q = __builtin_amdgcn_readfirstlane(st->start[t + 1]) - s - 1;
+      if (q > 0) dispatch<T, true, INTER, EXCL>(q, Fetch<T>{st, s}, q, true, xrow, prow, stride);
     }
   } else {
     constexpr int P = 64 / RW;
     const int j = lane / RW;
-    while (roots) {
-      int my_s = 0, my_q = -1, qmax = 0;
-#pragma unroll
-      for (int jj = 0; jj < P; ++jj) {
-        if (roots) {
-          const int s = __builtin_ctzll(roots);
-          roots &= roots - 1;
-          const int e = roots ? __builtin_ctzll(roots) : b.len;
-          const int q = e - s - 1;
-          qmax = q > qmax ? q : qmax;
-          if (j == jj) {
-            my_s = s;
-            my_q = q;
-          }
-        }
-      }
-      const bool active = my_q > 0;
-      if (my_q < 0) my_q = 0;
+    for (int base = 0; base < nroots; base += P) {
+      const int t = base + j;
+      const bool valid = t < nroots;
+      const int my_s = valid ? st->start[t] : 0;
+      const int my_q = valid ? st->start[t + 1] - my_s - 1 : 0;
+      const int qmax = wave_max_small(my_q);
       if (qmax > 0)
-        dispatch<T, false, INTER>(qmax, Fetch<T, false>{b, my_s}, my_q, active, xrow, prow, stride);
+        dispatch<T, false, INTER, false>(qmax, Fetch<T>{st, my_s}, my_q, my_q > 0, xrow, prow, stride);
     }
   }
+  // the next bin overwrites the stage
+  __builtin_amdgcn_wave_barrier();
 }
 
 // One workgroup: rows [tile*RW, tile*RW + RW) of output group g, bins of
-// slice s of that group.  Workgroups are dealt to the 8 XCDs round-robin; when
+// slice s of that group.  PRIV: every wave accumulates into a phi tile of its
+// own (summed when the tile is written), so waves never contend; with one
+// path per wave (RW == 64) the accumulation then needs no atomics.  Workgroups are dealt to the 8 XCDs round-robin; when
 // the (group, slice) units divide evenly among the XCDs, consecutive
 // workgroups on an XCD take the same unit for successive row tiles, so each
 // XCD's L2 holds only its own part of the model.
-template <typename T, int RW, bool INTER, int WAVES>
+template <typename T, int RW, bool INTER, int WAVES, bool PRIV>
 __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const float* __restrict__ X,
                                                          T* __restrict__ phi, Launch L) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -531,6 +543,10 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
 
   float* xs = reinterpret_cast<float*>(smem);
   T* ps = reinterpret_cast<T*>(smem + (size_t)RW * L.sx * sizeof(float));
+  constexpr int NT = PRIV ? WAVES : 1;  // phi tiles
+  const int tile_elems = RW * L.sp;
+  Stage<T>* stages = reinterpret_cast<Stage<T>*>(
+      smem + (((size_t)RW * L.sx * sizeof(float) + (size_t)NT * tile_elems * sizeof(T) + 15) & ~(size_t)15));
 
   // stage the X tile (coalesced along each row) and clear the phi tile
   for (int i = threadIdx.x; i < RW * M; i += kThreads) {
@@ -538,7 +554,7 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
     const int64_t row = r0 + r;
     xs[r * L.sx + c] = row < L.rows ? X[row * L.ld + c] : 0.0f;
   }
-  for (int i = threadIdx.x; i < RW * L.sp; i += kThreads) ps[i] = T(0);
+  for (int i = threadIdx.x; i < NT * tile_elems; i += kThreads) ps[i] = T(0);
   __syncthreads();
 
   const int wave = threadIdx.x >> 6;
@@ -550,7 +566,7 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   const int b_lo = gb0 + min(nb, s * chunk);
   const int b_hi = gb0 + min(nb, (s + 1) * chunk);
   const float* xrow = xs + r * L.sx;
-  T* prow = ps + r * L.sp;
+  T* prow = ps + (PRIV ? wave * tile_elems : 0) + r * L.sp;
   const int stride = M + 1;
 
   int bi = b_lo + wave;
@@ -560,7 +576,7 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
       Bin<T> nxt;
       const int bn = bi + WAVES;
       if (bn < b_hi) nxt = load_bin(d, bn, lane);
-      process_bin<T, RW, INTER>(cur, lane, xrow, prow, stride);
+      process_bin<T, RW, INTER, PRIV && RW == 64>(stages + wave, cur, lane, xrow, prow, stride);
       cur = nxt;
     }
   }
@@ -574,6 +590,8 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
     const int64_t row = r0 + rr;
     if (row >= L.rows) continue;
     T val = ps[rr * L.sp + c];
+#pragma unroll
+    for (int w = 1; w < NT; ++w) val += ps[w * tile_elems + rr * L.sp + c];
     if (c == W - 1 && s == 0) val += bias;
     T* out = phi + (row * G + g) * (int64_t)W + c;
     if (L.accumulate) unsafeAtomicAdd(out, val);
@@ -594,6 +612,7 @@ __global__ void fill_zero(T* __restrict__ p, int64_t n) {
 struct DeviceInfo {
   int cus = 256;
   int lds_per_block = 64 * 1024;
+  int lds_per_cu = 160 * 1024;
 };
 
 DeviceInfo device_info() {
@@ -615,6 +634,11 @@ DeviceInfo device_info() {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
         n > 0)
       info.lds_per_block = n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) ==
+            hipSuccess &&
+        n > 0)
+      info.lds_per_cu = n;
+    info.lds_per_cu = std::max(info.lds_per_cu, info.lds_per_block);
     cache[dev] = info;
     have[dev] = 1;
   }
@@ -623,7 +647,7 @@ DeviceInfo device_info() {
 
 inline int odd_at_least(int n) { return n | 1; }
 
-template <typename T, int RW, bool INTER, int WAVES>
+template <typename T, int RW, bool INTER, int WAVES, bool PRIV>
 gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64_t rows,
                      int64_t ld, void* phi, hipStream_t stream, int splits, int32_t sx, int32_t sp,
                      int32_t width, size_t lds) {
@@ -645,7 +669,7 @@ gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64
   }
   const int64_t grid = (int64_t)L.tiles * m->num_groups * splits;
   if (grid > 0x7fffffffLL) return fail(GTS_EINVAL, "problem too large for one launch");
-  auto kern = shap_kernel<T, RW, INTER, WAVES>;
+  auto kern = shap_kernel<T, RW, INTER, WAVES, PRIV>;
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return fail(GTS_EDEVICE, "cannot set the LDS size of the kernel to %zu bytes", lds);
@@ -667,34 +691,41 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
   const int32_t width = (int32_t)width64;
   const int32_t sx = odd_at_least(M);
   const int32_t sp = odd_at_least(width);
-  // Row tile: the largest RW whose X and phi tiles fit in 64 KB (several
-  // workgroups per CU, 4 waves each).  If that leaves fewer than 8 rows per
-  // wave (more than 8 paths per round, while a bin holds about 64/L paths),
-  // use up to the whole LDS of a workgroup for 8 rows, with 8 waves.
-  auto need = [&](int rw) { return (size_t)rw * ((size_t)sx * sizeof(float) + (size_t)sp * sizeof(T)); };
+  // Row tile and accumulation.  If 64 rows with a private phi tile for each
+  // of 4 waves fit in 64 KB, use them (no contention, no atomics).  Otherwise
+  // 8 waves share one tile: the largest RW whose tiles fit in 64 KB (several
+  // workgroups per CU), or, if that would leave fewer than 8 rows per wave,
+  // 8 rows (then 4) using up to the whole LDS of a workgroup.
+  auto need = [&](int rw, int waves, bool priv) {
+    const size_t tiles = (size_t)rw * ((size_t)sx * sizeof(float) +
+                                       (priv ? (size_t)waves : 1) * (size_t)sp * sizeof(T));
+    return ((tiles + 15) & ~(size_t)15) + (size_t)waves * sizeof(Stage<T>);
+  };
   int RW = 0;
-  int waves = 4;
-  for (int cand : {64, 32, 16, 8}) {
-    if (need(cand) <= 64 * 1024) {
-      RW = cand;
-      break;
+  int waves = 8;
+  bool priv = false;
+  if (need(64, 4, true) <= 64 * 1024) {
+    RW = 64;
+    waves = 4;
+    priv = true;
+  } else {
+    for (int cand : {64, 32, 16, 8}) {
+      if (need(cand, 8, false) <= 64 * 1024) {
+        RW = cand;
+        break;
+      }
     }
-  }
-  if (RW == 0 && (int64_t)need(8) <= dev.lds_per_block) {
-    RW = 8;
-    waves = 8;
-  }
-  if (RW == 0 && (int64_t)need(4) <= dev.lds_per_block) {
-    RW = 4;
-    waves = need(4) > 64 * 1024 ? 8 : 4;
+    if (RW == 0 && (int64_t)need(8, 8, false) <= dev.lds_per_block) RW = 8;
+    if (RW == 0 && (int64_t)need(4, 8, false) <= dev.lds_per_block) RW = 4;
   }
   if (RW == 0) return fail(GTS_EINVAL, "M = %d needs more LDS than a workgroup has", M);
-  const size_t lds = need(RW);
-  // enough workgroups to give every CU several; (group, slice) units a
-  // multiple of the 8 XCDs when the bin list is split
+  const size_t lds = need(RW, waves, priv);
+  // enough workgroups for two rounds of every CU at the occupancy the LDS
+  // allows; (group, slice) units a multiple of the 8 XCDs when split
   const int64_t tiles = (rows + RW - 1) / RW;
   const int64_t base = tiles * G;
-  const int64_t target = 8LL * dev.cus;
+  const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, dev.lds_per_cu / (int64_t)lds));
+  const int64_t target = 2 * per_cu * dev.cus;
   const int64_t bins_per_group = std::max<int64_t>(1, m->num_bins / G);
   int splits = 1;
   if (base < target) {
@@ -703,11 +734,12 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
     want = (want + step - 1) / step * step;
     splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
   }
-#define GTS_LAUNCH(rw)                                                                       \
-  return waves == 8 ? launch_rw<T, rw, INTER, 8>(m, blob, X, rows, ld, phi, stream, splits, sx, \
-                                                 sp, width, lds)                                \
-                    : launch_rw<T, rw, INTER, 4>(m, blob, X, rows, ld, phi, stream, splits, sx, \
-                                                 sp, width, lds)
+#define GTS_LAUNCH(rw)                                                                    \
+  return launch_rw<T, rw, INTER, 8, false>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, \
+                                           width, lds)
+  if (priv)
+    return launch_rw<T, 64, INTER, 4, true>(m, blob, X, rows, ld, phi, stream, splits, sx, sp,
+                                            width, lds);
   switch (RW) {
     case 64: GTS_LAUNCH(64);
     case 32: GTS_LAUNCH(32);

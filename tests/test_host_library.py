@@ -164,13 +164,35 @@ def test_model_layout_roundtrip():
         assert desc.max_path_len == 9
         n = len(packed)
         feat = np.frombuffer(blob, np.int32, n, desc.off[0])
-        assert np.array_equal(feat, packed["feature_idx"])
         lo = np.frombuffer(blob, np.float32, n, desc.off[1])
         hi = np.frombuffer(blob, np.float32, n, desc.off[2])
-        assert np.array_equal(lo, packed["lower"]) and np.array_equal(hi, packed["upper"])
         z = np.frombuffer(blob, ft, n, desc.off[3])
-        want = np.where(roots, packed["v"], packed["zero_fraction"]).astype(ft)
-        assert np.array_equal(z, want)
+        # each path keeps its root first and stores its feature-sorted
+        # elements as a cyclic rotation; bins are unchanged
+        zsrc = np.where(roots, packed["v"], packed["zero_fraction"]).astype(ft)
+        coll_sorted = coll_stored = 0
+        for b in range(len(offs) - 1):
+            r = np.flatnonzero(roots[offs[b]:offs[b + 1]]) + offs[b]
+            ends = np.append(r[1:], offs[b + 1])
+            seen_sorted, seen_stored = set(), set()
+            for a, e in zip(r, ends):
+                assert feat[a] == -1 and z[a] == zsrc[a]
+                q = e - a - 1
+                if q == 0:
+                    continue
+                sf = packed["feature_idx"][a + 1:e]
+                rho = int(np.flatnonzero(sf == feat[a + 1])[0])
+                want = a + 1 + (np.arange(q) + rho) % q
+                assert np.array_equal(feat[a + 1:e], sf[want - a - 1])
+                assert np.array_equal(lo[a + 1:e], packed["lower"][want])
+                assert np.array_equal(hi[a + 1:e], packed["upper"][want])
+                assert np.array_equal(z[a + 1:e], zsrc[want])
+                for k in range(q):
+                    coll_sorted += (k, sf[k]) in seen_sorted
+                    coll_stored += (k, feat[a + 1 + k]) in seen_stored
+                    seen_sorted.add((k, sf[k]))
+                    seen_stored.add((k, feat[a + 1 + k]))
+        assert coll_stored * 5 < coll_sorted, (coll_stored, coll_sorted)
         bstart = np.frombuffer(blob, np.int32, len(offs), desc.off[4])
         assert np.array_equal(bstart, offs)
         gb = np.frombuffer(blob, np.int32, 11, desc.off[5])
