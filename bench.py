@@ -2,25 +2,33 @@
 
 One step is one pass of the whole path over one batch of rows of the
 covtype-shaped workload (100 trees, depth <= 8, split probability 0.85,
-M = 54, 10 000 rows, fp32): path extraction with duplicate merging,
-Best-Fit-Decreasing packing, device layout and upload of the model (host),
-then the SHAP kernel over the batch (device).  The rows X are resident in
-HBM before timing starts.  `value` is rows explained per second.
+M = 54, 10 000 rows, fp32): path extraction with duplicate merging and the
+bias, Best-Fit-Decreasing packing into 64-element bins, device layout and
+upload of the model (host), then the SHAP kernel over the batch (device).
+The rows X are resident in HBM before timing starts.  `value` is rows
+explained per second over the timed steps.
 
-The same line carries:
-  roofline      the SHAP kernel's modelled FP32 VALU rate against the MI355X
-                vector peak (op model: 10 q^2 + 8 q flops per (row, path)
-                with q path features), its duration from HIP events on the
-                launch stream, and HBM traffic from rocprofv3 counters;
-  kernel        kernel-only rows/s;
-  interactions  the same pipeline with the interaction kernel on the first
-                1000 rows (op model 10q^2 + 8q + q(q-1)(10q+4));
-  cpu_baseline  the fp64 CPU oracle (Algorithm 1, OpenMP over rows) on a
-                row prefix of the same batch, on the host's cores.
+The same JSON line carries:
+  roofline      the SHAP kernel's modelled VALU rate against the MI355X
+                vector peak (op model per (row, path) with q path features:
+                10 q^2 + 8 q flops; interactions add q (q-1)(10 q + 4)),
+                its mean duration from HIP events on the launch stream over
+                back-to-back launches, and its HBM traffic from rocprofv3
+                FETCH_SIZE / WRITE_SIZE, scaled by the same counters' reading
+                of a plain device copy (null when the kernel source differs
+                from the one the counters were taken on);
+  kernel        kernel-only rows/s (median, mean and std of the launches);
+  configs       every workload of the suite (tiny, covtype-shaped, deep fp32
+                and fp64, wide multiclass, interactions): host preparation
+                time, kernel time and rows/s, modelled rate and fraction;
+  cpu_baseline  the fp64 CPU oracle (Algorithm 1, OpenMP over rows) on a row
+                prefix of the same batch, on the host's cores, and on one
+                thread.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -32,24 +40,51 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_FP32_TFLOPS = 157.3   # MI355X FP32 vector, vendor figure
-PEAK_FP64_TFLOPS = 78.6
-PEAK_HBM_GBS = 8000.0
+PEAK_FP64_TFLOPS = 78.6    # MI355X FP64 vector
+METRIC = "rows/sec for SHAP values and SHAP interaction values; % FP32 VALU peak"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2010_13972_amd", "csrc", "gts_kernels.hip")
 
 WORKLOAD_TEXT = {
+    "tiny": "tiny: 10 full depth-3 trees, M=8, X~U[0,1), 256 rows",
     "covtype_med": "covtype-shaped: 100 trees, depth<=8, p_split=0.85, M=54 "
-                   "(10 N(0,1) + 44 Bernoulli(0.2)), 10k background rows for cover",
-    "tiny": "tiny: 10 full depth-3 trees, M=8, U[0,1)",
-    "deep": "deep: 1000 trees, depth<=16, p_split=0.7, <=1024 leaves, M=8, N(0,1)",
-    "wide": "wide: 10 classes x 100 rounds, depth<=8, p_split=0.85, M=784, 50% zeros",
+                   "(10 N(0,1) + 44 Bernoulli(0.2)), 10k rows",
+    "deep": "deep: 1000 trees, depth<=16, p_split=0.7, <=1024 leaves, M=8, N(0,1), 10k rows",
+    "wide": "wide: 10 classes x 100 rounds, depth<=8, p_split=0.85, M=784, 50% zeros, 10k rows",
+    "interactions": "covtype-shaped model, 1000 rows, SHAP interaction values",
 }
 
-# measured traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
-# scaled by a plain copy's reading); None until counters exist for the
-# current kernel
-TRAFFIC_BYTES = {}
+# The suite: (name, workload, dtype, interactions)
+SUITE = [
+    ("tiny_f64", "tiny", "f64", False),
+    ("covtype_med_f32", "covtype_med", "f32", False),
+    ("deep_f32", "deep", "f32", False),
+    ("deep_f64", "deep", "f64", False),
+    ("wide_f32", "wide", "f32", False),
+    ("interactions_f32", "interactions", "f32", True),
+]
+
+# HBM traffic of the SHAP kernel per launch, from rocprofv3 --pmc FETCH_SIZE
+# and --pmc WRITE_SIZE runs of `bench.py --copy-probe`, each scaled by the
+# ratio of a plain 256 MiB copy's true bytes to the counter's reading of it.
+# Keyed by (workload, dtype, interactions); `source` is the SHA-256 of the
+# kernel source the counters were taken on.
+TRAFFIC = {}
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_for(key):
+    t = TRAFFIC.get(key)
+    if t is None or t["source"] != kernel_source_hash():
+        return None
+    return t["fetch_bytes"] + t["write_bytes"]
 
 
 def modelled_flops(q: np.ndarray, interactions: bool) -> float:
+    """Per row: the op model summed over the extracted paths."""
     q = q.astype(np.float64)
     f = 10 * q * q + 8 * q
     if interactions:
@@ -63,8 +98,14 @@ def path_features(gts, ens) -> np.ndarray:
     return np.diff(np.append(roots, len(el))) - 1
 
 
+def kernel_fn(gts, interactions):
+    return gts.shap_interactions if interactions else gts.shap
+
+
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
-    fn = gts.shap_interactions if interactions else gts.shap
+    """Whole-path steps: prepare (host + upload) then the kernel, timed on the
+    host clock; the kernel bracketed by HIP events on its stream."""
+    fn = kernel_fn(gts, interactions)
     stream = torch.cuda.current_stream()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
@@ -75,48 +116,126 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
-        model = gts.prepare(ens, dtype)            # extract + pack + layout + upload
+        model = gts.prepare(ens, dtype)            # extract + merge + pack + layout + upload
         ev[k][0].record(stream)
-        out = fn(model, Xd, out=out)               # the kernel(s)
+        out = fn(model, Xd, out=out)               # the kernel
         ev[k][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    return wall, kern_ms, out, model
+    kern = np.array([a.elapsed_time(b) for a, b in ev])
+    return wall, kern, out, model
 
 
-def time_kernel_only(torch, gts, model, Xd, steps, interactions):
-    fn = gts.shap_interactions if interactions else gts.shap
+def time_kernel(torch, gts, model, Xd, reps, interactions):
+    """Kernel-only: each launch bracketed by HIP events on the launch stream."""
+    fn = kernel_fn(gts, interactions)
+    stream = torch.cuda.current_stream()
     out = fn(model, Xd)
+    out = fn(model, Xd, out=out)
     torch.cuda.synchronize()
-    a = torch.cuda.Event(enable_timing=True)
-    b = torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(steps):
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        a.record(stream)
         fn(model, Xd, out=out)
-    b.record()
+        b.record(stream)
     torch.cuda.synchronize()
-    return a.elapsed_time(b) / steps
+    return np.array([a.elapsed_time(b) for a, b in ev])
+
+
+def time_prepare(gts, ens, dtype, reps=5):
+    """Host preparation (one gts_prepare_model call) and the upload."""
+    import torch
+    host, up = [], []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        desc, blob, bias = gts.prepare_blob(ens, dtype)
+        t1 = time.perf_counter()
+        gts.upload(desc, blob, ens.num_features, ens.num_groups, dtype, bias)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        host.append(t1 - t0)
+        up.append(t2 - t1)
+    return 1e3 * float(np.median(host)), 1e3 * float(np.median(up)), int(len(blob))
+
+
+def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
+    w = synth.workload(workload)
+    ens = w.ensemble
+    rows = w.X.shape[0]
+    Xd = torch.from_numpy(w.X).cuda()
+    q = path_features(gts, ens)
+    host_ms, upload_ms, blob_bytes = time_prepare(gts, ens, dtype)
+    model = gts.prepare(ens, dtype)
+    k = time_kernel(torch, gts, model, Xd, reps, interactions)
+    med = float(np.median(k))
+    flops = modelled_flops(q, interactions) * rows
+    peak = PEAK_FP64_TFLOPS if dtype == "f64" else PEAK_FP32_TFLOPS
+    achieved = flops / (med * 1e-3) / 1e12
+    return {
+        "workload": WORKLOAD_TEXT[workload], "dtype": dtype, "rows": rows,
+        "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
+                   + (f", {ens.num_features + 1}]" if interactions else "]")),
+        "paths": int(len(q)), "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
+        "host_prepare_ms": host_ms, "upload_ms": upload_ms, "model_bytes": blob_bytes,
+        "kernel_ms_median": med, "kernel_ms_mean": float(k.mean()),
+        "kernel_ms_std": float(k.std()), "kernel_runs": len(k),
+        "kernel_rows_per_s": rows / (med * 1e-3),
+        "end_to_end_rows_per_s": rows / ((host_ms + upload_ms + med) * 1e-3),
+        "modelled_tflops": achieved, "peak_tflops": peak, "frac": achieved / peak,
+        "traffic_bytes": traffic_for((workload, dtype, interactions)),
+    }
 
 
 def cpu_baseline(oracle, ens, X, budget_s: float, interactions: bool):
+    """The oracle as it stands, on a row prefix sized to about budget_s of
+    work on all usable cores, then on one thread for a third of that."""
     threads = len(os.sched_getaffinity(0))
     env = os.environ.get("OMP_NUM_THREADS")
     if env and env.isdigit():
         threads = min(threads, int(env))
     fn = oracle.interactions if interactions else oracle.treeshap
-    n = 8 if interactions else 64
-    while True:
-        n = min(n, X.shape[0])
-        t0 = time.perf_counter()
-        fn(ens, X[:n], nthreads=threads)
-        dt = time.perf_counter() - t0
-        if dt >= budget_s / 3 or n == X.shape[0]:
-            break
-        n = min(X.shape[0], int(n * max(2.0, budget_s / 3 / max(dt, 1e-3))))
+
+    def run(nthreads, budget):
+        n = 8 if interactions else 64
+        while True:
+            n = min(n, X.shape[0])
+            t0 = time.perf_counter()
+            fn(ens, X[:n], nthreads=nthreads)
+            dt = time.perf_counter() - t0
+            if dt >= budget / 3 or n == X.shape[0]:
+                return n, dt
+            n = min(X.shape[0], int(n * max(2.0, budget / 3 / max(dt, 1e-3))))
+
+    n, dt = run(threads, budget_s)
+    n1, dt1 = run(1, budget_s / 3)
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n} of {X.shape[0]} rows, {dt:.2f} s, fp64 "
-                      f"{'conditioning interactions' if interactions else 'Algorithm 1'}"}
+            "sample": f"first {n} of {X.shape[0]} rows in {dt:.2f} s, fp64 "
+                      f"{'conditioning interactions' if interactions else 'Algorithm 1'}, "
+                      f"OpenMP over rows",
+            "one_thread_value": n1 / dt1, "one_thread_sample": f"first {n1} rows in {dt1:.2f} s",
+            "cpu": cpu}
+
+
+def copy_probe(torch):
+    """A plain device copy of 256 MiB (read 256 MiB, write 256 MiB) whose
+    FETCH_SIZE / WRITE_SIZE readings calibrate the kernel's."""
+    n = 64 << 20
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    return n * 4
 
 
 def main():
@@ -124,17 +243,22 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="covtype_med", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--workload", default="covtype_med",
+                    choices=["tiny", "covtype_med", "deep", "wide"])
     ap.add_argument("--dtype", default=None, choices=["f32", "f64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-interactions", action="store_true")
+    ap.add_argument("--no-suite", action="store_true",
+                    help="skip the per-workload suite (kernel and preparation of every workload)")
+    ap.add_argument("--suite-reps", type=int, default=10)
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run a plain 256 MiB device copy first (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; multi-GPU row sharding is "
-                                   "described in DESIGN.md but not implemented",
-                          "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this build runs on one GPU only; the row-sharded "
+                                   "multi-GPU design is documented but not built",
+                          "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
 
     import torch
@@ -142,7 +266,10 @@ def main():
 
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a HIP device")
-    gts.lib()  # fail loudly if libgts.so is missing
+    gts.lib()  # fails loudly if libgts.so is missing
+
+    if args.copy_probe:
+        copy_probe(torch)
 
     w = synth.workload(args.workload)
     dtype = args.dtype or w.dtype
@@ -151,45 +278,44 @@ def main():
     Xd = torch.from_numpy(w.X).cuda()
     q = path_features(gts, ens)
 
-    wall, kern_ms, out, model = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                              args.warmup, False)
-    ms_per_step = 1e3 * wall / args.steps
-    value = rows * args.steps / wall
-    k_only_ms = time_kernel_only(torch, gts, model, Xd, args.steps, False)
+    wall, kern, out, model = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
+                                           args.warmup, False)
+    # The roofline takes the kernel's mean launch duration from back-to-back
+    # launches (each bracketed by HIP events on its stream).  Inside the
+    # whole-path steps the GPU idles while the host prepares the next model,
+    # so there the events also hold the host's launch latency.
+    k_only = time_kernel(torch, gts, model, Xd, max(5, args.steps), False)
+    kern_ms = float(k_only.mean())
     flops = modelled_flops(q, False) * rows
     peak = PEAK_FP64_TFLOPS if dtype == "f64" else PEAK_FP32_TFLOPS
     achieved = flops / (kern_ms * 1e-3) / 1e12
     line = {
-        "metric": "rows/sec for SHAP values and SHAP interaction values; % FP32 VALU peak",
-        "value": value, "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "metric": METRIC,
+        "value": rows * args.steps / wall, "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * wall / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic (seeded ensembles and rows shaped like the paper's models)",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "rows": rows,
-                   "paths": int(len(q)), "path_elements": int((q + 1).sum()),
+                   "trees": int(ens.num_trees), "paths": int(len(q)),
+                   "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
                    "output": f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}]",
-                   "step": "extract + merge + BFD pack + layout + upload + SHAP kernel"},
+                   "step": "extract + merge + bias + BFD pack (B=64) + layout + upload "
+                           "+ SHAP kernel"},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
-                     "traffic": TRAFFIC_BYTES.get((args.workload, dtype, "shap")),
-                     "kernel": "rowlane_kernel (SHAP)", "kernel_ms": kern_ms,
-                     "modelled_gflop_per_launch": flops / 1e9},
-        "kernel": {"rows_per_s": rows / (k_only_ms * 1e-3), "ms": k_only_ms},
+                     "traffic": traffic_for((args.workload, dtype, False)),
+                     "kernel": "shap_kernel", "kernel_ms": kern_ms,
+                     "kernel_ms_in_steps": float(kern.mean()),
+                     "modelled_gflop_per_launch": flops / 1e9,
+                     "note": "peak is the packed-FP32 vendor figure; FP32 code that is "
+                             "not packed issues at half of it"},
+        "kernel": {"rows_per_s": rows / (float(np.median(k_only)) * 1e-3),
+                   "ms_median": float(np.median(k_only)), "ms_mean": float(k_only.mean()),
+                   "ms_std": float(k_only.std()), "runs": len(k_only)},
     }
-    if not args.no_interactions and args.workload == "covtype_med":
-        wi = synth.workload("interactions")
-        Xi = torch.from_numpy(wi.X).cuda()
-        walli, kerni, _, modeli = time_pipeline(torch, gts, ens, Xi, "f32", max(3, args.steps // 4),
-                                                1, True)
-        si = max(3, args.steps // 4)
-        ki = time_kernel_only(torch, gts, modeli, Xi, si, True)
-        fi = modelled_flops(q, True) * wi.X.shape[0]
-        line["interactions"] = {
-            "value": wi.X.shape[0] * si / walli, "unit": "rows/s", "rows": wi.X.shape[0],
-            "ms_per_step": 1e3 * walli / si, "kernel_rows_per_s": wi.X.shape[0] / (ki * 1e-3),
-            "kernel_ms": kerni,
-            "roofline": {"bound": "alu", "achieved": fi / (kerni * 1e-3) / 1e12,
-                         "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-                         "frac": fi / (kerni * 1e-3) / 1e12 / PEAK_FP32_TFLOPS}}
+    if not args.no_suite:
+        line["configs"] = {name: suite_entry(torch, gts, synth, wl, dt, inter, args.suite_reps)
+                           for name, wl, dt, inter in SUITE}
     if not args.no_cpu_baseline:
         import oracle
         line["cpu_baseline"] = cpu_baseline(oracle, ens, w.X, args.cpu_budget, False)
