@@ -4,6 +4,9 @@
 // zero fractions and the bias are reproducible bit for bit.
 #include <algorithm>
 #include <atomic>
+#include <condition_variable>
+#include <mutex>
+#include <pthread.h>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -86,133 +89,261 @@ gts_status validate_ensemble(const gts_ensemble* e) {
   return GTS_OK;
 }
 
-// Reusable per-thread buffers for walking trees.
-struct Walker {
-  struct Frame {
-    int32_t node;
-    int32_t depth;
-    Split into;  // the split that leads to `node`
-  };
-  std::vector<Frame> stack;
-  std::vector<Split> path;    // splits from the root to the current node
-  std::vector<Split> merged;  // the current leaf's merged elements
-  std::vector<unsigned char> seen;
+// A small persistent pool of worker threads for the host passes (tree walks,
+// bin rotation).  run(n, body) calls body() on the caller and on up to n-1
+// workers at once; body pulls its work from a shared counter, so it is
+// correct with any number of participants.  One parallel region runs at a
+// time; a caller that finds the pool busy runs body() alone.  The pool is
+// never destroyed (its threads end with the process) and a forked child
+// starts a fresh one.
+class Pool {
+ public:
+  static Pool& get() {
+    static std::once_flag once;
+    std::call_once(once, [] { pthread_atfork(nullptr, nullptr, [] { instance() = nullptr; }); });
+    std::lock_guard<std::mutex> lock(create_mu());
+    if (instance() == nullptr) instance() = new Pool();
+    return *instance();
+  }
 
-  // Section 3.2: order the leaf's splits by feature (insertion sort is stable,
-  // so repeats stay in root-to-leaf order), then fold repeats into one
-  // element: intersect the ranges, multiply the zero fractions.
-  size_t merge(size_t depth) {
-    merged.resize(depth);
-    Split* s = merged.data();
-    for (size_t i = 0; i < depth; ++i) {
-      const Split key = path[i];
-      size_t j = i;
-      while (j > 0 && s[j - 1].feature > key.feature) {
-        s[j] = s[j - 1];
-        --j;
-      }
-      s[j] = key;
+  template <typename Body>
+  void run(int n, Body&& body) {
+    if (n <= 1 || !run_mu_.try_lock()) {
+      body();
+      return;
     }
-    size_t m = 0;
-    for (size_t i = 0; i < depth; ++i) {
-      if (m > 0 && s[m - 1].feature == s[i].feature) {
-        Split& acc = s[m - 1];
-        if (s[i].lower > acc.lower) acc.lower = s[i].lower;
-        if (s[i].upper < acc.upper) acc.upper = s[i].upper;
-        acc.zero_fraction = acc.zero_fraction * s[i].zero_fraction;
-      } else {
-        s[m] = s[i];
-        s[m].zero_fraction = 1.0 * s[i].zero_fraction;
-        ++m;
+    std::function<void()> fn(std::ref(body));
+    {
+      std::unique_lock<std::mutex> lock(mu_);
+      while ((int)workers_.size() < n - 1) {
+        const int id = (int)workers_.size();
+        workers_.emplace_back([this, id] { loop(id); });
+        workers_.back().detach();
       }
+      job_ = &fn;
+      want_ = n - 1;
+      pending_ = n - 1;
+      ++gen_;
     }
+    cv_.notify_all();
+    body();
+    {
+      std::unique_lock<std::mutex> lock(mu_);
+      done_.wait(lock, [this] { return pending_ == 0; });
+      job_ = nullptr;
+    }
+    run_mu_.unlock();
+  }
+
+ private:
+  static Pool*& instance() {
+    static Pool* p = nullptr;
+    return p;
+  }
+  static std::mutex& create_mu() {
+    static std::mutex m;
     return m;
   }
 
-  // Depth-first walk of tree t, left child (x < t) first.  Calls
-  // leaf(node, m) with `merged[0..m)` holding the leaf's merged elements.
-  template <typename LeafFn>
+  void loop(int id) {
+    uint64_t seen = 0;
+    std::unique_lock<std::mutex> lock(mu_);
+    for (;;) {
+      cv_.wait(lock, [&] { return gen_ != seen; });
+      seen = gen_;
+      if (id >= want_) continue;
+      const std::function<void()>* fn = job_;
+      lock.unlock();
+      (*fn)();
+      lock.lock();
+      if (--pending_ == 0) done_.notify_one();
+    }
+  }
+
+  std::mutex run_mu_, mu_;
+  std::condition_variable cv_, done_;
+  std::vector<std::thread> workers_;
+  const std::function<void()>* job_ = nullptr;
+  uint64_t gen_ = 0;
+  int want_ = 0;
+  int pending_ = 0;
+};
+
+// Per-thread state for walking trees depth first.  The merged elements of the
+// path from the root to the current node are kept up to date on the way down
+// and restored on the way up (Section 3.2): for every feature on the path,
+// the intersection of its ranges and the product of its zero fractions taken
+// in root-to-leaf order, and the features on the path in ascending order.
+struct Walker {
+  struct Frame {
+    int32_t node;
+    int32_t stage;  // 0: not entered yet, 1: in its left subtree, 2: in its right subtree
+  };
+  struct Undo {
+    int32_t feature;
+    float lower, upper;
+    double zero_fraction;
+  };
+  std::vector<Frame> stack;
+  std::vector<Undo> undo;
+  std::vector<int32_t> count;   // [M] splits on the path, per feature
+  std::vector<float> lower;     // [M]
+  std::vector<float> upper;     // [M]
+  std::vector<double> zf;       // [M]
+  std::vector<int32_t> active;  // features with count > 0, ascending
+  std::vector<Split> merged;    // the current leaf's merged elements
+  std::vector<unsigned char> seen;
+  bool clean = false;
+
+  void reset(int32_t M) {
+    const float inf = std::numeric_limits<float>::infinity();
+    if (!clean || (int32_t)count.size() != M) {
+      count.assign((size_t)M, 0);
+      lower.assign((size_t)M, -inf);
+      upper.assign((size_t)M, inf);
+      zf.assign((size_t)M, 1.0);
+      active.clear();
+    }
+    undo.clear();
+    stack.clear();
+    clean = false;
+  }
+
+  // Enter a split on feature f (range [lo, hi), cover ratio).  Without
+  // VALUES only the set of features on the path is kept.
+  template <bool VALUES>
+  void push(int32_t f, float lo, float hi, double ratio) {
+    const size_t i = (size_t)f;
+    if (VALUES) {
+      undo.push_back(Undo{f, lower[i], upper[i], zf[i]});
+      if (lo > lower[i]) lower[i] = lo;
+      if (hi < upper[i]) upper[i] = hi;
+      zf[i] = zf[i] * ratio;
+    } else {
+      undo.push_back(Undo{f, 0.0f, 0.0f, 0.0});
+    }
+    if (count[i]++ == 0) {
+      active.push_back(f);
+      size_t k = active.size() - 1;
+      for (; k > 0 && active[k - 1] > f; --k) active[k] = active[k - 1];
+      active[k] = f;
+    }
+  }
+
+  template <bool VALUES>
+  void pop() {
+    const Undo u = undo.back();
+    undo.pop_back();
+    const size_t i = (size_t)u.feature;
+    if (VALUES) {
+      lower[i] = u.lower;
+      upper[i] = u.upper;
+      zf[i] = u.zero_fraction;
+    }
+    if (--count[i] == 0) {
+      size_t k = 0;
+      while (active[k] != u.feature) ++k;
+      for (; k + 1 < active.size(); ++k) active[k] = active[k + 1];
+      active.pop_back();
+    }
+  }
+
+  // Depth-first walk of tree t, left child (x < t) first, validating every
+  // node it reaches.  Calls leaf(node, m) with m merged elements; with EMIT
+  // they are in merged[0..m), in ascending feature order (without EMIT only
+  // m is computed).
+  template <bool EMIT, typename LeafFn>
   gts_status walk(const gts_ensemble* e, int64_t t, LeafFn&& leaf) {
     const int64_t base = e->tree_node_offsets[t];
     const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
+    reset(e->num_features);
     seen.assign((size_t)n, 0);
-    stack.clear();
-    stack.push_back(Frame{0, 0, Split{}});
+    stack.push_back(Frame{0, 0});
     const float inf = std::numeric_limits<float>::infinity();
     while (!stack.empty()) {
-      const Frame fr = stack.back();
-      stack.pop_back();
+      Frame& fr = stack.back();
       const int32_t node = fr.node;
-      if (seen[(size_t)node])
-        return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
-                    (long long)t, node);
-      seen[(size_t)node] = 1;
-      if (path.size() < (size_t)fr.depth) path.resize((size_t)fr.depth);
-      if (fr.depth > 0) path[(size_t)fr.depth - 1] = fr.into;
       const int64_t gi = base + node;
-      const double r = e->cover[gi];
-      if (!(r >= 0.0) || !std::isfinite(r))
-        return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
-                    (long long)t, node);
-      const int32_t a = e->left[gi], b = e->right[gi];
-      if (a < 0 && b < 0) {
-        if (!std::isfinite(e->value[gi]))
-          return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
-        leaf(node, merge((size_t)fr.depth));
-        continue;
+      if (fr.stage == 0) {
+        if (seen[(size_t)node])
+          return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
+                      (long long)t, node);
+        seen[(size_t)node] = 1;
+        const double r = e->cover[gi];
+        if (!(r >= 0.0) || !std::isfinite(r))
+          return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
+                      (long long)t, node);
+        const int32_t a = e->left[gi], b = e->right[gi];
+        if (a < 0 && b < 0) {
+          if (!std::isfinite(e->value[gi]))
+            return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t,
+                        node);
+          const size_t m = active.size();
+          if (EMIT) {
+            merged.resize(m);
+            for (size_t i = 0; i < m; ++i) {
+              const size_t f = (size_t)active[i];
+              merged[i] = Split{active[i], lower[f], upper[f], zf[f]};
+            }
+          }
+          stack.pop_back();
+          leaf(node, m);
+          continue;
+        }
+        if (a < 0 || b < 0 || a >= n || b >= n)
+          return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
+                      node);
+        const int32_t d = e->feature[gi];
+        if (d < 0 || d >= e->num_features)
+          return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)",
+                      (long long)t, node, d, e->num_features);
+        const float th = e->threshold[gi];
+        if (std::isnan(th))
+          return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
+        fr.stage = 1;
+        push<EMIT>(d, -inf, th, EMIT ? cover_ratio(e->cover[base + a], r) : 0.0);
+        stack.push_back(Frame{a, 0});
+      } else if (fr.stage == 1) {
+        pop<EMIT>();
+        fr.stage = 2;
+        const int32_t b = e->right[gi];
+        push<EMIT>(e->feature[gi], e->threshold[gi], inf,
+                   EMIT ? cover_ratio(e->cover[base + b], e->cover[gi]) : 0.0);
+        stack.push_back(Frame{b, 0});
+      } else {
+        pop<EMIT>();
+        stack.pop_back();
       }
-      if (a < 0 || b < 0 || a >= n || b >= n)
-        return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
-                    node);
-      const int32_t d = e->feature[gi];
-      if (d < 0 || d >= e->num_features)
-        return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)", (long long)t,
-                    node, d, e->num_features);
-      const float th = e->threshold[gi];
-      if (std::isnan(th))
-        return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
-      const double ra = e->cover[base + a], rb = e->cover[base + b];
-      // the right child is pushed first so that the left child is visited first
-      stack.push_back(Frame{b, fr.depth + 1, Split{d, th, inf, cover_ratio(rb, r)}});
-      stack.push_back(Frame{a, fr.depth + 1, Split{d, -inf, th, cover_ratio(ra, r)}});
     }
+    clean = true;
     return GTS_OK;
   }
 };
 
-// Runs fn(t, walker) for every tree on up to `threads` threads (dynamic
-// chunks of trees); returns the per-tree statuses.
-template <typename Fn>
-void for_each_tree(int64_t T, int threads, std::vector<gts_status>& status, Fn&& fn) {
-  status.assign((size_t)T, GTS_OK);
-  if (threads <= 1) {
-    Walker w;
-    for (int64_t t = 0; t < T; ++t) status[(size_t)t] = fn(t, w);
-    return;
-  }
-  std::atomic<int64_t> next{0};
-  constexpr int64_t kChunk = 8;
-  auto worker = [&]() {
-    Walker w;
-    for (;;) {
-      const int64_t a = next.fetch_add(kChunk);
-      if (a >= T) break;
-      const int64_t b = std::min(T, a + kChunk);
-      for (int64_t t = a; t < b; ++t) status[(size_t)t] = fn(t, w);
-    }
-  };
-  std::vector<std::thread> pool;
-  pool.reserve((size_t)threads - 1);
-  for (int i = 1; i < threads; ++i) pool.emplace_back(worker);
-  worker();
-  for (auto& th : pool) th.join();
-}
-
-int host_threads(int64_t work_items) {
+int host_threads(int64_t work) {
   unsigned hw = std::thread::hardware_concurrency();
   if (hw == 0) hw = 1;
-  const int64_t by_work = (work_items + 31) / 32;  // at least ~32 trees per thread
+  const int64_t by_work = (work + 1023) / 1024;  // at least ~1k nodes (or elements) a thread
   return (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)hw, 16, by_work}));
+}
+
+// Runs fn(t, walker) for every tree on the pool (dynamic chunks of trees);
+// returns the per-tree statuses.
+template <typename Fn>
+void for_each_tree(const gts_ensemble* e, std::vector<gts_status>& status, Fn&& fn) {
+  const int64_t T = e->num_trees;
+  status.assign((size_t)T, GTS_OK);
+  std::atomic<int64_t> next{0};
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(8, T / 64));
+  Pool::get().run(host_threads(e->num_nodes), [&]() {
+    static thread_local Walker w;
+    for (;;) {
+      const int64_t a = next.fetch_add(chunk);
+      if (a >= T) break;
+      const int64_t b = std::min(T, a + chunk);
+      for (int64_t t = a; t < b; ++t) status[(size_t)t] = fn(t, w);
+    }
+  });
 }
 
 }  // namespace
@@ -238,13 +369,12 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
   if (st != GTS_OK) return st;
   try {
     const int64_t T = ens->num_trees;
-    const int threads = host_threads(T);
     // pass 1: elements and paths per tree
     std::vector<int64_t> tree_elems((size_t)T + 1, 0), tree_paths((size_t)T + 1, 0);
     std::vector<gts_status> status;
-    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+    for_each_tree(ens, status, [&](int64_t t, Walker& w) {
       int64_t ne = 0, np = 0;
-      gts_status s = w.walk(ens, t, [&](int32_t, size_t m) {
+      gts_status s = w.walk<false>(ens, t, [&](int32_t, size_t m) {
         ne += (int64_t)m + 1;
         ++np;
       });
@@ -256,7 +386,7 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
       if (status[(size_t)t] != GTS_OK) {
         // re-walk the first bad tree here so the message is this thread's
         Walker w;
-        return w.walk(ens, t, [](int32_t, size_t) {});
+        return w.walk<false>(ens, t, [](int32_t, size_t) {});
       }
     }
     for (int64_t t = 0; t < T; ++t) {
@@ -274,13 +404,13 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
                   (long long)n);
     // pass 2: write the elements; keep each path's bias term v * prod(z)
     std::vector<double> term(bias ? (size_t)paths : 0);
-    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+    for_each_tree(ens, status, [&](int64_t t, Walker& w) {
       const int64_t base = ens->tree_node_offsets[t];
       const int32_t group = ens->tree_group[t];
       int64_t k = tree_elems[(size_t)t];
       int64_t p = tree_paths[(size_t)t];
       const float inf = std::numeric_limits<float>::infinity();
-      return w.walk(ens, t, [&](int32_t leaf, size_t m) {
+      return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
         if (bias) {
           double prod = 1.0;
@@ -459,22 +589,28 @@ void assign_bins(const int32_t* size, const int32_t* group, int64_t P, int32_t c
     while (j < order.size() && group[order[j]] == g) ++j;
     const int64_t first_bin = K;
     if (alg == GTS_PACK_BFD) {
+      // open bins by residual r in [1, cap]: a min-heap of bin numbers each,
+      // and bit r-1 of `open` set when that heap is not empty
       for (BinHeap& h : by_resid) h.clear();
+      uint64_t open = 0;
       for (size_t k = i; k < j; ++k) {
         const int32_t s = size[order[k]];
-        int64_t b = -1;
-        int32_t r = s;
-        for (; r <= cap; ++r)
-          if (!by_resid[(size_t)r].empty()) {
-            b = heap_pop(by_resid[(size_t)r]);
-            break;
-          }
-        if (b < 0) {
+        int64_t b;
+        int32_t r;
+        const uint64_t fit = s >= 1 ? open >> (s - 1) : open;
+        if (fit != 0) {
+          r = s + __builtin_ctzll(fit);
+          b = heap_pop(by_resid[(size_t)r]);
+          if (by_resid[(size_t)r].empty()) open &= ~(1ull << (r - 1));
+        } else {
           b = K++;
           r = cap;
         }
         const int32_t left = r - s;
-        if (left > 0) heap_push(by_resid[(size_t)left], b);
+        if (left > 0) {
+          heap_push(by_resid[(size_t)left], b);
+          open |= 1ull << (left - 1);
+        }
         bin_of[(size_t)order[k]] = b;
       }
     } else if (alg == GTS_PACK_FFD) {
@@ -636,18 +772,34 @@ void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t 
     if (q > 1) {
       const int32_t* f = feat + a + 1;
       int32_t best = 0, best_cost = INT32_MAX;
-      for (int32_t i = 0; i < q; ++i) {
-        const int32_t rho = (t + i) % q;
-        int32_t cost = 0;
-        for (int32_t k = 0; k < q; ++k) cost += (int32_t)((used[(size_t)f[(k + rho) % q]] >> k) & 1u);
-        if (cost < best_cost) {
-          best_cost = cost;
-          best = rho;
-          if (cost == 0) break;
+      // cost[rho]: collisions if element j goes to position (j - rho) mod q;
+      // only features an earlier path of the bin has at some position < q
+      // contribute
+      int32_t cost[kMaxPathLen];
+      for (int32_t k = 0; k < q; ++k) cost[k] = 0;
+      const uint64_t in_q = q >= 64 ? ~0ull : (1ull << q) - 1;
+      for (int32_t j = 0; j < q; ++j) {
+        uint64_t bits = used[(size_t)f[j]] & in_q;
+        while (bits) {
+          const int32_t k = __builtin_ctzll(bits);
+          bits &= bits - 1;
+          const int32_t rho = j >= k ? j - k : j - k + q;
+          ++cost[rho];
         }
       }
-      for (int32_t k = 0; k < q; ++k) {
-        const int64_t src = a + 1 + (k + best) % q;
+      int32_t rho = t % q;
+      for (int32_t i = 0; i < q; ++i) {
+        if (cost[rho] < best_cost) {
+          best_cost = cost[rho];
+          best = rho;
+          if (best_cost == 0) break;
+        }
+        if (++rho == q) rho = 0;
+      }
+      int32_t src_k = best;
+      for (int32_t k = 0; k < q; ++k, ++src_k) {
+        if (src_k == q) src_k = 0;
+        const int64_t src = a + 1 + src_k;
         fbuf[k] = feat[src];
         lbuf[k] = lo[src];
         hbuf[k] = hi[src];
@@ -672,15 +824,14 @@ void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t 
   touched.clear();
 }
 
-// Applies rotate_bin to every bin of a written blob, bins spread over threads.
+// Applies rotate_bin to every bin of a written blob, bins spread over the pool.
 void rotate_bins(const gts_model& m, char* blob, const int64_t* bin_offsets) {
   int32_t* feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]);
   float* lo = reinterpret_cast<float*>(blob + m.off[kLower]);
   float* hi = reinterpret_cast<float*>(blob + m.off[kUpper]);
   const int64_t K = m.num_bins;
-  const int threads = (int)std::max<int64_t>(1, std::min<int64_t>(host_threads(K / 8), 16));
   std::atomic<int64_t> next{0};
-  auto worker = [&]() {
+  Pool::get().run(host_threads(m.num_elements), [&]() {
     std::vector<uint64_t> used((size_t)m.num_features, 0);
     std::vector<int32_t> touched;
     constexpr int64_t kChunk = 64;
@@ -697,11 +848,7 @@ void rotate_bins(const gts_model& m, char* blob, const int64_t* bin_offsets) {
                      bin_offsets[b + 1], used, touched);
       }
     }
-  };
-  std::vector<std::thread> pool;
-  for (int i = 1; i < threads; ++i) pool.emplace_back(worker);
-  worker();
-  for (auto& th : pool) th.join();
+  });
 }
 
 }  // namespace
@@ -851,19 +998,18 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
   if (st != GTS_OK) return st;
   try {
     const int64_t T = ens->num_trees;
-    const int threads = host_threads(T);
     // walk 1: the merged length of every path, per tree
     std::vector<std::vector<int32_t>> tree_sizes((size_t)T);
     std::vector<gts_status> status;
-    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+    for_each_tree(ens, status, [&](int64_t t, Walker& w) {
       std::vector<int32_t>& sz = tree_sizes[(size_t)t];
       sz.clear();
-      return w.walk(ens, t, [&](int32_t, size_t m) { sz.push_back((int32_t)m + 1); });
+      return w.walk<false>(ens, t, [&](int32_t, size_t m) { sz.push_back((int32_t)m + 1); });
     });
     for (int64_t t = 0; t < T; ++t)
       if (status[(size_t)t] != GTS_OK) {
         Walker w;
-        return w.walk(ens, t, [](int32_t, size_t) {});
+        return w.walk<false>(ens, t, [](int32_t, size_t) {});
       }
     std::vector<int64_t> tree_first((size_t)T + 1, 0);
     for (int64_t t = 0; t < T; ++t)
@@ -900,10 +1046,10 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     // walk 2: each path's elements straight to their packed position
     std::vector<double> term((size_t)P);
     const float inf = std::numeric_limits<float>::infinity();
-    for_each_tree(T, threads, status, [&](int64_t t, Walker& w) {
+    for_each_tree(ens, status, [&](int64_t t, Walker& w) {
       const int64_t base = ens->tree_node_offsets[t];
       int64_t p = tree_first[(size_t)t];
-      return w.walk(ens, t, [&](int32_t leaf, size_t m) {
+      return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
         double prod = 1.0;
         for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
