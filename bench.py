@@ -66,14 +66,32 @@ SUITE = [
 # HBM traffic of the SHAP kernel per launch, from rocprofv3 --pmc FETCH_SIZE
 # and --pmc WRITE_SIZE runs of `bench.py --copy-probe`, each scaled by the
 # ratio of a plain 256 MiB copy's true bytes to the counter's reading of it.
-# Keyed by (workload, dtype, interactions); `source` is the SHA-256 of the
-# kernel source the counters were taken on.
-TRAFFIC = {}
+# Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
+# of the kernel source the counters were taken on.
+TRAFFIC = {
+    ("covtype_med", "f32", False): {"fetch_bytes": 18700998, "write_bytes": 35200000,
+                                    "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
+    ("interactions", "f32", True): {"fetch_bytes": 3321833, "write_bytes": 96800000,
+                                    "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
+    ("deep", "f32", False): {"fetch_bytes": 43088220, "write_bytes": 11520000,
+                             "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
+    ("deep", "f64", False): {"fetch_bytes": 57125688, "write_bytes": 17280000,
+                             "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
+    ("wide", "f32", False): {"fetch_bytes": 6322184028, "write_bytes": 316800000,
+                             "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
+}
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """SHA-256 of the kernel source's code: line comments and blank lines are
+    dropped, so editing a comment keeps the measured traffic."""
+    code = []
+    with open(KERNEL_SOURCE) as f:
+        for line in f:
+            c = line.split("//", 1)[0].rstrip()
+            if c.strip():
+                code.append(c)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()
 
 
 def traffic_for(key):
@@ -244,7 +262,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="covtype_med",
-                    choices=["tiny", "covtype_med", "deep", "wide"])
+                    choices=["tiny", "covtype_med", "deep", "wide", "interactions"],
+                    help="the batch one step explains (interactions: the interaction kernel "
+                         "on the covtype-shaped model)")
     ap.add_argument("--dtype", default=None, choices=["f32", "f64"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-suite", action="store_true",
@@ -272,6 +292,7 @@ def main():
         copy_probe(torch)
 
     w = synth.workload(args.workload)
+    inter = args.workload == "interactions"
     dtype = args.dtype or w.dtype
     ens = w.ensemble
     rows = w.X.shape[0]
@@ -279,14 +300,14 @@ def main():
     q = path_features(gts, ens)
 
     wall, kern, out, model = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                           args.warmup, False)
+                                           args.warmup, inter)
     # The roofline takes the kernel's mean launch duration from back-to-back
     # launches (each bracketed by HIP events on its stream).  Inside the
     # whole-path steps the GPU idles while the host prepares the next model,
     # so there the events also hold the host's launch latency.
-    k_only = time_kernel(torch, gts, model, Xd, max(5, args.steps), False)
+    k_only = time_kernel(torch, gts, model, Xd, max(5, args.steps), inter)
     kern_ms = float(k_only.mean())
-    flops = modelled_flops(q, False) * rows
+    flops = modelled_flops(q, inter) * rows
     peak = PEAK_FP64_TFLOPS if dtype == "f64" else PEAK_FP32_TFLOPS
     achieved = flops / (kern_ms * 1e-3) / 1e12
     line = {
@@ -298,13 +319,15 @@ def main():
         "config": {"workload": WORKLOAD_TEXT[args.workload], "rows": rows,
                    "trees": int(ens.num_trees), "paths": int(len(q)),
                    "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
-                   "output": f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}]",
+                   "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
+                              + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": "extract + merge + bias + BFD pack (B=64) + layout + upload "
-                           "+ SHAP kernel"},
+                           + ("+ interaction kernel" if inter else "+ SHAP kernel")},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
-                     "traffic": traffic_for((args.workload, dtype, False)),
-                     "kernel": "shap_kernel", "kernel_ms": kern_ms,
+                     "traffic": traffic_for((args.workload, dtype, inter)),
+                     "kernel": "shap_kernel" + (" (interactions)" if inter else ""),
+                     "kernel_ms": kern_ms,
                      "kernel_ms_in_steps": float(kern.mean()),
                      "modelled_gflop_per_launch": flops / 1e9,
                      "note": "peak is the packed-FP32 vendor figure; FP32 code that is "
@@ -318,7 +341,7 @@ def main():
                            for name, wl, dt, inter in SUITE}
     if not args.no_cpu_baseline:
         import oracle
-        line["cpu_baseline"] = cpu_baseline(oracle, ens, w.X, args.cpu_budget, False)
+        line["cpu_baseline"] = cpu_baseline(oracle, ens, w.X, args.cpu_budget, inter)
     print(json.dumps(line), flush=True)
 
 

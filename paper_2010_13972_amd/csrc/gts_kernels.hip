@@ -4,18 +4,20 @@
 // Work units.  The model arrives packed into bins of at most 64 path
 // elements (Section 3.3, Best-Fit-Decreasing).  A wave takes one bin at a
 // time and loads it with one element per lane -- the element-per-thread layout
-// of the paper's kernel -- prefetching the next bin while it computes.  A
-// ballot over "is a root element" marks where each path starts.
+// of the paper's kernel -- prefetching the next bin while it computes.  It
+// copies the bin into a per-wave staging area in LDS, and a ballot over "is a
+// root element" gives the lane where each path starts.
 //
 // Lanes.  Unlike the paper's kernel, a lane does not own a path element: it
 // owns a (row, path) pair and runs the whole per-path dynamic programme of
 // Algorithm 1 in its registers.  A wave covers RW rows x (64/RW) paths.  With
-// RW == 64 all lanes share one path, whose elements are broadcast from the
-// bin's lanes with v_readlane into scalar registers; with fewer rows per wave
-// each lane pulls its own path's elements with ds_bpermute.  Trip counts are
-// compile-time constants (one variant per path length up to 16 features), so
-// a wave never diverges on path length.  This does the q^2 work of a path once
-// per row instead of spreading it over q lanes that then need q shuffles each.
+// RW == 64 all lanes share one path and read its elements from the staging
+// area at the same address (an LDS broadcast); with fewer rows per wave each
+// group of RW lanes reads its own path's elements.  Trip counts are
+// compile-time constants (one variant per path length up to 16 features, 8
+// for interactions), so a wave never diverges on path length.  This does the
+// q^2 work of a path once per row instead of spreading it over q lanes that
+// then need q shuffles each.
 //
 // Arithmetic.  EXTEND keeps permutation weights w_k, which are the
 // coefficients E_k of prod_k (z_k + o_k t) scaled by k!(l-k)!/(l+1)!.  The
@@ -514,10 +516,11 @@ __device__ __forceinline__ void process_bin(Stage<T>* st, const Bin<T>& b, int l
 // One workgroup: rows [tile*RW, tile*RW + RW) of output group g, bins of
 // slice s of that group.  PRIV: every wave accumulates into a phi tile of its
 // own (summed when the tile is written), so waves never contend; with one
-// path per wave (RW == 64) the accumulation then needs no atomics.  Workgroups are dealt to the 8 XCDs round-robin; when
-// the (group, slice) units divide evenly among the XCDs, consecutive
-// workgroups on an XCD take the same unit for successive row tiles, so each
-// XCD's L2 holds only its own part of the model.
+// path per wave (RW == 64) the accumulation then needs no atomics.
+// Workgroups are dealt to the 8 XCDs round-robin; when the (group, slice)
+// units divide evenly among the XCDs, consecutive workgroups on an XCD take
+// the same unit for successive row tiles, so each XCD's L2 holds only its own
+// part of the model.
 template <typename T, int RW, bool INTER, int WAVES, bool PRIV>
 __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const float* __restrict__ X,
                                                          T* __restrict__ phi, Launch L) {
