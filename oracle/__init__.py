@@ -187,20 +187,27 @@ class Oracle:
         el["zero_fraction"], el["v"] = cols["zero"], cols["v"]
         return el, int(n_paths.value), bias
 
-    def pack_bfd(self, sizes, groups, capacity: int = 64):
-        """Best-Fit-Decreasing per group.  Returns (bin_of[p], lane_of[p], num_bins)."""
+    def pack(self, sizes, groups, capacity: int = 64, alg: str = "bfd"):
+        """Bin packing of Section 3.3 per group with alg in {"bfd", "ffd", "nf",
+        "none"}.  Returns (bin_of[p], lane_of[p], num_bins)."""
+        if alg not in ("bfd", "ffd", "nf", "none"):
+            raise ValueError(f"unknown packing algorithm {alg!r}")
         sizes = np.ascontiguousarray(sizes, np.int32)
         groups = np.ascontiguousarray(groups, np.int32)
         n = sizes.shape[0]
         bin_of = np.zeros(n, np.int64)
         lane_of = np.zeros(n, np.int32)
-        f = self._lib.or_pack_bfd
+        f = getattr(self._lib, "or_pack_" + alg)
         f.restype = ctypes.c_int64
         k = f(ctypes.c_int64(n), _p(sizes), _p(groups), ctypes.c_int32(capacity),
               _p(bin_of), _p(lane_of))
         if k < 0:
             raise ValueError("an item is larger than the bin capacity")
         return bin_of, lane_of, int(k)
+
+    def pack_bfd(self, sizes, groups, capacity: int = 64):
+        """Best-Fit-Decreasing per group.  Returns (bin_of[p], lane_of[p], num_bins)."""
+        return self.pack(sizes, groups, capacity, "bfd")
 
 
 def __getattr__(name):

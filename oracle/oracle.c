@@ -24,8 +24,9 @@
  *       pair), by subset enumeration; also its Eq. (3)-(6) counterpart.
  *   or_extract_paths
  *       Section 3.1-3.2: unique root-to-leaf paths, duplicates merged.
- *   or_pack_bfd
- *       Section 3.3: Best-Fit-Decreasing bin packing of path lengths.
+ *   or_pack_bfd, or_pack_ffd, or_pack_nf, or_pack_none
+ *       Section 3.3 and Table 1: Best-Fit-Decreasing, First-Fit-Decreasing,
+ *       Next-Fit and one-path-per-bin packing of path lengths.
  *
  * Readings of points the paper leaves open (each applied on both sides):
  *   - a split sends x left iff x < threshold (Section 3.1's half-open ranges),
@@ -780,5 +781,114 @@ OR_EXPORT int64_t or_pack_bfd(int64_t n, const int32_t *size,
   }
   free(resid);
   free(it);
+  return nbins;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Section 3.3 / Table 1: the other packing heuristics                       */
+/* ------------------------------------------------------------------------ */
+/*
+ * First-Fit-Decreasing: the processing order of or_pack_bfd (by group, then
+ * non-increasing size, then ascending path index); each item goes to the
+ * lowest-numbered open bin of its group that still holds it, else a new bin.
+ * Same outputs and return value as or_pack_bfd.
+ */
+OR_EXPORT int64_t or_pack_ffd(int64_t n, const int32_t *size,
+                              const int32_t *group, int32_t capacity,
+                              int64_t *bin_of, int32_t *lane_of) {
+  item_t *it = (item_t *)malloc(sizeof(item_t) * (size_t)(n > 0 ? n : 1));
+  for (int64_t p = 0; p < n; p++) {
+    if (size[p] < 1 || size[p] > capacity) { free(it); return -1; }
+    it[p].size = size[p];
+    it[p].group = group[p];
+    it[p].idx = p;
+  }
+  qsort(it, (size_t)n, sizeof(item_t), cmp_item);
+  int32_t *resid = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+  int64_t nbins = 0, group_first_bin = 0;
+  int32_t cur_group = n > 0 ? it[0].group : 0;
+  for (int64_t k = 0; k < n; k++) {
+    if (it[k].group != cur_group) {
+      cur_group = it[k].group;
+      group_first_bin = nbins;
+    }
+    const int32_t s = it[k].size;
+    int64_t first = -1;
+    for (int64_t b = group_first_bin; b < nbins; b++) {
+      if (resid[b] >= s) { first = b; break; }
+    }
+    if (first < 0) {
+      first = nbins++;
+      resid[first] = capacity;
+    }
+    bin_of[it[k].idx] = first;
+    lane_of[it[k].idx] = capacity - resid[first];
+    resid[first] -= s;
+  }
+  free(resid);
+  free(it);
+  return nbins;
+}
+
+/*
+ * Next-Fit: items in path order within each group (groups ascending); one bin
+ * is open at a time, and an item that does not fit in it closes it and opens
+ * a new one.  A new group always starts a new bin.  Same outputs as
+ * or_pack_bfd.
+ */
+OR_EXPORT int64_t or_pack_nf(int64_t n, const int32_t *size,
+                             const int32_t *group, int32_t capacity,
+                             int64_t *bin_of, int32_t *lane_of) {
+  for (int64_t p = 0; p < n; p++)
+    if (size[p] < 1 || size[p] > capacity) return -1;
+  int64_t nbins = 0;
+  /* groups ascending: visit the distinct group ids in increasing order */
+  int32_t g = INT32_MIN;
+  for (;;) {
+    int found = 0;
+    int32_t next = 0;
+    for (int64_t p = 0; p < n; p++)
+      if (group[p] > g && (!found || group[p] < next)) { next = group[p]; found = 1; }
+    if (!found) break;
+    g = next;
+    int32_t resid = -1; /* no open bin in this group yet */
+    for (int64_t p = 0; p < n; p++) {
+      if (group[p] != g) continue;
+      if (resid < size[p]) {
+        nbins++;
+        resid = capacity;
+      }
+      bin_of[p] = nbins - 1;
+      lane_of[p] = capacity - resid;
+      resid -= size[p];
+    }
+  }
+  return nbins;
+}
+
+/*
+ * The "none" baseline of Table 5: every path alone in its own bin, bins in
+ * the order of (group, path index).  Same outputs as or_pack_bfd.
+ */
+OR_EXPORT int64_t or_pack_none(int64_t n, const int32_t *size,
+                               const int32_t *group, int32_t capacity,
+                               int64_t *bin_of, int32_t *lane_of) {
+  for (int64_t p = 0; p < n; p++)
+    if (size[p] < 1 || size[p] > capacity) return -1;
+  int64_t nbins = 0;
+  int32_t g = INT32_MIN;
+  for (;;) {
+    int found = 0;
+    int32_t next = 0;
+    for (int64_t p = 0; p < n; p++)
+      if (group[p] > g && (!found || group[p] < next)) { next = group[p]; found = 1; }
+    if (!found) break;
+    g = next;
+    for (int64_t p = 0; p < n; p++) {
+      if (group[p] != g) continue;
+      bin_of[p] = nbins++;
+      lane_of[p] = 0;
+    }
+  }
   return nbins;
 }

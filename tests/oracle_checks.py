@@ -348,10 +348,138 @@ def check_bfd_properties(orc):
         raise AssertionError("an item larger than the capacity must be rejected")
 
 
+def check_golden_packers(orc):
+    with open(os.path.join(GOLDEN, "bin_packing.json")) as f:
+        fx = json.load(f)["other_algorithms"]
+    for case in fx["cases"]:
+        b, l, k = orc.pack(case["sizes"], case["groups"], case["capacity"], case["alg"])
+        assert k == case["num_bins"], (case["why"], k)
+        assert list(b) == case["bin_of"], (case["why"], list(b))
+        assert list(l) == case["lane_of"], (case["why"], list(l))
+    t5 = fx["table5_adult_small"]
+    sizes = np.full(80, 4)
+    groups = np.zeros(80)
+    for cap, key in ((32, "bins_at_32"), (64, "bins_at_64")):
+        for alg, want in t5[key].items():
+            assert orc.pack(sizes, groups, cap, alg)[2] == want, (alg, cap)
+
+
+def _processing_order(sizes, groups, decreasing):
+    """Items in the order the heuristics of Section 3.3 take them: by group,
+    then (decreasing algorithms) non-increasing size, then path index."""
+    n = len(sizes)
+    if decreasing:
+        return sorted(range(n), key=lambda p: (groups[p], -sizes[p], p))
+    return sorted(range(n), key=lambda p: (groups[p], p))
+
+
+def verify_greedy_packing(alg, sizes, groups, cap, bin_of, lane_of, k):
+    """Checks a packing against the rule of its heuristic, one placement at a
+    time: bins are visited in the processing order and every choice is
+    compared with the rule's requirement on the residuals at that moment."""
+    order = _processing_order(sizes, groups, alg in ("bfd", "ffd"))
+    fill = {}            # bin -> lanes used so far
+    group_of_bin = {}
+    opened = 0
+    current = None       # NF: the open bin
+    for p in order:
+        s, g, b = int(sizes[p]), int(groups[p]), int(bin_of[p])
+        mine = [c for c in range(opened) if group_of_bin[c] == g]
+        fits = [c for c in mine if cap - fill[c] >= s]
+        if alg == "none":
+            want = None
+        elif alg == "nf":
+            want = current if (current is not None and group_of_bin[current] == g
+                               and cap - fill[current] >= s) else None
+        elif alg == "ffd":
+            want = fits[0] if fits else None
+        else:  # bfd: smallest residual, then lowest bin
+            want = min(fits, key=lambda c: (cap - fill[c], c)) if fits else None
+        if want is None:
+            assert b == opened, (alg, "a new bin is numbered in opening order", p)
+            group_of_bin[b] = g
+            fill[b] = 0
+            opened += 1
+        else:
+            assert b == want, (alg, "rule picks another bin", p, b, want)
+        assert lane_of[p] == fill[b], (alg, "lanes in placement order", p)
+        fill[b] += s
+        assert fill[b] <= cap
+        current = b
+    assert opened == k
+
+
+def check_packer_rules(orc):
+    rng = np.random.default_rng(11)
+    for trial in range(24):
+        n = int(rng.integers(1, 120))
+        cap = int(rng.choice([8, 10, 32, 64]))
+        sizes = rng.integers(1, cap + 1, size=n)
+        if trial % 3 == 0:   # many equal sizes: tie rules decide
+            sizes = rng.integers(max(1, cap // 4), max(2, cap // 4) + 2, size=n)
+        groups = rng.integers(0, 1 + trial % 3, size=n)
+        for alg in ("bfd", "ffd", "nf", "none"):
+            b, l, k = orc.pack(sizes, groups, cap, alg)
+            verify_greedy_packing(alg, sizes, groups, cap, b, l, k)
+
+
+def _optimum_bins(sizes, cap):
+    """Fewest bins for a handful of items, by exhaustive search."""
+    sizes = sorted(sizes, reverse=True)
+    best = [len(sizes)]
+
+    def place(i, fills):
+        if len(fills) >= best[0]:
+            return
+        if i == len(sizes):
+            best[0] = len(fills)
+            return
+        seen = set()
+        for c in range(len(fills)):
+            if fills[c] + sizes[i] <= cap and fills[c] not in seen:
+                seen.add(fills[c])
+                fills[c] += sizes[i]
+                place(i + 1, fills)
+                fills[c] -= sizes[i]
+        fills.append(sizes[i])
+        place(i + 1, fills)
+        fills.pop()
+
+    place(0, [])
+    return best[0]
+
+
+def check_packer_bounds(orc):
+    """Table 1: worst-case ratios against the optimum -- Next-Fit 2, FFD and BFD
+    11/9 (with the additive 6/9); exhaustive optima on small instances."""
+    rng = np.random.default_rng(5)
+    for trial in range(40):
+        n = int(rng.integers(1, 9))
+        cap = int(rng.choice([6, 10, 16]))
+        sizes = rng.integers(1, cap + 1, size=n)
+        opt = _optimum_bins(sizes.tolist(), cap)
+        zeros = np.zeros(n)
+        assert opt >= math.ceil(sizes.sum() / cap)
+        for alg in ("bfd", "ffd"):
+            k = orc.pack(sizes, zeros, cap, alg)[2]
+            assert opt <= k <= 11 * opt / 9 + 6 / 9, (alg, sizes.tolist(), cap, k, opt)
+        k = orc.pack(sizes, zeros, cap, "nf")[2]
+        assert opt <= k <= 2 * opt, ("nf", sizes.tolist(), cap, k, opt)
+        assert orc.pack(sizes, zeros, cap, "none")[2] == n
+    for alg in ("ffd", "nf", "none"):
+        try:
+            orc.pack([65], [0], 64, alg)
+        except ValueError:
+            pass
+        else:
+            raise AssertionError(f"{alg}: an item larger than the capacity must be rejected")
+
+
 ALL_CHECKS = [
     check_golden_shap, check_golden_interactions, check_golden_paths,
     check_golden_path_games, check_golden_bfd, check_stumps, check_symmetry_axiom,
     check_random_routes_agree, check_local_accuracy, check_interaction_properties,
     check_bias_is_background_mean, check_single_path_closed_forms, check_path_linearity,
-    check_extraction_invariants, check_bfd_properties,
+    check_extraction_invariants, check_bfd_properties, check_golden_packers,
+    check_packer_rules, check_packer_bounds,
 ]

@@ -79,10 +79,10 @@ def _paths_of(el):
     return roots, sizes, el["group"][roots]
 
 
-def _check_pack_against_oracle(orc, el, cap):
-    packed, offs = gts.pack_paths(el, cap, "bfd")
+def _check_pack_against_oracle(orc, el, cap, alg="bfd"):
+    packed, offs = gts.pack_paths(el, cap, alg)
     roots, sizes, groups = _paths_of(el)
-    bin_of, lane_of, k = orc.pack_bfd(sizes, groups, cap)
+    bin_of, lane_of, k = orc.pack(sizes, groups, cap, alg)
     assert len(offs) == k + 1
     # rebuild the oracle's packed element order and compare raw bytes
     order = np.lexsort((lane_of, bin_of))
@@ -94,24 +94,37 @@ def _check_pack_against_oracle(orc, el, cap):
 
 @pytest.mark.parametrize("name", EXTRACT_CASES)
 @pytest.mark.parametrize("cap", [64, 32, 17])
-def test_pack_paths_bitwise_equal_to_oracle_bfd(orc, name, cap):
+@pytest.mark.parametrize("alg", ["bfd", "ffd", "nf", "none"])
+def test_pack_paths_bitwise_equal_to_oracle(orc, name, cap, alg):
     w = _workload(name)
     el, _, _ = gts.extract_paths(w.ensemble)
     if int(np.max(_paths_of(el)[1])) > cap:
         with pytest.raises(gts.GtsError) as e:
-            gts.pack_paths(el, cap, "bfd")
+            gts.pack_paths(el, cap, alg)
         assert e.value.status == gts.GTS_EPATHLEN
         return
-    _check_pack_against_oracle(orc, el, cap)
+    _check_pack_against_oracle(orc, el, cap, alg)
+
+
+@pytest.mark.parametrize("alg", ["bfd", "ffd", "nf", "none"])
+def test_pack_shuffled_groups_bitwise_equal_to_oracle(orc, alg):
+    """Trees of several output groups interleaved in input order."""
+    rng = np.random.default_rng(8)
+    sizes = rng.integers(1, 65, size=700)
+    groups = rng.integers(0, 5, size=700)
+    el = _synthetic_elements(sizes, groups)
+    _check_pack_against_oracle(orc, el, 64, alg)
 
 
 def test_pack_golden_instances(orc):
-    """The hand-worked BFD instances, run through the library."""
+    """The hand-worked packing instances (BFD, FFD, NF, none), run through the
+    library."""
     import json
     fx = json.load(open(os.path.join(ROOT, "tests", "golden", "bin_packing.json")))
-    for case in fx["cases"]:
+    cases = [dict(c, alg="bfd") for c in fx["cases"]] + fx["other_algorithms"]["cases"]
+    for case in cases:
         el = _synthetic_elements(case["sizes"], case["groups"])
-        packed, offs = gts.pack_paths(el, case["capacity"], "bfd")
+        packed, offs = gts.pack_paths(el, case["capacity"], case["alg"])
         assert len(offs) - 1 == case["num_bins"]
         roots = np.flatnonzero(el["feature_idx"] == -1)
         for p, (b, lane) in enumerate(zip(case["bin_of"], case["lane_of"])):
@@ -318,7 +331,7 @@ def test_device_calls_reject_bad_arguments_without_touching_the_gpu():
 
 @pytest.mark.parametrize("name", ["tiny", "covtype_med", "wide", "random0", "random2"])
 @pytest.mark.parametrize("dtype", ["f32", "f64"])
-@pytest.mark.parametrize("alg", ["bfd", "nf"])
+@pytest.mark.parametrize("alg", ["bfd", "ffd", "nf", "none"])
 def test_prepare_model_equals_the_three_step_route(name, dtype, alg):
     """gts_prepare_model writes byte for byte the blob and descriptor of
     gts_model_layout(gts_pack_paths(gts_extract_paths(.)))."""

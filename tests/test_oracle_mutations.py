@@ -60,7 +60,16 @@ MUTATIONS = [
      "if (best < 0) best = b;", 1),
     ("bfd_ties_by_descending_index", "return (x->idx > y->idx) - (x->idx < y->idx);",
      "return (x->idx < y->idx) - (x->idx > y->idx);", 1),
-    ("bfd_mixes_groups", "group_first_bin = nbins;\n", "\n", 1),
+    ("bfd_mixes_groups", "group_first_bin = nbins;\n", "\n", 2),
+    ("ffd_takes_last_fit", "if (resid[b] >= s) { first = b; break; }",
+     "if (resid[b] >= s) { first = b; }", 1),
+    ("ffd_lane_after_placement", "lane_of[it[k].idx] = capacity - resid[first];\n    resid[first] -= s;",
+     "resid[first] -= s;\n    lane_of[it[k].idx] = capacity - resid[first];", 1),
+    ("nf_closes_exactly_fitting_bin", "if (resid < size[p]) {", "if (resid <= size[p]) {", 1),
+    ("nf_keeps_bin_across_groups", "int32_t resid = -1; /* no open bin in this group yet */",
+     "static int32_t resid = -1;", 1),
+    ("none_bins_in_path_order_only", "      if (group[p] != g) continue;\n      bin_of[p] = nbins++;",
+     "      if (group[p] != g) continue;\n      bin_of[p] = p;\n      nbins++;", 1),
 ]
 
 
