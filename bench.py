@@ -256,6 +256,121 @@ def copy_probe(torch):
     return n * 4
 
 
+# ---------------------------------------------------------------------------
+# experiments (each prints one JSON line of its own instead of the bench line)
+# ---------------------------------------------------------------------------
+
+PACK_WORKLOADS = [("tiny", "f64", False), ("covtype_med", "f32", False), ("deep", "f32", False),
+                  ("wide", "f32", False), ("interactions", "f32", True)]
+
+
+def experiment_packers(torch, gts, synth, reps):
+    """Section 4.1 / Table 5 on the synthetic models: for each heuristic and
+    bin capacity, the bin count K, the utilisation sum(L) / (B K), the host
+    packing time (gts_pack_paths on the extracted paths, median of 3), and
+    the kernel time on the model packed that way."""
+    table = []
+    for wl, dtype, inter in PACK_WORKLOADS:
+        w = synth.workload(wl)
+        ens = w.ensemble
+        el, _, _ = gts.extract_paths(ens)
+        roots = np.flatnonzero(el["feature_idx"] == -1)
+        sizes = np.diff(np.append(roots, len(el)))
+        Xd = torch.from_numpy(w.X).cuda()
+        rows = w.X.shape[0]
+        for cap in (32, 64):
+            for alg in ("none", "nf", "ffd", "bfd"):
+                rec = {"workload": wl, "dtype": dtype, "interactions": inter, "B": cap,
+                       "alg": alg, "paths": int(len(sizes)), "elements": int(sizes.sum())}
+                if int(sizes.max()) > cap:
+                    rec["skipped"] = f"longest path {int(sizes.max())} > B"
+                    table.append(rec)
+                    continue
+                t = []
+                for _ in range(3):
+                    t0 = time.perf_counter()
+                    packed, offs = gts.pack_paths(el, cap, alg)
+                    t.append(time.perf_counter() - t0)
+                K = len(offs) - 1
+                model = gts.prepare(ens, dtype, bin_capacity=cap, alg=alg)
+                assert model.num_bins == K
+                k = time_kernel(torch, gts, model, Xd, reps, inter)
+                rec.update({"bins": K, "utilisation": float(sizes.sum()) / (cap * K),
+                            "pack_ms": 1e3 * float(np.median(t)),
+                            "kernel_ms": float(np.median(k)),
+                            "kernel_rows_per_s": rows / (float(np.median(k)) * 1e-3)})
+                table.append(rec)
+                print(json.dumps(rec), file=sys.stderr, flush=True)
+    return {"experiment": "packers", "table": table}
+
+
+def experiment_rows(torch, gts, synth, oracle, workloads, cpu_limit_s):
+    """The paper's latency sweep (Fig. 4): time to explain n rows for n from
+    1 to 2^20 with the model prepared once.  GPU: the kernel alone on
+    device-resident rows (HIP events), and host to host (upload of X from
+    pinned memory, kernel, download of phi), median of several calls.  CPU: the
+    oracle on all cores while one call stays under cpu_limit_s."""
+    threads = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS")
+    if env and env.isdigit():
+        threads = min(threads, int(env))
+    out = {"experiment": "rows", "cpu_threads": threads, "sweeps": []}
+    for wl in workloads:
+        w = synth.workload(wl)
+        ens = w.ensemble
+        dtype = w.dtype
+        inter = wl == "interactions"
+        fn = kernel_fn(gts, inter)
+        host_ms, upload_ms, _ = time_prepare(gts, ens, dtype)
+        model = gts.prepare(ens, dtype)
+        nmax = 1 << (16 if inter else 20)
+        Xall = synth.sweep_rows(wl, nmax)
+        Xpin = torch.from_numpy(Xall).pin_memory()
+        Xdev = torch.empty_like(Xpin, device="cuda")
+        Xdev.copy_(Xpin)
+        width = ens.num_groups * (ens.num_features + 1) * ((ens.num_features + 1) if inter else 1)
+        phi_host = torch.empty(nmax * width, dtype=model.torch_dtype).pin_memory()
+        stream = torch.cuda.current_stream()
+        cpu_fn = oracle.interactions if inter else oracle.treeshap
+        cpu_open = True
+        points = []
+        n = 1
+        while n <= nmax:
+            reps = 20 if n <= 4096 else 5
+            # device-resident rows
+            k = time_kernel(torch, gts, model, Xdev[:n], reps, inter)
+            # host to host
+            phi_dev = fn(model, Xdev[:n])
+            torch.cuda.synchronize()
+            hh = []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                Xdev[:n].copy_(Xpin[:n], non_blocking=True)
+                fn(model, Xdev[:n], out=phi_dev)
+                phi_host[:n * width].copy_(phi_dev.reshape(-1), non_blocking=True)
+                stream.synchronize()
+                hh.append(time.perf_counter() - t0)
+            rec = {"rows": n, "gpu_kernel_ms": float(np.median(k)),
+                   "gpu_host_to_host_ms": 1e3 * float(np.median(hh))}
+            if cpu_open:
+                t0 = time.perf_counter()
+                cpu_fn(ens, Xall[:n], nthreads=threads)
+                dt = time.perf_counter() - t0
+                rec["cpu_ms"] = 1e3 * dt
+                if dt > cpu_limit_s:
+                    cpu_open = False
+            points.append(rec)
+            print(json.dumps(dict(rec, workload=wl)), file=sys.stderr, flush=True)
+            n *= 4
+        cross = [p["rows"] for p in points
+                 if "cpu_ms" in p and p["gpu_host_to_host_ms"] < p["cpu_ms"]]
+        out["sweeps"].append({"workload": wl, "dtype": dtype, "interactions": inter,
+                              "host_prepare_ms": host_ms, "upload_ms": upload_ms,
+                              "gpu_faster_from_rows": min(cross) if cross else None,
+                              "points": points})
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -271,6 +386,12 @@ def main():
                     help="skip the per-workload suite (kernel and preparation of every workload)")
     ap.add_argument("--suite-reps", type=int, default=10)
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--experiment", default=None, choices=["packers", "rows"],
+                    help="instead of the bench line, print one JSON line of an experiment: "
+                         "the packing heuristics (Table 5 with kernel times) or the rows "
+                         "sweep (Fig. 4)")
+    ap.add_argument("--sweep-workloads", default="covtype_med,deep,interactions")
+    ap.add_argument("--cpu-limit", type=float, default=4.0)
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     args = ap.parse_args()
@@ -290,6 +411,16 @@ def main():
 
     if args.copy_probe:
         copy_probe(torch)
+
+    if args.experiment == "packers":
+        print(json.dumps(experiment_packers(torch, gts, synth, args.suite_reps)), flush=True)
+        return
+    if args.experiment == "rows":
+        import oracle
+        print(json.dumps(experiment_rows(torch, gts, synth, oracle,
+                                         args.sweep_workloads.split(","), args.cpu_limit)),
+              flush=True)
+        return
 
     w = synth.workload(args.workload)
     inter = args.workload == "interactions"

@@ -24,7 +24,8 @@ Construction rules (shared by every workload):
 
 * RNG: ``PCG64(SeedSequence(201013972, spawn_key=(workload_id, stream)))``,
   streams 0 = structure/features/thresholds, 1 = leaf values,
-  2 = background rows, 3 = explained rows.
+  2 = background rows, 3 = explained rows, 4 = extra rows for row-count
+  sweeps (``sweep_rows``).
 * Trees grow breadth first; a node at depth d < max_depth splits with
   probability p; under a leaf cap a split that would exceed it is not taken.
   Node storage is BFS order per tree, root at local index 0.
@@ -263,6 +264,15 @@ def workload(name: str, rows: Optional[int] = None) -> Workload:
     if rows is not None:
         return Workload(w.name, w.ensemble, w.X_background, w.X[:rows], w.dtype)
     return w
+
+
+def sweep_rows(name: str, n: int) -> np.ndarray:
+    """``n`` rows from the feature distribution of a named workload, drawn from
+    a stream of their own (for sweeps over the number of explained rows)."""
+    if name == "interactions":
+        name = "covtype_med"
+    _, _, _, _, M, _, _, dist, _, _, _ = _SPECS[name]
+    return _features(dist, rng_for(_WORKLOAD_ID[name], 4), n, M)
 
 
 def random_workload(seed: int, *, num_trees: int = 3, max_depth: int = 4,
