@@ -25,20 +25,30 @@
 // multiply-add), and the scale factors reappear in the final sums as the
 // Shapley weights c_k = k!(q-1-k)!/q!.  UNWIND of an element with o = 1
 // divides the polynomial by (z + t) from the top coefficient down, like
-// Algorithm 1's o != 0 branch; for o = 0 the contribution reduces to
-// -v * sum_k c_k E_k, shared by every such element, so no division by a zero
-// fraction is ever needed.
+// Algorithm 1's o != 0 branch.  Its Shapley-weighted sum is linear in the
+// quotient, so it is a polynomial in -z whose coefficients
+// G_m = sum_{j>m} c_{j-1-m} E_j are shared by every element of the path: one
+// multiply-add per coefficient per element (Horner) instead of a division and
+// a weighted sum.  For o = 0 the contribution reduces to -v * sum_k c_k E_k,
+// shared by every such element, so no division by a zero fraction is ever
+// needed.  Per-element constants of a path (v (1 - z)) are computed once per
+// bin when it is staged, not once per row.
 //
 // Accumulation.  A workgroup owns a tile of RW rows of one output group and a
 // slice of that group's bins.  Contributions go to a phi tile in LDS (an
-// atomic add built from compare-and-swap); the tile is written to HBM once
-// (atomically added when several workgroups share the row tile).
+// atomic add built from compare-and-swap, the compare-and-swaps of a path
+// issued together so their LDS round trips overlap) or, when a wave has a
+// tile of its own and one path at a time, a plain read-modify-write.  An
+// interaction pair is added to one of its two entries and the tile write sums
+// the mirror entries, so the output is exactly symmetric.  The tile is written
+// to HBM once (atomically added when several workgroups share the row tile).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdint>
 #include <mutex>
 #include <numeric>
+#include <type_traits>
 #include <vector>
 
 #include "gts_internal.h"
@@ -46,7 +56,7 @@
 namespace gts {
 namespace {
 
-constexpr int kMaxUnrolledShap = 16;   // longest path (features) with unrolled code
+constexpr int kMaxUnrolledShap = 12;   // longest path (features) with unrolled code
 constexpr int kMaxUnrolledInter = 8;
 
 template <typename T>
@@ -120,9 +130,77 @@ __device__ __forceinline__ void lds_add(double* p, double v) {
   } while (old != assumed);
 }
 
-// Accumulate into the phi tile.  EXCL: no other lane or wave can update the
-// same entry at the same time (a wave-private tile with one path per wave),
-// so a plain read-modify-write suffices.
+// Bit patterns of the tile entries, for compare-and-swap.
+template <typename T> struct Bits;
+template <> struct Bits<float> {
+  using U = unsigned;
+  static __device__ __forceinline__ U of(float x) { return __float_as_uint(x); }
+  static __device__ __forceinline__ float val(U u) { return __uint_as_float(u); }
+};
+template <> struct Bits<double> {
+  using U = unsigned long long;
+  static __device__ __forceinline__ U of(double x) { return (U)__double_as_longlong(x); }
+  static __device__ __forceinline__ double val(U u) { return __longlong_as_double((long long)u); }
+};
+
+// How a lane adds the contributions of one path to the phi tile.
+//   kExclusive  no other lane or wave updates these entries meanwhile (a
+//               wave-private tile with one path per wave): plain
+//               read-modify-writes, all reads issued before any write.
+//   kBatched    all reads are issued, then all compare-and-swaps, so the LDS
+//               round trips overlap.  For one path per wave, or entries that
+//               rarely coincide across lanes (interaction pairs).
+//   kPaired     read and compare-and-swap entry by entry; the check of the
+//               results waits until the end.  For several paths per wave:
+//               two of its paths may share a feature, but rarely at the same
+//               step.
+// An entry that another lane or wave changed between the read and the
+// compare-and-swap is added again with the compare-and-swap loop.
+enum AddMode { kExclusive, kBatched, kPaired };
+
+// Add val[i] to *p[i] for every i with on[i]; the addresses of one lane are
+// distinct.  p[i] must be a valid tile address even where on[i] is false.
+template <AddMode MODE, typename T, int N>
+__device__ __forceinline__ void tile_add(T* const (&p)[N], const T (&val)[N], const bool (&on)[N]) {
+  if constexpr (MODE == kExclusive) {
+    T old[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) old[i] = *p[i];
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+      if (on[i]) *p[i] = old[i] + val[i];
+  } else {
+    using U = typename Bits<T>::U;
+    U old[N], got[N];
+    if constexpr (MODE == kBatched) {
+#pragma unroll
+      for (int i = 0; i < N; ++i) old[i] = *reinterpret_cast<const U*>(p[i]);
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        got[i] = on[i] ? atomicCAS(reinterpret_cast<U*>(p[i]), old[i],
+                                   Bits<T>::of(Bits<T>::val(old[i]) + val[i]))
+                       : old[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        old[i] = *reinterpret_cast<const U*>(p[i]);
+        got[i] = on[i] ? atomicCAS(reinterpret_cast<U*>(p[i]), old[i],
+                                   Bits<T>::of(Bits<T>::val(old[i]) + val[i]))
+                       : old[i];
+      }
+    }
+    bool retry = false;
+#pragma unroll
+    for (int i = 0; i < N; ++i) retry |= got[i] != old[i];
+    if (retry) {
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        if (got[i] != old[i]) lds_add(p[i], val[i]);
+    }
+  }
+}
+
+// Single entry, for the runtime-length path code.
 template <bool EXCL, typename T>
 __device__ __forceinline__ void acc_add(T* p, T v) {
   if constexpr (EXCL) *p += v;
@@ -158,75 +236,121 @@ __device__ __forceinline__ Bin<T> load_bin(const DevModel<T>& d, int bi, int lan
   return b;
 }
 
-// One wave's copy of its current bin in LDS: element e (a lane of the bin)
-// as (feature, lower, upper, zero fraction or leaf value).  Paths start at a
-// table built from the root ballot: start[t] = bin lane of the t-th root,
-// start[#roots] = bin length.
-template <typename T>
-struct Stage {
-  int4 meta[64];   // feature, lower bits, upper bits, z bits (fp32 z only)
-  T zd[64];        // z in the model dtype
-  int start[65];
+// One wave's copy of its current bin in LDS.  head[slot] = (feature, lower
+// bits, upper bits, fp32 z bits); aux[slot] holds w = v (1 - z), v the leaf
+// value of the element's path (and z itself for fp64 models); on a root, z
+// and w hold v.  path[t] = slot of the t-th root | (features of its path) << 8.
+//
+// GAPPED (several paths per wave): element e of the bin sits in slot
+// e + (number of even-length paths before its path).  The gap after every
+// path of even length makes the distance between consecutive path starts
+// odd, so lanes reading the k-th elements of up to 8 paths of equal length at
+// once hit different LDS banks; aux entries are 16 bytes so that an element's
+// head and aux share one address register.  Slot kSlots holds a neutral
+// element (feature 0, range (-inf, +inf), z = 1, w = 0): a player present
+// and absent alike, which changes no other player's Shapley value.  A lane
+// whose path is shorter than the wave's longest reads it in place of the
+// elements past its path's end.  Without GAPPED (one path per wave, every
+// read a broadcast) element e sits in slot e.
+template <typename T> struct Aux;
+template <> struct alignas(16) Aux<float> {
+  float w, pad0, pad1, pad2;
+};
+template <> struct alignas(16) Aux<double> {
+  double z, w;
 };
 
-template <typename T>
-__device__ __forceinline__ int stage_bin(Stage<T>* st, const Bin<T>& b, int lane) {
-  st->meta[lane] = make_int4(b.feat, __float_as_int(b.lo), __float_as_int(b.hi),
-                             sizeof(T) == 4 ? __float_as_int((float)b.z) : 0);
-  st->zd[lane] = b.z;
+template <typename T, bool GAPPED>
+struct Stage {
+  static constexpr int kSlots = GAPPED ? 96 : 64;   // 64 elements + a gap per even-length path
+  using AuxT = std::conditional_t<sizeof(T) == 4 && !GAPPED, float, Aux<T>>;
+  int4 head[kSlots + 1];
+  AuxT aux[kSlots + 1];
+  int path[64];
+
+  __device__ __forceinline__ T w(int e) const {
+    if constexpr (std::is_same_v<AuxT, float>) return aux[e];
+    else return aux[e].w;
+  }
+  __device__ __forceinline__ T z(int e) const {
+    if constexpr (sizeof(T) == 4) return __int_as_float(head[e].w);
+    else return aux[e].z;
+  }
+};
+
+template <typename T, bool GAPPED>
+__device__ __forceinline__ void init_stage(Stage<T, GAPPED>* st, int lane) {
+  using S = Stage<T, GAPPED>;
+  if (lane == 0) {
+    st->head[S::kSlots] = make_int4(0, __float_as_int(-INFINITY), __float_as_int(INFINITY),
+                                    __float_as_int(1.0f));
+    typename S::AuxT n{};
+    if constexpr (std::is_same_v<typename S::AuxT, float>) {
+      n = 0.0f;
+    } else {
+      if constexpr (sizeof(T) == 8) n.z = 1.0;
+      n.w = T(0);
+    }
+    st->aux[S::kSlots] = n;
+  }
+}
+
+template <typename T, bool GAPPED>
+__device__ __forceinline__ int stage_bin(Stage<T, GAPPED>* st, const Bin<T>& b, int lane) {
   const bool root = b.feat == -1;
   const uint64_t roots = __ballot(root);
+  const uint64_t upto = roots & ((2ull << lane) - 1ull);      // roots at or below this lane
+  const int rl = upto ? 63 - __clzll((long long)upto) : lane;  // this element's root
+  const uint64_t above = roots & ~((2ull << lane) - 1ull);
+  const int len = (above ? __builtin_ctzll(above) : b.len) - lane;  // path length, on a root
+  int slot = lane;
+  if constexpr (GAPPED) {
+    const uint64_t evens = __ballot(root && (len & 1) == 0);
+    slot += __popcll(evens & ((1ull << rl) - 1ull));
+  }
+  const T v = __shfl(b.z, rl);   // a root's zero-fraction slot holds v
+  const T w = root ? v : v * (T(1) - b.z);
+  st->head[slot] = make_int4(b.feat, __float_as_int(b.lo), __float_as_int(b.hi),
+                             sizeof(T) == 4 ? __float_as_int((float)b.z) : 0);
+  typename Stage<T, GAPPED>::AuxT ax{};
+  if constexpr (std::is_same_v<typename Stage<T, GAPPED>::AuxT, float>) {
+    ax = w;
+  } else {
+    if constexpr (sizeof(T) == 8) ax.z = b.z;
+    ax.w = w;
+  }
+  st->aux[slot] = ax;
   const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(roots >> 32),
                                              __builtin_amdgcn_mbcnt_lo((unsigned)roots, 0u));
-  if (root) st->start[rank] = lane;
-  const int nroots = __popcll(roots);
-  if (lane == 0) st->start[nroots] = b.len;
+  if (root) st->path[rank] = slot | ((len - 1) << 8);
   // the stores above are read by other lanes of this wave only
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  return nroots;
+  return __popcll(roots);
 }
 
-// Element k (0-based among the path's features) of the path whose root is
-// at bin lane s; s is wave-uniform when one path fills the wave.
-template <typename T>
-struct Fetch {
-  const Stage<T>* st;
-  int s;
-  __device__ __forceinline__ void get(int k, int& f, float& lo, float& hi, T& z) const {
-    const int e = (s + 1 + k) & 63;
-    const int4 m = st->meta[e];
-    f = m.x;
-    lo = __int_as_float(m.y);
-    hi = __int_as_float(m.z);
-    if constexpr (sizeof(T) == 4) z = __int_as_float(m.w);
-    else z = st->zd[e];
-  }
-  __device__ __forceinline__ T v() const {
-    if constexpr (sizeof(T) == 4) return __int_as_float(st->meta[s & 63].w);
-    else return st->zd[s & 63];
-  }
-};
-
-// Feature, presence test o_k = [lower <= x < upper] and zero fraction of
-// the first Q elements.  Elements k >= q are padding: present with
-// probability 1 and absent with probability 1 (z = o = 1), which changes no
-// other element's Shapley value; f = -1 marks them unwritten.
-template <typename T, int Q, bool UNIFORM>
-__device__ __forceinline__ void load_path(const Fetch<T>& fe, int q, const float* __restrict__ xrow,
-                                          int (&f)[Q], bool (&o)[Q], T (&z)[Q]) {
+// Feature, presence test o_k = [lower <= x < upper], zero fraction and
+// v (1 - z) of the first Q feature elements of the path whose root is in
+// slot s (wave-uniform when UNIFORM).  A lane whose path has q < Q features
+// reads the neutral element for k >= q; on[k] = k < q marks the elements
+// whose contributions are written.
+template <typename T, int Q, bool UNIFORM, bool GAPPED>
+__device__ __forceinline__ void load_path(const Stage<T, GAPPED>* st, int s, int q,
+                                          const float* __restrict__ xrow, int (&f)[Q],
+                                          bool (&o)[Q], T (&z)[Q], T (&w)[Q], bool (&on)[Q]) {
 #pragma unroll
   for (int k = 0; k < Q; ++k) {
-    int fk;
-    float lo, hi;
-    T zk;
-    fe.get(k, fk, lo, hi, zk);
     const bool real = UNIFORM || k < q;
-    const float x = xrow[real ? fk : 0];
-    f[k] = real ? fk : -1;
-    o[k] = real ? (lo <= x) && (x < hi) : true;
-    z[k] = real ? zk : T(1);
+    const int e = real ? s + 1 + k : Stage<T, GAPPED>::kSlots;
+    const int4 head = st->head[e];
+    f[k] = head.x;
+    const float x = xrow[head.x];
+    o[k] = (__int_as_float(head.y) <= x) && (x < __int_as_float(head.z));
+    if constexpr (sizeof(T) == 4) z[k] = __int_as_float(head.w);
+    else z[k] = st->aux[e].z;
+    w[k] = st->w(e);
+    on[k] = real;
   }
 }
 
@@ -259,26 +383,39 @@ __device__ __forceinline__ void unwind_one(const T (&E)[Q + 1], T zi, T (&D)[Q])
 // per-lane path arithmetic
 // ---------------------------------------------------------------------------
 
-// SHAP values: phi[f_i] += v (o_i - z_i) * sum_k c_k D^i_k
-template <typename T, int Q, bool EXCL>
+// SHAP values.  With D^i = E / (z_i + t) (synthetic division from the top,
+// D^i_k = sum_{j>k} E_j (-z_i)^{j-1-k}), the unwound sum of element i is
+// sum_k c_k D^i_k = sum_m (-z_i)^m G_m with G_m = sum_{j>m} c_{j-1-m} E_j.
+// phi[f_i] += v (1 - z_i) * that sum when o_i = 1, and -v sum_k c_k E_k
+// when o_i = 0.
+template <typename T, int Q, AddMode MODE>
 __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
-                                          T v, bool active, T* __restrict__ prow) {
+                                          const T (&w)[Q], const bool (&on)[Q], T v,
+                                          T* __restrict__ prow) {
   T E[Q + 1];
   extend_all<T, Q>(o, z, E);
   T t_all = T(0);
 #pragma unroll
   for (int k = 0; k < Q; ++k) t_all = fma(T(shapley_weight(Q, k)), E[k], t_all);
+  T G[Q];
+#pragma unroll
+  for (int m = 0; m < Q; ++m) {
+    G[m] = T(shapley_weight(Q, Q - 1 - m)) * E[Q];
+#pragma unroll
+    for (int j = Q - 1; j > m; --j) G[m] = fma(T(shapley_weight(Q, j - 1 - m)), E[j], G[m]);
+  }
   const T neg_vt = -v * t_all;
+  T* p[Q];
+  T val[Q];
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
-    T D[Q];
-    unwind_one<T, Q>(E, z[i], D);
-    T s = T(0);
+    T s = G[Q - 1];
 #pragma unroll
-    for (int k = 0; k < Q; ++k) s = fma(T(shapley_weight(Q, k)), D[k], s);
-    const T phi = o[i] ? v * (T(1) - z[i]) * s : neg_vt;
-    if (active && f[i] >= 0) acc_add<EXCL>(&prow[f[i]], phi);
+    for (int m = Q - 2; m >= 0; --m) s = fma(-z[i], s, G[m]);
+    val[i] = o[i] ? w[i] * s : neg_vt;
+    p[i] = prow + f[i];
   }
+  tile_add<MODE>(p, val, on);
 }
 
 // Interaction values.  For elements i != c the interaction through this path
@@ -288,10 +425,12 @@ __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q],
 //   (1,1): S_ic from E / ((z_i + t)(z_c + t))
 //   (1,0): (o_c - z_c) S_ic = -sum_k c'_k D^i_k         (D^i = E / (z_i + t))
 //   (0,0): (o_i - z_i)(o_c - z_c) S_ic = sum_k c'_k E_k
-// and phi_ii = phi_i - sum_{c != i} Delta_ic (Eq. 6).
-template <typename T, int Q, bool EXCL>
+// and phi_ii = phi_i - sum_{c != i} Delta_ic (Eq. 6).  Each pair is added to
+// the entry [f_i][f_c] only; the tile write adds the mirror entries.
+template <typename T, int Q, AddMode MODE>
 __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
-                                           T v, bool active, T* __restrict__ prow, int stride) {
+                                           const T (&w)[Q], const bool (&on)[Q], T v,
+                                           T* __restrict__ prow, int stride) {
   T E[Q + 1];
   extend_all<T, Q>(o, z, E);
   T t_all = T(0);
@@ -312,11 +451,21 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
     T s = T(0);
 #pragma unroll
     for (int k = 0; k < Q; ++k) s = fma(T(shapley_weight(Q, k)), D[k], s);
-    diag[c] = o[c] ? v * (T(1) - z[c]) * s : -v * t_all;
+    diag[c] = o[c] ? w[c] * s : -v * t_all;
     tp[c] = T(0);
     if constexpr (Q >= 2) {
 #pragma unroll
       for (int k = 0; k < Q - 1; ++k) tp[c] = fma(T(shapley_weight(Q - 1, k)), D[k], tp[c]);
+    }
+    if (c == 0) continue;
+    T* p[Q];
+    T val[Q];
+    bool pon[Q];
+#pragma unroll
+    for (int i = 0; i < Q; ++i) {
+      p[i] = prow;
+      val[i] = T(0);
+      pon[i] = false;
     }
 #pragma unroll
     for (int i = 0; i < c; ++i) {
@@ -330,51 +479,47 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
         for (int k = 0; k < Q - 1; ++k) s11 = fma(T(shapley_weight(Q - 1, k)), DD[k], s11);
       }
       T delta;
-      if (o[i] && o[c]) delta = half_v * (T(1) - z[i]) * (T(1) - z[c]) * s11;
-      else if (o[i]) delta = -half_v * (T(1) - z[i]) * tp[i];
-      else if (o[c]) delta = -half_v * (T(1) - z[c]) * tp[c];
+      if (o[i] && o[c]) delta = T(0.5) * w[i] * (T(1) - z[c]) * s11;
+      else if (o[i]) delta = T(-0.5) * w[i] * tp[i];
+      else if (o[c]) delta = T(-0.5) * w[c] * tp[c];
       else delta = half_v * t_pair;
       diag[c] -= delta;
       diag[i] -= delta;
-      if (active && f[i] >= 0 && f[c] >= 0) {
-        acc_add<EXCL>(&prow[f[i] * stride + f[c]], delta);
-        acc_add<EXCL>(&prow[f[c] * stride + f[i]], delta);
-      }
+      pon[i] = on[i] && on[c];
+      p[i] = prow + f[i] * stride + f[c];
+      val[i] = delta;
     }
+    tile_add<MODE == kExclusive ? kExclusive : kBatched>(p, val, pon);
   }
+  T* p[Q];
 #pragma unroll
-  for (int c = 0; c < Q; ++c)
-    if (active && f[c] >= 0) acc_add<EXCL>(&prow[f[c] * stride + f[c]], diag[c]);
+  for (int c = 0; c < Q; ++c) p[c] = prow + f[c] * stride + f[c];
+  tile_add<MODE>(p, diag, on);
 }
 
 // Paths longer than the unrolled variants: the same arithmetic with runtime
-// loops, always in fp64.  Dividing the weight polynomial from its top
-// coefficient down cancels more and more as paths grow; in fp32 the error
-// passes the parity bound beyond about 20 features, in fp64 it stays far
-// inside it for the longest path a wave64 holds (63 features).  FP64 FMAs run
-// at the rate of unpacked FP32 ones on gfx950.
-template <typename T, bool INTER, bool EXCL>
-__device__ void path_dyn(const Fetch<T>& fe, int qfetch, int q, bool active,
-                         const float* __restrict__ xrow, T* __restrict__ prow, int stride) {
+// loops, always in fp64, unwinding by explicit synthetic division.  Dividing
+// the weight polynomial from its top coefficient down cancels more and more
+// as paths grow; in fp32 the error passes the parity bound beyond about 16
+// features, in fp64 it stays far inside it for the longest path a wave64
+// holds (63 features).  FP64 FMAs run at the rate of unpacked FP32 ones on
+// gfx950.  q = 0 (no path) does nothing.
+template <typename T, bool INTER, AddMode MODE, bool GAPPED>
+__device__ void path_dyn(const Stage<T, GAPPED>* st, int s, int q, const float* __restrict__ xrow,
+                         T* __restrict__ prow, int stride) {
   double E[kMaxPathLen];
   double z[kMaxPathLen];
   double D[kMaxPathLen];
   int f[kMaxPathLen];
   uint64_t obits = 0;
-  for (int k = 0; k < qfetch; ++k) {
-    int fk;
-    float lo, hi;
-    T zt;
-    fe.get(k, fk, lo, hi, zt);
-    const double zk = (double)zt;
-    if (k < q) {
-      const float x = xrow[fk];
-      f[k] = fk;
-      z[k] = zk;
-      obits |= (uint64_t)((lo <= x) && (x < hi)) << k;
-    }
+  for (int k = 0; k < q; ++k) {
+    const int4 head = st->head[s + 1 + k];
+    const float x = xrow[head.x];
+    f[k] = head.x;
+    z[k] = (double)st->z(s + 1 + k);
+    obits |= (uint64_t)((__int_as_float(head.y) <= x) && (x < __int_as_float(head.z))) << k;
   }
-  const double v = (double)fe.v();
+  const double v = (double)st->w(s);
   E[0] = 1.0;
   for (int l = 1; l <= q; ++l) {
     const double zl = z[l - 1];
@@ -393,7 +538,7 @@ __device__ void path_dyn(const Fetch<T>& fe, int qfetch, int q, bool active,
       for (int k = 0; k < q; ++k) s = fma(shapley_weight(q, k), D[k], s);
       const bool oi = (obits >> i) & 1u;
       const double phi = oi ? v * (1.0 - z[i]) * s : -v * t_all;
-      if (active) acc_add<EXCL>(&prow[f[i]], (T)phi);
+      acc_add<MODE == kExclusive>(&prow[f[i]], (T)phi);
     }
   } else {
     double DD[kMaxPathLen];
@@ -424,51 +569,47 @@ __device__ void path_dyn(const Fetch<T>& fe, int qfetch, int q, bool active,
         else delta = half_v * t_pair;
         diag[c] -= delta;
         diag[i] -= delta;
-        if (active) {
-          acc_add<EXCL>(&prow[f[i] * stride + f[c]], (T)delta);
-          acc_add<EXCL>(&prow[f[c] * stride + f[i]], (T)delta);
-        }
+        acc_add<MODE == kExclusive>(&prow[f[i] * stride + f[c]], (T)delta);
       }
     }
-    for (int c = 0; c < q; ++c)
-      if (active) acc_add<EXCL>(&prow[f[c] * stride + f[c]], (T)diag[c]);
+    for (int c = 0; c < q; ++c) acc_add<MODE == kExclusive>(&prow[f[c] * stride + f[c]], (T)diag[c]);
   }
 }
 
-template <typename T, int Q, bool UNIFORM, bool INTER, bool EXCL>
-__device__ __forceinline__ void path_fixed(const Fetch<T>& fe, int q, bool active,
+template <typename T, int Q, bool UNIFORM, bool INTER, AddMode MODE, bool GAPPED>
+__device__ __forceinline__ void path_fixed(const Stage<T, GAPPED>* st, int s, int q,
                                            const float* __restrict__ xrow, T* __restrict__ prow,
                                            int stride) {
   int f[Q];
-  bool o[Q];
-  T z[Q];
-  load_path<T, Q, UNIFORM>(fe, q, xrow, f, o, z);
-  const T v = fe.v();
-  if constexpr (INTER) inter_math<T, Q, EXCL>(f, o, z, v, active, prow, stride);
-  else shap_math<T, Q, EXCL>(f, o, z, v, active, prow);
+  bool o[Q], on[Q];
+  T z[Q], w[Q];
+  load_path<T, Q, UNIFORM, GAPPED>(st, s, q, xrow, f, o, z, w, on);
+  const T v = st->w(s);
+  if constexpr (INTER) inter_math<T, Q, MODE>(f, o, z, w, on, v, prow, stride);
+  else shap_math<T, Q, MODE>(f, o, z, w, on, v, prow);
 }
 
-// Q = features of the longest path in the wave's current set (uniform)
-template <typename T, bool UNIFORM, bool INTER, bool EXCL>
-__device__ __forceinline__ void dispatch(int Q, const Fetch<T>& fe, int q, bool active,
+// Q = features of the longest path in the wave's current set (uniform); q =
+// this lane's path (0: none).
+template <typename T, bool UNIFORM, bool INTER, AddMode MODE, bool GAPPED>
+__device__ __forceinline__ void dispatch(int Q, const Stage<T, GAPPED>* st, int s, int q,
                                          const float* xrow, T* prow, int stride) {
-  static_assert(kMaxUnrolledShap == 16 && kMaxUnrolledInter == 8, "update the case lists");
+  static_assert(kMaxUnrolledShap == 12 && kMaxUnrolledInter == 8, "update the case lists");
   if constexpr (INTER) {
     switch (Q) {
-#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, true, EXCL>(fe, q, active, xrow, prow, stride); break;
+#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, true, MODE, GAPPED>(st, s, q, xrow, prow, stride); break;
       GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
       GTS_CASE(7) GTS_CASE(8)
 #undef GTS_CASE
-      default: path_dyn<T, true, EXCL>(fe, Q, q, active, xrow, prow, stride); break;
+      default: path_dyn<T, true, MODE, GAPPED>(st, s, q, xrow, prow, stride); break;
     }
   } else {
     switch (Q) {
-#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, false, EXCL>(fe, q, active, xrow, prow, stride); break;
+#define GTS_CASE(n) case n: path_fixed<T, n, UNIFORM, false, MODE, GAPPED>(st, s, q, xrow, prow, stride); break;
       GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
       GTS_CASE(7) GTS_CASE(8) GTS_CASE(9) GTS_CASE(10) GTS_CASE(11) GTS_CASE(12)
-      GTS_CASE(13) GTS_CASE(14) GTS_CASE(15) GTS_CASE(16)
 #undef GTS_CASE
-      default: path_dyn<T, false, EXCL>(fe, Q, q, active, xrow, prow, stride); break;
+      default: path_dyn<T, false, MODE, GAPPED>(st, s, q, xrow, prow, stride); break;
     }
   }
 }
@@ -487,14 +628,15 @@ __device__ __forceinline__ int wave_max_small(int v) {
 // All paths of one bin.  RW == 64: one path at a time for the whole wave.
 // RW < 64: rounds of up to P = 64/RW paths, lane (j, r) = (path j, row r).
 template <typename T, int RW, bool INTER, bool EXCL>
-__device__ __forceinline__ void process_bin(Stage<T>* st, const Bin<T>& b, int lane,
+__device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>& b, int lane,
                                             const float* xrow, T* prow, int stride) {
   const int nroots = stage_bin(st, b, lane);
   if constexpr (RW == 64) {
     for (int t = 0; t < nroots; ++t) {
-      const int s = __builtin_amdgcn_readfirstlane(st->start[t]);
-      const int q = __builtin_amdgcn_readfirstlane(st->start[t + 1]) - s - 1;
-      if (q > 0) dispatch<T, true, INTER, EXCL>(q, Fetch<T>{st, s}, q, true, xrow, prow, stride);
+      const int info = __builtin_amdgcn_readfirstlane(st->path[t]);
+      const int s = info & 0xff;
+      const int q = info >> 8;
+      if (q > 0) dispatch<T, true, INTER, EXCL ? kExclusive : kBatched, false>(q, st, s, q, xrow, prow, stride);
     }
   } else {
     constexpr int P = 64 / RW;
@@ -502,11 +644,11 @@ __device__ __forceinline__ void process_bin(Stage<T>* st, const Bin<T>& b, int l
     for (int base = 0; base < nroots; base += P) {
       const int t = base + j;
       const bool valid = t < nroots;
-      const int my_s = valid ? st->start[t] : 0;
-      const int my_q = valid ? st->start[t + 1] - my_s - 1 : 0;
+      const int info = valid ? st->path[t] : 0;
+      const int my_s = info & 0xff;
+      const int my_q = info >> 8;
       const int qmax = wave_max_small(my_q);
-      if (qmax > 0)
-        dispatch<T, false, INTER, false>(qmax, Fetch<T>{st, my_s}, my_q, my_q > 0, xrow, prow, stride);
+      if (qmax > 0) dispatch<T, false, INTER, kPaired, true>(qmax, st, my_s, my_q, xrow, prow, stride);
     }
   }
   // the next bin overwrites the stage
@@ -548,7 +690,7 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   T* ps = reinterpret_cast<T*>(smem + (size_t)RW * L.sx * sizeof(float));
   constexpr int NT = PRIV ? WAVES : 1;  // phi tiles
   const int tile_elems = RW * L.sp;
-  Stage<T>* stages = reinterpret_cast<Stage<T>*>(
+  Stage<T, RW < 64>* stages = reinterpret_cast<Stage<T, RW < 64>*>(
       smem + (((size_t)RW * L.sx * sizeof(float) + (size_t)NT * tile_elems * sizeof(T) + 15) & ~(size_t)15));
 
   // stage the X tile (coalesced along each row) and clear the phi tile
@@ -560,9 +702,10 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   for (int i = threadIdx.x; i < NT * tile_elems; i += kThreads) ps[i] = T(0);
   __syncthreads();
 
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int r = lane % RW;
+  init_stage(stages + wave, lane);
   const int gb0 = d.group_bins[g], gb1 = d.group_bins[g + 1];
   const int nb = gb1 - gb0;
   const int chunk = (nb + L.splits - 1) / L.splits;
@@ -585,16 +728,27 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   }
   __syncthreads();
 
-  // write the tile: phi[row][g][.]; the bias goes to the last entry
+  // write the tile: phi[row][g][.]; the bias goes to the last entry.  An
+  // interaction pair was added to one of its two entries: each of them gets
+  // the sum of both.
   const T bias = d.bias[g];
   const int W = L.width;
   for (int i = threadIdx.x; i < RW * W; i += kThreads) {
     const int rr = i / W, c = i - rr * W;
     const int64_t row = r0 + rr;
     if (row >= L.rows) continue;
+    int cm = c;
+    if constexpr (INTER) {
+      const int a = c / stride, bcol = c - a * stride;
+      cm = bcol * stride + a;
+    }
     T val = ps[rr * L.sp + c];
+    if (cm != c) val += ps[rr * L.sp + cm];
 #pragma unroll
-    for (int w = 1; w < NT; ++w) val += ps[w * tile_elems + rr * L.sp + c];
+    for (int w = 1; w < NT; ++w) {
+      val += ps[w * tile_elems + rr * L.sp + c];
+      if (cm != c) val += ps[w * tile_elems + rr * L.sp + cm];
+    }
     if (c == W - 1 && s == 0) val += bias;
     T* out = phi + (row * G + g) * (int64_t)W + c;
     if (L.accumulate) unsafeAtomicAdd(out, val);
@@ -695,25 +849,33 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
   const int32_t sx = odd_at_least(M);
   const int32_t sp = odd_at_least(width);
   // Row tile and accumulation.  If 64 rows with a private phi tile for each
-  // of 4 waves fit in 64 KB, use them (no contention, no atomics).  Otherwise
-  // 8 waves share one tile: the largest RW whose tiles fit in 64 KB (several
-  // workgroups per CU), or, if that would leave fewer than 8 rows per wave,
-  // 8 rows (then 4) using up to the whole LDS of a workgroup.
+  // of 4 waves fit in half a CU's LDS (two workgroups per CU), use them (no
+  // contention, no atomics).  Otherwise 8 waves share one tile: the largest
+  // RW whose tiles fit in 64 KB (several workgroups per CU), or, if that
+  // would leave fewer than 8 rows per wave, 8 rows (then 4) using up to the
+  // whole LDS of a workgroup.
   auto need = [&](int rw, int waves, bool priv) {
     const size_t tiles = (size_t)rw * ((size_t)sx * sizeof(float) +
                                        (priv ? (size_t)waves : 1) * (size_t)sp * sizeof(T));
-    return ((tiles + 15) & ~(size_t)15) + (size_t)waves * sizeof(Stage<T>);
+    const size_t stage = rw == 64 ? sizeof(Stage<T, false>) : sizeof(Stage<T, true>);
+    return ((tiles + 15) & ~(size_t)15) + (size_t)waves * stage;
   };
   int RW = 0;
   int waves = 8;
   bool priv = false;
-  if (need(64, 4, true) <= 64 * 1024) {
+#ifndef GTS_PRIV_LDS_MAX
+#define GTS_PRIV_LDS_MAX (64 * 1024)
+#endif
+  if ((int64_t)need(64, 4, true) <= std::min<int64_t>(GTS_PRIV_LDS_MAX, dev.lds_per_block)) {
     RW = 64;
     waves = 4;
     priv = true;
   } else {
+#ifndef GTS_SHARED_LDS_MAX
+#define GTS_SHARED_LDS_MAX (64 * 1024)
+#endif
     for (int cand : {64, 32, 16, 8}) {
-      if (need(cand, 8, false) <= 64 * 1024) {
+      if ((int64_t)need(cand, 8, false) <= std::min<int64_t>(GTS_SHARED_LDS_MAX, dev.lds_per_block)) {
         RW = cand;
         break;
       }
