@@ -263,7 +263,10 @@ template <> struct alignas(16) Aux<double> {
 template <typename T, bool GAPPED>
 struct Stage {
   static constexpr int kSlots = GAPPED ? 96 : 64;   // 64 elements + a gap per even-length path
-  using AuxT = std::conditional_t<sizeof(T) == 4 && !GAPPED, float, Aux<T>>;
+#ifndef GTS_WIDE_AUX
+#define GTS_WIDE_AUX 0
+#endif
+  using AuxT = std::conditional_t<sizeof(T) == 4 && !(GAPPED && GTS_WIDE_AUX), float, Aux<T>>;
   int4 head[kSlots + 1];
   AuxT aux[kSlots + 1];
   int path[64];
@@ -882,6 +885,22 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
     }
     if (RW == 0 && (int64_t)need(8, 8, false) <= dev.lds_per_block) RW = 8;
     if (RW == 0 && (int64_t)need(4, 8, false) <= dev.lds_per_block) RW = 4;
+    // Waves per workgroup for a shared tile of RW <= 16 rows: as many waves
+    // per CU as the LDS allows, up to 24 (the VGPR budget of the SHAP
+    // kernels) or 16 (interactions).
+    if (RW != 0 && RW <= 16) {
+      const int cap = INTER ? 16 : 24;
+      int best = 0;
+      for (int w : {8, 12, 16}) {
+        const int64_t n = need(RW, w, false);
+        if (n > dev.lds_per_block) continue;
+        const int per_cu = (int)std::min<int64_t>(cap, w * (dev.lds_per_cu / n));
+        if (per_cu > best) {
+          best = per_cu;
+          waves = w;
+        }
+      }
+    }
   }
   if (RW == 0) return fail(GTS_EINVAL, "M = %d needs more LDS than a workgroup has", M);
   const size_t lds = need(RW, waves, priv);
@@ -899,18 +918,27 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
     want = (want + step - 1) / step * step;
     splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
   }
-#define GTS_LAUNCH(rw)                                                                    \
-  return launch_rw<T, rw, INTER, 8, false>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, \
+#define GTS_LAUNCH(rw, w)                                                                 \
+  return launch_rw<T, rw, INTER, w, false>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, \
                                            width, lds)
   if (priv)
     return launch_rw<T, 64, INTER, 4, true>(m, blob, X, rows, ld, phi, stream, splits, sx, sp,
                                             width, lds);
   switch (RW) {
-    case 64: GTS_LAUNCH(64);
-    case 32: GTS_LAUNCH(32);
-    case 16: GTS_LAUNCH(16);
-    case 8: GTS_LAUNCH(8);
-    default: GTS_LAUNCH(4);
+    case 64: GTS_LAUNCH(64, 8);
+    case 32: GTS_LAUNCH(32, 8);
+    case 16:
+      if (waves == 12) GTS_LAUNCH(16, 12);
+      if (waves == 16) GTS_LAUNCH(16, 16);
+      GTS_LAUNCH(16, 8);
+    case 8:
+      if (waves == 12) GTS_LAUNCH(8, 12);
+      if (waves == 16) GTS_LAUNCH(8, 16);
+      GTS_LAUNCH(8, 8);
+    default:
+      if (waves == 12) GTS_LAUNCH(4, 12);
+      if (waves == 16) GTS_LAUNCH(4, 16);
+      GTS_LAUNCH(4, 8);
   }
 #undef GTS_LAUNCH
 }
