@@ -590,8 +590,9 @@ OR_EXPORT int or_path_brute(int32_t q, const int32_t *feature,
  * element per distinct split feature in ascending feature order.  A left
  * turn at threshold t bounds the range above by t, a right turn below by t;
  * repeats of a feature intersect the ranges and multiply zero fractions in
- * root-to-leaf order.  bias[g] = sum over the group's paths (path_idx order)
- * of v * (1 * z_1 * z_2 * ...) in element order.
+ * root-to-leaf order.  The bias term of a path is v * (1 * z_1 * z_2 * ...)
+ * in element order; each tree sums its paths' terms in path order, and
+ * bias[g] sums the trees of group g in tree order.
  */
 
 typedef struct {
@@ -612,6 +613,7 @@ typedef struct {
   double *zero, *v;
   int64_t cap, n, paths;
   double *bias;
+  double tree_sum; /* the current tree's bias terms so far */
 } out_t;
 
 static void emit_leaf(const ens_t *e, int64_t t, int32_t leaf, raw_t *splits,
@@ -646,7 +648,7 @@ static void emit_leaf(const ens_t *e, int64_t t, int32_t leaf, raw_t *splits,
   }
   double prod = 1.0;
   for (int i = 0; i < nm; i++) prod = prod * m[i].z;
-  if (o->bias) o->bias[g] += v * prod;
+  o->tree_sum = o->tree_sum + v * prod;
   for (int i = -1; i < nm; i++) {
     if (o->n < o->cap) {
       int64_t k = o->n;
@@ -712,7 +714,11 @@ OR_EXPORT int64_t or_extract_paths(
     for (int32_t g = 0; g < G; g++) bias[g] = 0.0;
   const int D = ensemble_depth(&e);
   raw_t *splits = (raw_t *)malloc(sizeof(raw_t) * (size_t)(D + 1));
-  for (int64_t t = 0; t < T; t++) walk(&e, t, 0, splits, 0, &o);
+  for (int64_t t = 0; t < T; t++) {
+    o.tree_sum = 0.0;
+    walk(&e, t, 0, splits, 0, &o);
+    if (bias) bias[group[t]] = bias[group[t]] + o.tree_sum;
+  }
   free(splits);
   *num_paths = o.paths;
   return o.n;

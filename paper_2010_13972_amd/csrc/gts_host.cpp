@@ -320,6 +320,21 @@ struct Walker {
   }
 };
 
+// The bias of each output group from the paths' terms v * prod(z): every
+// tree sums its own paths' terms in path order, then each group sums its
+// trees' sums in tree order.  (A fixed two-level order that a device
+// reduction reproduces bit for bit with one thread per tree.)  tree_paths:
+// [T+1] first path of every tree.  bias[g] is overwritten.
+void sum_bias(const gts_ensemble* e, const int64_t* tree_paths, const double* term,
+              double* bias) {
+  for (int32_t g = 0; g < e->num_groups; ++g) bias[g] = 0.0;
+  for (int64_t t = 0; t < e->num_trees; ++t) {
+    double s = 0.0;
+    for (int64_t p = tree_paths[t]; p < tree_paths[t + 1]; ++p) s = s + term[p];
+    bias[e->tree_group[t]] = bias[e->tree_group[t]] + s;
+  }
+}
+
 int host_threads(int64_t work) {
   unsigned hw = std::thread::hardware_concurrency();
   if (hw == 0) hw = 1;
@@ -441,14 +456,7 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
         ++p;
       });
     });
-    if (bias) {
-      // sum in path order, like a single pass over the ensemble would
-      int64_t p = 0;
-      for (int64_t t = 0; t < T; ++t) {
-        const int32_t g = ens->tree_group[t];
-        for (; p < tree_paths[(size_t)t + 1]; ++p) bias[g] += term[(size_t)p];
-      }
-    }
+    if (bias) sum_bias(ens, tree_paths.data(), term.data(), bias);
     return GTS_OK;
   } catch (const std::bad_alloc&) {
     return fail(GTS_ENOMEM, "host allocation failed");
@@ -1066,15 +1074,8 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
         ++p;
       });
     });
-    // bias: sum in path order, like a single pass over the ensemble would
     std::vector<double> bsum((size_t)ens->num_groups, 0.0);
-    {
-      int64_t p = 0;
-      for (int64_t t = 0; t < T; ++t) {
-        const int32_t g = ens->tree_group[t];
-        for (; p < tree_first[(size_t)t + 1]; ++p) bsum[(size_t)g] += term[(size_t)p];
-      }
-    }
+    sum_bias(ens, tree_first.data(), term.data(), bsum.data());
     if (bias)
       for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = bsum[(size_t)g];
     if (blob) {
