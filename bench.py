@@ -177,6 +177,25 @@ def time_prepare(gts, ens, dtype, reps=5):
     return 1e3 * float(np.median(host)), 1e3 * float(np.median(up)), int(len(blob))
 
 
+def time_device_extract(torch, gts, ens, reps=5):
+    """gts_extract_paths_device (paths and bias on the GPU from device-resident
+    node arrays), wall clock per call including its two count read-backs;
+    gts_extract_paths on the host for comparison."""
+    dens = gts.DeviceEnsemble(ens)
+    raw, _, _ = gts.extract_paths_device(dens)
+    torch.cuda.synchronize()
+    dev, host = [], []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        gts.extract_paths_device(dens)
+        torch.cuda.synchronize()
+        dev.append(time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        gts.extract_paths(ens)
+        host.append(time.perf_counter() - t0)
+    return 1e3 * float(np.median(dev)), 1e3 * float(np.median(host))
+
+
 def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
     w = synth.workload(workload)
     ens = w.ensemble
@@ -184,6 +203,7 @@ def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
     Xd = torch.from_numpy(w.X).cuda()
     q = path_features(gts, ens)
     host_ms, upload_ms, blob_bytes = time_prepare(gts, ens, dtype)
+    dev_extract_ms, host_extract_ms = time_device_extract(torch, gts, ens)
     model = gts.prepare(ens, dtype)
     k = time_kernel(torch, gts, model, Xd, reps, interactions)
     med = float(np.median(k))
@@ -196,6 +216,7 @@ def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
                    + (f", {ens.num_features + 1}]" if interactions else "]")),
         "paths": int(len(q)), "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
         "host_prepare_ms": host_ms, "upload_ms": upload_ms, "model_bytes": blob_bytes,
+        "extract_ms_device": dev_extract_ms, "extract_ms_host": host_extract_ms,
         "kernel_ms_median": med, "kernel_ms_mean": float(k.mean()),
         "kernel_ms_std": float(k.std()), "kernel_runs": len(k),
         "kernel_rows_per_s": rows / (med * 1e-3),

@@ -5,6 +5,7 @@
  *
  * Pipeline (Section 3, steps 1-4):
  *   gts_extract_paths   host   ensemble -> merged unique root-to-leaf paths
+ *   gts_extract_paths_device  the same on the GPU, bit for bit
  *   gts_pack_paths      host   paths -> bins of <= 64 path elements
  *   gts_model_layout    host   packed paths -> one device-ready byte blob
  *   gts_prepare_model   host   the three steps above in one pass
@@ -126,9 +127,10 @@ typedef struct gts_model {
  * num_elements, num_paths  (out) totals; always written on GTS_OK and
  *           GTS_EBUFSIZE.
  * bias      (out, may be NULL) host double[G]: per group the sum over its
- *           paths, in path order, of v times the product of the path's zero
- *           fractions -- the expected model output f of the empty feature set
- *           (the bias term phi_0 of Eq. 1).
+ *           paths of v times the product of the path's zero fractions -- the
+ *           expected model output f of the empty feature set (the bias term
+ *           phi_0 of Eq. 1).  Each tree sums its paths' terms in path order,
+ *           then each group sums its trees' sums in tree order.
  * Errors: GTS_EINVAL for out-of-range children, a node reached twice (cycle
  * or shared child), feature outside [0, M), group outside [0, G), negative or
  * non-finite cover, NaN threshold; GTS_EBUFSIZE if capacity is too small.
@@ -136,6 +138,51 @@ typedef struct gts_model {
 gts_status gts_extract_paths(const gts_ensemble *ens, gts_path_element *out,
                              int64_t capacity, int64_t *num_elements,
                              int64_t *num_paths, double *bias);
+
+/*
+ * gts_extract_workspace_bytes -- size of the device workspace that
+ * gts_extract_paths_device needs for an ensemble of num_trees trees and
+ * num_nodes nodes (about 52 bytes per node).  Errors: GTS_EINVAL for NULL
+ * bytes or negative sizes.
+ */
+gts_status gts_extract_workspace_bytes(int64_t num_trees, int64_t num_nodes, int64_t *bytes);
+
+/*
+ * gts_extract_paths_device -- Sections 3.1 and 3.2 on the GPU: the output of
+ * gts_extract_paths (same elements in the same order, bit for bit, and the
+ * same bias), from an ensemble whose node arrays are in device memory.  One
+ * thread per leaf walks up to its root; scans over trees and paths place the
+ * paths; each tree sums its paths' bias terms in path order, each group its
+ * trees in tree order (the host's order).
+ *
+ * ens       host struct; num_features, num_groups, num_trees, num_nodes are
+ *           host values, every array pointer is a DEVICE pointer (same
+ *           layout as for gts_extract_paths).
+ * d_out     device array of `capacity` elements, or NULL to compute sizes
+ *           only.
+ * num_elements, num_paths  (out, host) totals; written on GTS_OK and
+ *           GTS_EBUFSIZE.
+ * d_bias    device double[G] or NULL.
+ * d_workspace  caller's device memory of workspace_bytes >=
+ *           gts_extract_workspace_bytes(num_trees, num_nodes); its contents
+ *           are overwritten and may be reused once the stream has passed the
+ *           call's work.
+ * stream    hipStream_t (NULL = default stream).  The call waits for the
+ *           stream twice (to read the path and element counts); the writes of
+ *           d_out and d_bias are enqueued and complete with the stream.
+ * Errors: GTS_EINVAL for a malformed ensemble.  Unlike the host call, which
+ * checks only the nodes reachable from each root, every node is checked
+ * (cover, child indices, feature, threshold, leaf value, at most one parent,
+ * no parent for a root); leaves not reachable from their root are skipped,
+ * as on the host.  Paths deeper than 256 splits give GTS_EINVAL, merged
+ * paths of more than 63 features GTS_EPATHLEN (a bin holds at most 64
+ * elements); GTS_EBUFSIZE for a workspace or capacity too small;
+ * GTS_EDEVICE if a HIP call fails.
+ */
+gts_status gts_extract_paths_device(const gts_ensemble *ens, gts_path_element *d_out,
+                                    int64_t capacity, int64_t *num_elements,
+                                    int64_t *num_paths, double *d_bias, void *d_workspace,
+                                    int64_t workspace_bytes, void *stream);
 
 /*
  * gts_pack_paths -- Section 3.3 (bin packing for work allocation).

@@ -2,8 +2,10 @@
 
 The host half (extraction, packing, layout) is plain C++ built by g++ without
 floating-point contraction; the device half is HIP C++ built by hipcc for
-gfx950 with packed-FP32 instruction selection disabled.  Both objects are
-linked into ``paper_2010_13972_amd/libgts.so``.
+gfx950 with packed-FP32 instruction selection disabled: the SHAP kernels, and
+the device path extraction built without floating-point contraction (its
+output must equal the host's bit for bit).  The objects are linked into
+``paper_2010_13972_amd/libgts.so``.
 """
 from __future__ import annotations
 
@@ -22,9 +24,10 @@ ARCH = "gfx950"
 
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall", "-Wextra",
               "-Wno-unused-parameter"]
-HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
-             "-ffp-contract=fast", "-munsafe-fp-atomics",
-             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+HIP_COMMON = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
+              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+HIP_FLAGS = HIP_COMMON + ["-ffp-contract=fast", "-munsafe-fp-atomics"]
+EXTRACT_FLAGS = HIP_COMMON + ["-ffp-contract=off"]
 
 
 def _run(cmd, verbose):
@@ -47,15 +50,18 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
                 os.path.join(CSRC, "gts_host.cpp"), "-o", host_obj]
     dev_cmd = ["hipcc", *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c",
                os.path.join(CSRC, "gts_kernels.hip"), "-o", dev_obj]
+    ext_obj = os.path.join(BUILD, "gts_extract.o")
+    ext_cmd = ["hipcc", *EXTRACT_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c",
+               os.path.join(CSRC, "gts_extract.hip"), "-o", ext_obj]
     if save_temps:
         dev_cmd += ["-save-temps=obj"]
-    with ThreadPoolExecutor(2) as ex:
-        futs = [ex.submit(_run, host_cmd, verbose), ex.submit(_run, dev_cmd, verbose)]
+    with ThreadPoolExecutor(3) as ex:
+        futs = [ex.submit(_run, c, verbose) for c in (host_cmd, dev_cmd, ext_cmd)]
         for f in futs:
             f.result()
     tmp = LIB + ".tmp"
-    _run(["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC", host_obj, dev_obj, "-o", tmp],
-         verbose)
+    _run(["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC", host_obj, dev_obj, ext_obj,
+          "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

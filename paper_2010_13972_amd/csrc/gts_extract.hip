@@ -1,0 +1,533 @@
+// Path extraction on the GPU (Sections 3.1-3.2): the unique root-to-leaf
+// paths of an ensemble whose node arrays are in device memory, with repeated
+// features merged, written in the canonical order of gts_extract_paths and
+// bit for bit equal to it, plus the bias of every output group.
+//
+// One thread per node validates it and links it to its parent; one thread
+// per leaf then walks up to its tree's root, which
+//   - counts the leaves under every node (atomic increments on the way up),
+//   - gives the leaf's rank in depth-first preorder with the left child
+//     first: the number of leaves under every left sibling it passes,
+//   - collects the splits of its path, which it replays from the root down to
+//     merge repeated features (ranges intersected, zero fractions multiplied
+//     in root-to-leaf order, features kept in ascending order).
+// Scans over trees and paths place every path; each tree sums its paths' bias
+// terms v * prod(z) in path order and each group its trees' sums in tree
+// order, the order the host uses.
+//
+// Compiled without floating-point contraction: the cover ratios (IEEE
+// division), their products and the bias sums round exactly as on the host.
+#include <hip/hip_runtime.h>
+
+#include <rocprim/device/device_scan.hpp>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+
+#include "gts_internal.h"
+
+namespace gts {
+namespace {
+
+constexpr int kMaxDepth = 256;      // longest root-to-leaf chain of splits
+constexpr int kMaxMerged = kMaxPathLen - 1;  // features a merged path may hold
+constexpr int kThreads = 256;
+
+// Error codes recorded by the kernels (first one wins).
+enum ExtractError : int {
+  kOk = 0,
+  kBadOffsets = 1,
+  kBadGroup = 2,
+  kBadCover = 3,
+  kBadValue = 4,
+  kBadChild = 5,
+  kBadFeature = 6,
+  kNanThreshold = 7,
+  kTwoParents = 8,
+  kRootHasParent = 9,
+  kTooDeep = 10,
+  kTooLong = 11
+};
+
+struct DevEnsemble {
+  const int64_t* __restrict__ off;
+  const int32_t* __restrict__ group;
+  const int32_t* __restrict__ left;
+  const int32_t* __restrict__ right;
+  const int32_t* __restrict__ feature;
+  const float* __restrict__ threshold;
+  const double* __restrict__ cover;
+  const double* __restrict__ value;
+  int64_t T;
+  int64_t N;
+  int32_t M;
+  int32_t G;
+};
+
+// Workspace arrays (every array 256-byte aligned in the caller's buffer).
+struct Work {
+  int32_t* err;        // [4] code, tree, node, unused
+  int32_t* parent;     // [N] local index of the parent, -1 for none
+  int32_t* npar;       // [N] number of parents
+  int32_t* leaves;     // [N] reachable leaves under the node
+  int32_t* rank;       // [N] on a reachable leaf: preorder rank in its tree, else -1
+  int32_t* merged;     // [N] on a reachable leaf: merged path length (features)
+  int64_t* tree_leaves;  // [T+1] reachable leaves per tree
+  int64_t* tree_off;     // [T+1] their exclusive scan: first path of every tree
+  int64_t* path_leaf;    // [N] leaf node (global index) of each path
+  int64_t* path_elems;   // [N+1] elements per path
+  int64_t* elem_off;     // [N+1] their exclusive scan: first element of every path
+  double* term;          // [N] bias term of each path
+  double* tree_sum;      // [T] bias terms summed per tree
+  void* scan_tmp;
+  size_t scan_bytes;
+};
+
+__device__ __forceinline__ void record(int32_t* err, int code, int64_t tree, int64_t node) {
+  if (atomicCAS(&err[0], 0, code) == 0) {
+    err[1] = (int32_t)tree;
+    err[2] = (int32_t)node;
+  }
+}
+
+// Tree of global node gi: the last t with off[t] <= gi.
+__device__ __forceinline__ int64_t tree_of(const DevEnsemble& e, int64_t gi) {
+  int64_t lo = 0, hi = e.T - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (e.off[mid] <= gi) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ double cover_ratio(double child, double parent) {
+  return parent > 0.0 ? child / parent : 0.0;
+}
+
+__device__ __forceinline__ bool is_leaf(const DevEnsemble& e, int64_t gi) {
+  return e.left[gi] < 0 && e.right[gi] < 0;
+}
+
+__global__ void k_zero(double* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.0;
+}
+
+__global__ void k_init(DevEnsemble e, Work w) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < e.N) {
+    w.parent[i] = -1;
+    w.npar[i] = 0;
+    w.leaves[i] = 0;
+    w.rank[i] = -1;
+    w.merged[i] = 0;
+  }
+  if (i <= e.T) w.tree_leaves[i] = 0;
+  if (i <= e.N) w.path_elems[i] = 0;
+  if (i < 4) w.err[i] = 0;
+}
+
+// Tree table: offsets start at 0, grow strictly, end at N; groups in range.
+__global__ void k_trees(DevEnsemble e, Work w) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= e.T) return;
+  const int64_t a = e.off[t], b = e.off[t + 1];
+  if ((t == 0 && a != 0) || b <= a || b - a > INT32_MAX || (t == e.T - 1 && b != e.N))
+    record(w.err, kBadOffsets, t, -1);
+  const int32_t g = e.group[t];
+  if (g < 0 || g >= e.G) record(w.err, kBadGroup, t, -1);
+}
+
+// Per node: field checks and the parent links.
+__global__ void k_nodes(DevEnsemble e, Work w) {
+  const int64_t gi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= e.N) return;
+  const int64_t t = tree_of(e, gi);
+  const int64_t base = e.off[t];
+  const int64_t size = e.off[t + 1] - base;
+  const int64_t n = gi - base;
+  const double r = e.cover[gi];
+  if (!(r >= 0.0) || !isfinite(r)) record(w.err, kBadCover, t, n);
+  const int32_t a = e.left[gi], b = e.right[gi];
+  if (a < 0 && b < 0) {
+    if (!isfinite(e.value[gi])) record(w.err, kBadValue, t, n);
+    return;
+  }
+  if (a < 0 || b < 0 || a >= size || b >= size) {
+    record(w.err, kBadChild, t, n);
+    return;
+  }
+  const int32_t d = e.feature[gi];
+  if (d < 0 || d >= e.M) record(w.err, kBadFeature, t, n);
+  if (isnan(e.threshold[gi])) record(w.err, kNanThreshold, t, n);
+  atomicAdd(&w.npar[base + a], 1);
+  atomicAdd(&w.npar[base + b], 1);
+  w.parent[base + a] = (int32_t)n;
+  w.parent[base + b] = (int32_t)n;
+}
+
+// Per node: every node has at most one parent, a root none.  Per reachable
+// leaf: count it under every node on its way up.  A leaf whose way up does
+// not end at its tree's root (a parentless inner node, or a loop found by
+// taking more steps than the tree has nodes) is not part of the tree.
+__global__ void k_count(DevEnsemble e, Work w) {
+  const int64_t gi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= e.N) return;
+  const int64_t t = tree_of(e, gi);
+  const int64_t base = e.off[t];
+  const int64_t size = e.off[t + 1] - base;
+  const int64_t n = gi - base;
+  const int32_t np = w.npar[gi];
+  if (np > 1) record(w.err, kTwoParents, t, n);
+  if (n == 0 && np > 0) record(w.err, kRootHasParent, t, n);
+  if (!is_leaf(e, gi)) return;
+  int64_t steps = 0;
+  int32_t a = (int32_t)n;
+  while (a != 0) {
+    a = w.parent[base + a];
+    if (a < 0 || ++steps > size) return;  // not reachable from the root
+  }
+  if (steps > kMaxDepth) {
+    record(w.err, kTooDeep, t, n);
+    return;
+  }
+  a = (int32_t)n;
+  atomicAdd(&w.leaves[base + a], 1);
+  while (a != 0) {
+    a = w.parent[base + a];
+    atomicAdd(&w.leaves[base + a], 1);
+  }
+}
+
+// The merged elements of the path ending at leaf n of the tree at base:
+// features ascending with their ranges and zero fractions.  Returns the
+// number of features, or -1 if more than kMaxMerged.
+struct Merged {
+  int32_t f[kMaxMerged];
+  float lo[kMaxMerged];
+  float hi[kMaxMerged];
+  double z[kMaxMerged];
+};
+
+__device__ int merge_path(const DevEnsemble& e, const Work& w, int64_t base, int32_t n,
+                          int32_t* chain, Merged& m) {
+  // chain[0..d) = the path's nodes from the leaf's parent up to the root
+  int d = 0;
+  int32_t c = n;
+  while (c != 0) {
+    c = w.parent[base + c];
+    chain[d++] = c;
+  }
+  int cnt = 0;
+  for (int k = d - 1; k >= 0; --k) {
+    const int32_t a = chain[k];
+    const int32_t child = k > 0 ? chain[k - 1] : n;
+    const int64_t ga = base + a;
+    const int32_t f = e.feature[ga];
+    const float th = e.threshold[ga];
+    const bool right = e.right[ga] == child;
+    const double ratio = cover_ratio(e.cover[base + child], e.cover[ga]);
+    int i = 0;
+    while (i < cnt && m.f[i] < f) ++i;
+    if (i == cnt || m.f[i] != f) {
+      if (cnt == kMaxMerged) return -1;
+      for (int j = cnt; j > i; --j) {
+        m.f[j] = m.f[j - 1];
+        m.lo[j] = m.lo[j - 1];
+        m.hi[j] = m.hi[j - 1];
+        m.z[j] = m.z[j - 1];
+      }
+      m.f[i] = f;
+      m.lo[i] = -INFINITY;
+      m.hi[i] = INFINITY;
+      m.z[i] = 1.0;
+      ++cnt;
+    }
+    if (right) {
+      if (th > m.lo[i]) m.lo[i] = th;
+    } else {
+      if (th < m.hi[i]) m.hi[i] = th;
+    }
+    m.z[i] = m.z[i] * ratio;
+  }
+  return cnt;
+}
+
+// Per reachable leaf: preorder rank (leaves under the left siblings passed on
+// the way up) and merged length; reachable leaves per tree.
+__global__ void k_rank(DevEnsemble e, Work w) {
+  const int64_t gi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= e.N) return;
+  const int64_t t = tree_of(e, gi);
+  const int64_t base = e.off[t];
+  const int32_t n = (int32_t)(gi - base);
+  if (n == 0) w.tree_leaves[t] = w.leaves[base];
+  if (!is_leaf(e, gi) || w.leaves[gi] == 0) return;  // not reachable
+  int32_t rank = 0;
+  int32_t c = n;
+  while (c != 0) {
+    const int32_t a = w.parent[base + c];
+    if (e.right[base + a] == c) rank += w.leaves[base + e.left[base + a]];
+    c = a;
+  }
+  w.rank[gi] = rank;
+  int32_t chain[kMaxDepth];
+  Merged m;
+  const int cnt = merge_path(e, w, base, n, chain, m);
+  if (cnt < 0) {
+    record(w.err, kTooLong, t, n);
+    return;
+  }
+  w.merged[gi] = cnt;
+}
+
+// Per reachable leaf: its path index; elements per path.
+__global__ void k_place(DevEnsemble e, Work w) {
+  const int64_t gi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gi >= e.N) return;
+  const int32_t r = w.rank[gi];
+  if (r < 0) return;
+  const int64_t t = tree_of(e, gi);
+  const int64_t p = w.tree_off[t] + r;
+  w.path_leaf[p] = gi;
+  w.path_elems[p] = (int64_t)w.merged[gi] + 1;
+}
+
+// Per path: write its elements; its bias term v * prod(z).
+__global__ void k_emit(DevEnsemble e, Work w, gts_path_element* __restrict__ out, int64_t P) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= P) return;
+  const int64_t gi = w.path_leaf[p];
+  const int64_t t = tree_of(e, gi);
+  const int64_t base = e.off[t];
+  const int32_t g = e.group[t];
+  int32_t chain[kMaxDepth];
+  Merged m;
+  const int cnt = merge_path(e, w, base, (int32_t)(gi - base), chain, m);
+  const double v = e.value[gi];
+  double prod = 1.0;
+  for (int i = 0; i < cnt; ++i) prod = prod * m.z[i];
+  w.term[p] = v * prod;
+  if (out == nullptr) return;
+  gts_path_element* el = out + w.elem_off[p];
+  gts_path_element r;
+  r.path_idx = p;
+  r.feature_idx = -1;
+  r.group = g;
+  r.lower = -INFINITY;
+  r.upper = INFINITY;
+  r.zero_fraction = 1.0;
+  r.v = v;
+  el[0] = r;
+  for (int i = 0; i < cnt; ++i) {
+    r.feature_idx = m.f[i];
+    r.lower = m.lo[i];
+    r.upper = m.hi[i];
+    r.zero_fraction = m.z[i];
+    el[i + 1] = r;
+  }
+}
+
+// Per tree: its paths' bias terms in path order.
+__global__ void k_tree_sum(DevEnsemble e, Work w) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= e.T) return;
+  double s = 0.0;
+  for (int64_t p = w.tree_off[t]; p < w.tree_off[t + 1]; ++p) s = s + w.term[p];
+  w.tree_sum[t] = s;
+}
+
+// Per group: its trees' sums in tree order.
+__global__ void k_bias(DevEnsemble e, Work w, double* __restrict__ bias) {
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= e.G) return;
+  double s = 0.0;
+  for (int64_t t = 0; t < e.T; ++t)
+    if (e.group[t] == g) s = s + w.tree_sum[t];
+  bias[g] = s;
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+
+constexpr int64_t kAlign = 256;
+
+inline int64_t up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t scan_temp_bytes(int64_t n) {
+  size_t bytes = 0;
+  int64_t* null = nullptr;
+  if (rocprim::exclusive_scan(nullptr, bytes, null, null, int64_t(0), (size_t)n,
+                              rocprim::plus<int64_t>()) != hipSuccess)
+    return 0;
+  return bytes;
+}
+
+// Byte offsets of the workspace arrays; returns the total.
+constexpr int kArrays = 15;
+
+int64_t plan(int64_t T, int64_t N, int64_t* o, size_t* scan_bytes) {
+  const int64_t n1 = N > 0 ? N : 1;
+  *scan_bytes = std::max(scan_temp_bytes(T + 1), scan_temp_bytes(n1 + 1));
+  const int64_t t1 = T > 0 ? T : 1;
+  const int64_t sizes[kArrays] = {4 * 4,        0,            4 * n1,           4 * n1,
+                                  4 * n1,       4 * n1,       4 * n1,           8 * (T + 1),
+                                  8 * (T + 1),  8 * n1,       8 * (n1 + 1),     8 * (n1 + 1),
+                                  8 * n1,       8 * t1,       (int64_t)*scan_bytes};
+  int64_t at = 0;
+  for (int i = 0; i < kArrays; ++i) {
+    o[i] = at;
+    at += up(sizes[i] > 0 ? sizes[i] : 1);
+  }
+  return at;
+}
+
+Work bind(void* ws, const int64_t* o, size_t scan_bytes) {
+  char* b = static_cast<char*>(ws);
+  Work w;
+  w.err = reinterpret_cast<int32_t*>(b + o[0]);
+  w.parent = reinterpret_cast<int32_t*>(b + o[2]);
+  w.npar = reinterpret_cast<int32_t*>(b + o[3]);
+  w.leaves = reinterpret_cast<int32_t*>(b + o[4]);
+  w.rank = reinterpret_cast<int32_t*>(b + o[5]);
+  w.merged = reinterpret_cast<int32_t*>(b + o[6]);
+  w.tree_leaves = reinterpret_cast<int64_t*>(b + o[7]);
+  w.tree_off = reinterpret_cast<int64_t*>(b + o[8]);
+  w.path_leaf = reinterpret_cast<int64_t*>(b + o[9]);
+  w.path_elems = reinterpret_cast<int64_t*>(b + o[10]);
+  w.elem_off = reinterpret_cast<int64_t*>(b + o[11]);
+  w.term = reinterpret_cast<double*>(b + o[12]);
+  w.tree_sum = reinterpret_cast<double*>(b + o[13]);
+  w.scan_tmp = b + o[14];
+  w.scan_bytes = scan_bytes;
+  return w;
+}
+
+const char* describe(int code) {
+  switch (code) {
+    case kBadOffsets: return "tree_node_offsets must start at 0, grow strictly and end at num_nodes";
+    case kBadGroup: return "tree group outside [0, G)";
+    case kBadCover: return "cover must be finite and >= 0";
+    case kBadValue: return "leaf value is not finite";
+    case kBadChild: return "child index out of range";
+    case kBadFeature: return "split feature outside [0, M)";
+    case kNanThreshold: return "threshold is NaN";
+    case kTwoParents: return "node reached twice (shared child or cycle)";
+    case kRootHasParent: return "the root is a child of another node (cycle)";
+    case kTooDeep: return "path deeper than the device extraction supports (256 splits)";
+    case kTooLong: return "merged path longer than a 64-element bin";
+    default: return "malformed ensemble";
+  }
+}
+
+inline unsigned blocks(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kThreads - 1) / kThreads); }
+
+}  // namespace
+}  // namespace gts
+
+using namespace gts;
+
+extern "C" gts_status gts_extract_workspace_bytes(int64_t num_trees, int64_t num_nodes,
+                                                  int64_t* bytes) {
+  clear_error();
+  if (bytes == nullptr) return fail(GTS_EINVAL, "bytes must not be NULL");
+  if (num_trees < 0 || num_nodes < 0) return fail(GTS_EINVAL, "sizes must be >= 0");
+  int64_t o[kArrays];
+  size_t sb = 0;
+  *bytes = plan(num_trees, num_nodes, o, &sb);
+  return GTS_OK;
+}
+
+extern "C" gts_status gts_extract_paths_device(const gts_ensemble* ens, gts_path_element* d_out,
+                                               int64_t capacity, int64_t* num_elements,
+                                               int64_t* num_paths, double* d_bias,
+                                               void* d_workspace, int64_t workspace_bytes,
+                                               void* stream) {
+  clear_error();
+  if (ens == nullptr || num_elements == nullptr || num_paths == nullptr)
+    return fail(GTS_EINVAL, "ensemble, num_elements and num_paths must not be NULL");
+  if (ens->num_features < 1 || ens->num_groups < 1 || ens->num_trees < 0 || ens->num_nodes < 0)
+    return fail(GTS_EINVAL, "ensemble sizes out of range");
+  if (capacity < 0) return fail(GTS_EINVAL, "capacity must be >= 0");
+  if (d_out == nullptr && capacity > 0) return fail(GTS_EINVAL, "out is NULL but capacity > 0");
+  const int64_t T = ens->num_trees, N = ens->num_nodes;
+  if (T > INT32_MAX || N > INT32_MAX) return fail(GTS_EINVAL, "ensemble too large");
+  *num_elements = 0;
+  *num_paths = 0;
+  if (T == 0) {
+    if (N != 0) return fail(GTS_EINVAL, "num_nodes must be 0 without trees");
+    if (d_bias) {
+      hipLaunchKernelGGL(k_zero, dim3(blocks(ens->num_groups)), dim3(kThreads), 0,
+                         static_cast<hipStream_t>(stream), d_bias, ens->num_groups);
+      if (hipGetLastError() != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed");
+    }
+    return GTS_OK;
+  }
+  if (!ens->tree_node_offsets || !ens->tree_group || !ens->left || !ens->right ||
+      !ens->feature || !ens->threshold || !ens->cover || !ens->value)
+    return fail(GTS_EINVAL, "an ensemble array pointer is NULL");
+  int64_t o[kArrays];
+  size_t scan_bytes = 0;
+  const int64_t need = plan(T, N, o, &scan_bytes);
+  if (d_workspace == nullptr || workspace_bytes < need)
+    return fail(GTS_EBUFSIZE, "workspace of %lld bytes needed", (long long)need);
+  DevEnsemble e{ens->tree_node_offsets, ens->tree_group, ens->left, ens->right, ens->feature,
+                ens->threshold, ens->cover, ens->value, T, N, ens->num_features,
+                ens->num_groups};
+  Work w = bind(d_workspace, o, scan_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const unsigned bn = blocks(std::max(N, T + 1)), bt = blocks(T);
+  hipLaunchKernelGGL(k_init, dim3(bn), dim3(kThreads), 0, s, e, w);
+  hipLaunchKernelGGL(k_trees, dim3(bt), dim3(kThreads), 0, s, e, w);
+  if (hipGetLastError() != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed");
+  // the node kernels read the offsets: check them first
+  int32_t err[4] = {0, 0, 0, 0};
+  if (hipMemcpyAsync(err, w.err, sizeof(err), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(GTS_EDEVICE, "copy of the error word failed");
+  if (err[0] != 0)
+    return fail(GTS_EINVAL, "tree %d: %s", err[1], describe(err[0]));
+  const unsigned b = blocks(N);
+  hipLaunchKernelGGL(k_nodes, dim3(b), dim3(kThreads), 0, s, e, w);
+  hipLaunchKernelGGL(k_count, dim3(b), dim3(kThreads), 0, s, e, w);
+  hipLaunchKernelGGL(k_rank, dim3(b), dim3(kThreads), 0, s, e, w);
+  if (hipGetLastError() != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed");
+  size_t sb = w.scan_bytes;
+  if (rocprim::exclusive_scan(w.scan_tmp, sb, w.tree_leaves, w.tree_off, int64_t(0),
+                              (size_t)(T + 1), rocprim::plus<int64_t>(), s) != hipSuccess)
+    return fail(GTS_EDEVICE, "scan over trees failed");
+  hipLaunchKernelGGL(k_place, dim3(b), dim3(kThreads), 0, s, e, w);
+  int64_t P = 0;
+  if (hipMemcpyAsync(err, w.err, sizeof(err), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipMemcpyAsync(&P, w.tree_off + T, sizeof(P), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(GTS_EDEVICE, "copy of the path count failed");
+  if (err[0] != 0)
+    return fail(err[0] == kTooLong ? GTS_EPATHLEN : GTS_EINVAL, "tree %d node %d: %s", err[1],
+                err[2], describe(err[0]));
+  // path_elems[P] is 0 (k_init), so the scan's last entry is the total
+  sb = w.scan_bytes;
+  if (rocprim::exclusive_scan(w.scan_tmp, sb, w.path_elems, w.elem_off, int64_t(0),
+                              (size_t)(P + 1), rocprim::plus<int64_t>(), s) != hipSuccess)
+    return fail(GTS_EDEVICE, "scan over paths failed");
+  int64_t n = 0;
+  if (hipMemcpyAsync(&n, w.elem_off + P, sizeof(n), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(GTS_EDEVICE, "copy of the element count failed");
+  *num_paths = P;
+  *num_elements = n;
+  if (d_out != nullptr && n > capacity)
+    return fail(GTS_EBUFSIZE, "capacity %lld < %lld elements", (long long)capacity,
+                (long long)n);
+  if (d_out == nullptr && d_bias == nullptr) return GTS_OK;
+  hipLaunchKernelGGL(k_emit, dim3(blocks(P)), dim3(kThreads), 0, s, e, w, d_out, P);
+  if (d_bias) {
+    hipLaunchKernelGGL(k_tree_sum, dim3(bt), dim3(kThreads), 0, s, e, w);
+    hipLaunchKernelGGL(k_bias, dim3(blocks(ens->num_groups)), dim3(kThreads), 0, s, e, w, d_bias);
+  }
+  if (hipGetLastError() != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed");
+  return GTS_OK;
+}

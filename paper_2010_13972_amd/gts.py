@@ -78,6 +78,11 @@ def lib() -> ctypes.CDLL:
         L.gts_prepare_model.argtypes = [ctypes.POINTER(_Ensemble), i32, i32, i32,
                                         ctypes.POINTER(ModelDesc), vp, i64, vp]
         L.gts_prepare_model.restype = st
+        L.gts_extract_workspace_bytes.argtypes = [i64, i64, vp]
+        L.gts_extract_workspace_bytes.restype = st
+        L.gts_extract_paths_device.argtypes = [ctypes.POINTER(_Ensemble), vp, i64, vp, vp, vp,
+                                               vp, i64, vp]
+        L.gts_extract_paths_device.restype = st
         for name in ("gts_shap", "gts_shap_interactions"):
             f = getattr(L, name)
             f.argtypes = [ctypes.POINTER(ModelDesc), vp, vp, i64, i64, vp, vp]
@@ -138,6 +143,59 @@ def extract_paths(ens) -> Tuple[np.ndarray, int, np.ndarray]:
     _check(lib().gts_extract_paths(ctypes.byref(s), _ptr(out), n.value, ctypes.byref(n),
                                    ctypes.byref(npaths), _ptr(bias)), "gts_extract_paths")
     return out, int(npaths.value), bias
+
+
+class DeviceEnsemble:
+    """An ensemble's node arrays in device memory (torch tensors), with the
+    gts_ensemble struct that points at them."""
+
+    def __init__(self, ens, device="cuda"):
+        import torch
+        _, arrs = _ensemble_struct(ens)
+        self.tensors = {k: torch.from_numpy(v).to(device) for k, v in arrs.items()}
+        t = self.tensors
+        self.num_trees = len(arrs["group"])
+        self.num_nodes = len(arrs["left"])
+        self.num_groups = ens.num_groups
+        self.struct = _Ensemble(ens.num_features, ens.num_groups, self.num_trees,
+                                self.num_nodes, t["off"].data_ptr(), t["group"].data_ptr(),
+                                t["left"].data_ptr(), t["right"].data_ptr(),
+                                t["feat"].data_ptr(), t["thr"].data_ptr(),
+                                t["cover"].data_ptr(), t["value"].data_ptr())
+
+
+def extract_paths_device(dens: DeviceEnsemble, stream=None, workspace=None):
+    """gts_extract_paths_device: (elements as a device uint8 tensor of
+    num_elements * 40 bytes, num_paths, bias as a device float64 tensor)."""
+    import torch
+    dev = dens.tensors["left"].device
+    ws_bytes = ctypes.c_int64(0)
+    _check(lib().gts_extract_workspace_bytes(dens.num_trees, dens.num_nodes,
+                                             ctypes.byref(ws_bytes)),
+           "gts_extract_workspace_bytes")
+    if workspace is None or workspace.numel() < ws_bytes.value:
+        workspace = torch.empty(ws_bytes.value, dtype=torch.uint8, device=dev)
+    n = ctypes.c_int64(0)
+    npaths = ctypes.c_int64(0)
+    h = _stream_handle(stream)
+    _check(lib().gts_extract_paths_device(ctypes.byref(dens.struct), None, 0, ctypes.byref(n),
+                                          ctypes.byref(npaths), None,
+                                          ctypes.c_void_p(workspace.data_ptr()),
+                                          workspace.numel(), h), "gts_extract_paths_device")
+    out = torch.empty(max(1, n.value) * PATH_ELEMENT.itemsize, dtype=torch.uint8, device=dev)
+    bias = torch.empty(dens.num_groups, dtype=torch.float64, device=dev)
+    _check(lib().gts_extract_paths_device(ctypes.byref(dens.struct),
+                                          ctypes.c_void_p(out.data_ptr()), n.value,
+                                          ctypes.byref(n), ctypes.byref(npaths),
+                                          ctypes.c_void_p(bias.data_ptr()),
+                                          ctypes.c_void_p(workspace.data_ptr()),
+                                          workspace.numel(), h), "gts_extract_paths_device")
+    return out[:n.value * PATH_ELEMENT.itemsize], int(npaths.value), bias
+
+
+def elements_from_device(raw) -> np.ndarray:
+    """A device byte tensor of gts_path_element records as a host array."""
+    return np.frombuffer(raw.cpu().numpy().tobytes(), dtype=PATH_ELEMENT).copy()
 
 
 def pack_paths(elements: np.ndarray, bin_capacity: int = 64,

@@ -360,3 +360,28 @@ def test_prepare_model_errors():
     with pytest.raises(gts.GtsError) as e:
         gts.prepare_blob(bad, "f32")
     assert e.value.status == gts.GTS_EINVAL
+
+
+def test_extract_workspace_and_device_argument_checks():
+    """Sizing and the argument checks of the device extraction run before any
+    HIP call."""
+    L = gts.lib()
+    b = ctypes.c_int64(0)
+    assert L.gts_extract_workspace_bytes(10, 1000, ctypes.byref(b)) == gts.GTS_OK
+    small = b.value
+    assert L.gts_extract_workspace_bytes(10, 100000, ctypes.byref(b)) == gts.GTS_OK
+    assert b.value > small >= 1000 * 40
+    assert L.gts_extract_workspace_bytes(-1, 10, ctypes.byref(b)) == gts.GTS_EINVAL
+    assert L.gts_extract_workspace_bytes(1, 10, None) == gts.GTS_EINVAL
+    n, p = ctypes.c_int64(0), ctypes.c_int64(0)
+    w = synth.workload("tiny")
+    s, keep = gts._ensemble_struct(w.ensemble)
+    vp = ctypes.c_void_p
+    f = L.gts_extract_paths_device
+    assert f(None, None, 0, ctypes.byref(n), ctypes.byref(p), None, None, 0, None) == gts.GTS_EINVAL
+    assert f(ctypes.byref(s), None, -1, ctypes.byref(n), ctypes.byref(p), None, None, 0,
+             None) == gts.GTS_EINVAL
+    assert f(ctypes.byref(s), None, 5, ctypes.byref(n), ctypes.byref(p), None, None, 0,
+             None) == gts.GTS_EINVAL
+    assert f(ctypes.byref(s), None, 0, ctypes.byref(n), ctypes.byref(p), None, None, 0,
+             None) == gts.GTS_EBUFSIZE
