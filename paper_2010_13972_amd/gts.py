@@ -262,28 +262,38 @@ def upload(desc: ModelDesc, blob: np.ndarray, num_features: int, num_groups: int
 
 
 def prepare_blob(ens, dtype: str = "f32", bin_capacity: int = 64, alg: str = "bfd",
-                 _cache={}):
+                 out: Optional[np.ndarray] = None, _cache={}):
     """gts_prepare_model: (ModelDesc, host blob, bias) straight from the
-    ensemble.  The blob size of the last model with the same node count is
-    tried first, so repeated preparation of one ensemble is a single call."""
+    ensemble.  The blob is written into ``out`` (a uint8 array, e.g. a view of
+    pinned memory) when it is large enough, else into a new array.  The blob
+    size of the last model with the same node count is tried first, so
+    repeated preparation of one ensemble is a single call."""
     s, keep = _ensemble_struct(ens)
     desc = ModelDesc()
     bias = np.zeros(ens.num_groups, np.float64)
     key = (ens.num_nodes, ens.num_trees, dtype, bin_capacity, alg)
     size = _cache.get(key, 0)
-    blob = np.empty(size, np.uint8) if size else None
+    if size and out is not None and out.nbytes >= size:
+        blob = out
+    else:
+        blob = np.empty(size, np.uint8) if size else None
+    cap = blob.nbytes if blob is not None else 0
     st = lib().gts_prepare_model(ctypes.byref(s), bin_capacity, PACK_ALGS[alg], DTYPES[dtype],
-                                 ctypes.byref(desc), _ptr(blob), size, _ptr(bias))
-    if st == GTS_OK and blob is not None and desc.bytes == size:
-        return desc, blob, bias
+                                 ctypes.byref(desc), _ptr(blob), cap, _ptr(bias))
+    if st == GTS_OK and blob is not None and desc.bytes <= cap:
+        _cache[key] = int(desc.bytes)
+        return desc, blob[:desc.bytes], bias
     if st not in (GTS_OK, GTS_EBUFSIZE):
         _check(st, "gts_prepare_model")
-    blob = np.empty(desc.bytes, np.uint8)
+    if out is not None and out.nbytes >= desc.bytes:
+        blob = out
+    else:
+        blob = np.empty(desc.bytes, np.uint8)
     _check(lib().gts_prepare_model(ctypes.byref(s), bin_capacity, PACK_ALGS[alg], DTYPES[dtype],
-                                   ctypes.byref(desc), _ptr(blob), len(blob), _ptr(bias)),
+                                   ctypes.byref(desc), _ptr(blob), blob.nbytes, _ptr(bias)),
            "gts_prepare_model")
     _cache[key] = int(desc.bytes)
-    return desc, blob, bias
+    return desc, blob[:desc.bytes], bias
 
 
 def prepare(ens, dtype: str = "f32", device="cuda", bin_capacity: int = 64,
