@@ -69,16 +69,16 @@ SUITE = [
 # Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
 # of the kernel source the counters were taken on.
 TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 18700998, "write_bytes": 35200000,
-                                    "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
-    ("interactions", "f32", True): {"fetch_bytes": 3321833, "write_bytes": 96800000,
-                                    "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
-    ("deep", "f32", False): {"fetch_bytes": 43088220, "write_bytes": 11520000,
-                             "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
-    ("deep", "f64", False): {"fetch_bytes": 57125688, "write_bytes": 17280000,
-                             "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
-    ("wide", "f32", False): {"fetch_bytes": 6322184028, "write_bytes": 316800000,
-                             "source": "d52943017fafabdcfba38ed842233166eda6a5e2c68b3deba8176e5aef92d5b0"},
+    ("covtype_med", "f32", False): {"fetch_bytes": 18740683, "write_bytes": 35200000,
+        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
+    ("interactions", "f32", True): {"fetch_bytes": 13808800, "write_bytes": 127751885,
+        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
+    ("deep", "f32", False): {"fetch_bytes": 43063521, "write_bytes": 11520000,
+        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
+    ("deep", "f64", False): {"fetch_bytes": 56777524, "write_bytes": 17280000,
+        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
+    ("wide", "f32", False): {"fetch_bytes": 5961550399, "write_bytes": 316800086,
+        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
 }
 
 
@@ -178,7 +178,8 @@ def time_kernel(torch, gts, model, Xd, reps, interactions):
     fn = kernel_fn(gts, interactions)
     stream = torch.cuda.current_stream()
     out = fn(model, Xd)
-    out = fn(model, Xd, out=out)
+    for _ in range(4):
+        out = fn(model, Xd, out=out)
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(reps)]
@@ -256,27 +257,37 @@ def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
 
 
 def cpu_baseline(oracle, ens, X, budget_s: float, interactions: bool):
-    """The oracle as it stands, on a row prefix sized to about budget_s of
-    work on all usable cores, then on one thread for a third of that."""
+    """The oracle as it stands, on all usable cores, on a bounded sample of
+    the batch: a row prefix grown until one call takes about budget_s / 2, or
+    the whole batch repeated until that much time has passed; then on one
+    thread for about budget_s / 4."""
     threads = len(os.sched_getaffinity(0))
     env = os.environ.get("OMP_NUM_THREADS")
     if env and env.isdigit():
         threads = min(threads, int(env))
     fn = oracle.interactions if interactions else oracle.treeshap
 
-    def run(nthreads, budget):
+    def run(nthreads, target):
         n = 8 if interactions else 64
         while True:
             n = min(n, X.shape[0])
             t0 = time.perf_counter()
             fn(ens, X[:n], nthreads=nthreads)
             dt = time.perf_counter() - t0
-            if dt >= budget / 3 or n == X.shape[0]:
-                return n, dt
-            n = min(X.shape[0], int(n * max(2.0, budget / 3 / max(dt, 1e-3))))
+            if dt >= target or n == X.shape[0]:
+                break
+            n = min(X.shape[0], max(n + 1, int(n * 1.05 * target / max(dt, 1e-3))))
+        passes = 1
+        if dt < target:
+            passes = max(1, int(np.ceil(target / max(dt, 1e-3))))
+            t0 = time.perf_counter()
+            for _ in range(passes):
+                fn(ens, X[:n], nthreads=nthreads)
+            dt = time.perf_counter() - t0
+        return n, passes, dt
 
-    n, dt = run(threads, budget_s)
-    n1, dt1 = run(1, budget_s / 3)
+    n, passes, dt = run(threads, budget_s / 2)
+    n1, passes1, dt1 = run(1, budget_s / 4)
     cpu = ""
     try:
         with open("/proc/cpuinfo") as f:
@@ -286,11 +297,12 @@ def cpu_baseline(oracle, ens, X, budget_s: float, interactions: bool):
                     break
     except OSError:
         pass
-    return {"value": n / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n} of {X.shape[0]} rows in {dt:.2f} s, fp64 "
-                      f"{'conditioning interactions' if interactions else 'Algorithm 1'}, "
-                      f"OpenMP over rows",
-            "one_thread_value": n1 / dt1, "one_thread_sample": f"first {n1} rows in {dt1:.2f} s",
+    what = "conditioning interactions" if interactions else "Algorithm 1"
+    return {"value": n * passes / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n} of {X.shape[0]} rows x {passes} pass(es) in {dt:.2f} s, fp64 "
+                      f"{what}, OpenMP over rows",
+            "one_thread_value": n1 * passes1 / dt1,
+            "one_thread_sample": f"first {n1} rows x {passes1} pass(es) in {dt1:.2f} s",
             "cpu": cpu}
 
 
@@ -435,7 +447,9 @@ def main():
     ap.add_argument("--no-suite", action="store_true",
                     help="skip the per-workload suite (kernel and preparation of every workload)")
     ap.add_argument("--suite-reps", type=int, default=10)
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--cpu-budget", type=float, default=16.0,
+                    help="seconds of oracle time for the CPU baseline (about half on all "
+                         "cores, a quarter on one thread)")
     ap.add_argument("--experiment", default=None, choices=["packers", "rows"],
                     help="instead of the bench line, print one JSON line of an experiment: "
                          "the packing heuristics (Table 5 with kernel times) or the rows "
