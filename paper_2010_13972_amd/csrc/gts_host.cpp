@@ -990,6 +990,97 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
   }
 }
 
+namespace gts {
+namespace {
+
+// One tree's paths from a single walk: merged feature elements of every path
+// (concatenated, ascending feature order), with each path's length (root
+// included), leaf value and bias term v * prod(z).
+struct TreeOut {
+  std::vector<Split> el;
+  std::vector<int64_t> first;  // per path: its first element in el
+  std::vector<int32_t> size;
+  std::vector<double> v;
+  std::vector<double> term;
+  void clear() {
+    el.clear();
+    first.clear();
+    size.clear();
+    v.clear();
+    term.clear();
+  }
+};
+
+// Writes the paths of bin b into the blob, rotating each path's features as
+// rotate_bin does (same choices, taken from the feature-sorted source).
+template <typename Z>
+void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees,
+               const int64_t* path_tree, const int64_t* tree_first, const int64_t* bin_paths,
+               int64_t p0, int64_t p1, const int64_t* dest, std::vector<uint64_t>& used,
+               std::vector<int32_t>& touched) {
+  const float inf = std::numeric_limits<float>::infinity();
+  int32_t* const feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]);
+  float* const lower = reinterpret_cast<float*>(blob + m.off[kLower]);
+  float* const upper = reinterpret_cast<float*>(blob + m.off[kUpper]);
+  Z* const zero = reinterpret_cast<Z*>(blob + m.off[kZero]);
+  uint64_t* const u = used.data();
+  int32_t t_in_bin = 0;
+  for (int64_t i = p0; i < p1; ++i, ++t_in_bin) {
+    const int64_t p = bin_paths[i];
+    const int64_t t = path_tree[p];
+    const TreeOut& tr = trees[(size_t)t];
+    const size_t j = (size_t)(p - tree_first[t]);
+    const Split* src = tr.el.data() + tr.first[j];
+    const int32_t q = tr.size[j] - 1;
+    const int64_t d = dest[p];
+    feat[d] = -1;
+    lower[d] = -inf;
+    upper[d] = inf;
+    zero[d] = (Z)tr.v[j];
+    int32_t best = 0;
+    if (q > 1) {
+      int32_t cost[kMaxPathLen];
+      for (int32_t k = 0; k < q; ++k) cost[k] = 0;
+      const uint64_t in_q = q >= 64 ? ~0ull : (1ull << q) - 1;
+      for (int32_t jj = 0; jj < q; ++jj) {
+        uint64_t bits = u[src[jj].feature] & in_q;
+        while (bits) {
+          const int32_t k = __builtin_ctzll(bits);
+          bits &= bits - 1;
+          ++cost[jj >= k ? jj - k : jj - k + q];
+        }
+      }
+      int32_t rho = t_in_bin % q, best_cost = INT32_MAX;
+      for (int32_t c = 0; c < q; ++c) {
+        if (cost[rho] < best_cost) {
+          best_cost = cost[rho];
+          best = rho;
+          if (best_cost == 0) break;
+        }
+        if (++rho == q) rho = 0;
+      }
+    }
+    int32_t sk = best;
+    for (int32_t k = 0; k < q; ++k, ++sk) {
+      if (sk == q) sk = 0;
+      const Split& e = src[sk];
+      const int64_t o = d + 1 + k;
+      feat[o] = e.feature;
+      lower[o] = e.lower;
+      upper[o] = e.upper;
+      zero[o] = (Z)e.zero_fraction;
+      uint64_t& bits = u[e.feature];
+      if (bits == 0) touched.push_back(e.feature);
+      bits |= 1ull << k;
+    }
+  }
+  for (int32_t f : touched) used[(size_t)f] = 0;
+  touched.clear();
+}
+
+}  // namespace
+}  // namespace gts
+
 extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_capacity,
                                         int32_t alg, int32_t dtype, gts_model* model,
                                         void* host_blob, int64_t blob_capacity, double* bias) {
@@ -1006,13 +1097,31 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
   if (st != GTS_OK) return st;
   try {
     const int64_t T = ens->num_trees;
-    // walk 1: the merged length of every path, per tree
-    std::vector<std::vector<int32_t>> tree_sizes((size_t)T);
+    const bool sizes_only = host_blob == nullptr && bias == nullptr;
+    // one walk: every path's merged elements (only their count for a size
+    // query), per tree
+    // (kept per calling thread between calls; the pool's workers write into
+    // the caller's copy)
+    static thread_local std::vector<TreeOut> tls_trees;
+    std::vector<TreeOut>& trees = tls_trees;
+    if ((int64_t)trees.size() < T) trees.resize((size_t)T);
     std::vector<gts_status> status;
     for_each_tree(ens, status, [&](int64_t t, Walker& w) {
-      std::vector<int32_t>& sz = tree_sizes[(size_t)t];
-      sz.clear();
-      return w.walk<false>(ens, t, [&](int32_t, size_t m) { sz.push_back((int32_t)m + 1); });
+      TreeOut& out = trees[(size_t)t];
+      out.clear();
+      if (sizes_only)
+        return w.walk<false>(ens, t, [&](int32_t, size_t m) { out.size.push_back((int32_t)m + 1); });
+      const int64_t base = ens->tree_node_offsets[t];
+      return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
+        const double v = ens->value[base + leaf];
+        double prod = 1.0;
+        for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
+        out.first.push_back((int64_t)out.el.size());
+        out.el.insert(out.el.end(), w.merged.begin(), w.merged.begin() + (std::ptrdiff_t)m);
+        out.size.push_back((int32_t)m + 1);
+        out.v.push_back(v);
+        out.term.push_back(v * prod);
+      });
     });
     for (int64_t t = 0; t < T; ++t)
       if (status[(size_t)t] != GTS_OK) {
@@ -1021,17 +1130,19 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       }
     std::vector<int64_t> tree_first((size_t)T + 1, 0);
     for (int64_t t = 0; t < T; ++t)
-      tree_first[(size_t)t + 1] = tree_first[(size_t)t] + (int64_t)tree_sizes[(size_t)t].size();
+      tree_first[(size_t)t + 1] = tree_first[(size_t)t] + (int64_t)trees[(size_t)t].size.size();
     const int64_t P = tree_first[(size_t)T];
     std::vector<int32_t> size((size_t)P), group((size_t)P);
+    std::vector<int64_t> path_tree((size_t)P);
     int64_t n = 0;
     int32_t maxlen = 0;
     for (int64_t t = 0; t < T; ++t) {
-      const std::vector<int32_t>& sz = tree_sizes[(size_t)t];
+      const std::vector<int32_t>& sz = trees[(size_t)t].size;
       for (size_t k = 0; k < sz.size(); ++k) {
         const int64_t p = tree_first[(size_t)t] + (int64_t)k;
         size[(size_t)p] = sz[k];
         group[(size_t)p] = ens->tree_group[t];
+        path_tree[(size_t)p] = t;
         n += sz[k];
         maxlen = std::max(maxlen, sz[k]);
       }
@@ -1046,41 +1157,51 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     assign_bins(size.data(), group.data(), P, bin_capacity, alg, pk, true);
     const BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
     *model = bp.m;
-    if (host_blob == nullptr && bias == nullptr) return GTS_OK;
+    if (sizes_only) return GTS_OK;
     if (host_blob != nullptr && blob_capacity < bp.m.bytes)
       return fail(GTS_EBUFSIZE, "blob_capacity %lld < %lld bytes", (long long)blob_capacity,
                   (long long)bp.m.bytes);
-    char* blob = static_cast<char*>(host_blob);
-    // walk 2: each path's elements straight to their packed position
-    std::vector<double> term((size_t)P);
-    const float inf = std::numeric_limits<float>::infinity();
-    for_each_tree(ens, status, [&](int64_t t, Walker& w) {
-      const int64_t base = ens->tree_node_offsets[t];
-      int64_t p = tree_first[(size_t)t];
-      return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
-        const double v = ens->value[base + leaf];
-        double prod = 1.0;
-        for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
-        term[(size_t)p] = v * prod;
-        if (blob) {
-          const int64_t d = pk.dest[(size_t)p];
-          put_element(bp.m, blob, d, -1, -inf, inf, v);
-          for (size_t i = 0; i < m; ++i) {
-            const Split& s = w.merged[i];
-            put_element(bp.m, blob, d + 1 + (int64_t)i, s.feature, s.lower, s.upper,
-                        s.zero_fraction);
-          }
-        }
-        ++p;
-      });
-    });
+    // bias: per-tree sums of the terms in path order, then per group
     std::vector<double> bsum((size_t)ens->num_groups, 0.0);
-    sum_bias(ens, tree_first.data(), term.data(), bsum.data());
+    for (int64_t t = 0; t < T; ++t) {
+      double acc = 0.0;
+      for (double x : trees[(size_t)t].term) acc = acc + x;
+      bsum[(size_t)ens->tree_group[t]] = bsum[(size_t)ens->tree_group[t]] + acc;
+    }
     if (bias)
       for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = bsum[(size_t)g];
+    char* blob = static_cast<char*>(host_blob);
     if (blob) {
       zero_padding(bp, blob);
-      rotate_bins(bp.m, blob, pk.bin_offsets.data());
+      // each bin's paths in placement order
+      const int64_t K = pk.K;
+      std::vector<int64_t> bin_first((size_t)K + 1, 0);
+      for (int64_t p = 0; p < P; ++p) ++bin_first[(size_t)pk.bin_of[(size_t)p] + 1];
+      for (int64_t b = 0; b < K; ++b) bin_first[(size_t)b + 1] += bin_first[(size_t)b];
+      std::vector<int64_t> bin_paths((size_t)P);
+      for (int64_t p = 0; p < P; ++p)
+        bin_paths[(size_t)(bin_first[(size_t)pk.bin_of[(size_t)p]] + pk.slot[(size_t)p])] = p;
+      std::atomic<int64_t> next{0};
+      Pool::get().run(host_threads(n), [&]() {
+        std::vector<uint64_t> used((size_t)ens->num_features, 0);
+        std::vector<int32_t> touched;
+        constexpr int64_t kChunk = 64;
+        for (;;) {
+          const int64_t b0 = next.fetch_add(kChunk);
+          if (b0 >= K) break;
+          const int64_t b1 = std::min(K, b0 + kChunk);
+          for (int64_t b = b0; b < b1; ++b) {
+            if (dtype == GTS_F64)
+              write_bin<double>(bp.m, blob, trees, path_tree.data(), tree_first.data(),
+                                bin_paths.data(), bin_first[(size_t)b], bin_first[(size_t)b + 1],
+                                pk.dest.data(), used, touched);
+            else
+              write_bin<float>(bp.m, blob, trees, path_tree.data(), tree_first.data(),
+                               bin_paths.data(), bin_first[(size_t)b], bin_first[(size_t)b + 1],
+                               pk.dest.data(), used, touched);
+          }
+        }
+      });
       write_bins_and_bias(bp, blob, pk.bin_offsets.data(), pk.bin_group.data(), bsum.data());
     }
     return GTS_OK;
