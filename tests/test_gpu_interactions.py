@@ -85,3 +85,17 @@ def test_full_size_workload(torch, orc):
     assert np.all(np.abs(row_sum - phi[..., :M]) <= bound)
     assert np.allclose(inter[..., M, M], phi[..., M], rtol=1e-6, atol=1e-7)
     assert np.all(inter[..., M, :M] == 0) and np.all(inter[..., :M, M] == 0)
+
+
+def test_large_row_count_interactions(torch, orc):
+    """2^16 rows (the rows sweep's largest interaction batch): sampled rows
+    against the conditioning oracle, every row's sums against gts_shap."""
+    w = synth.workload("interactions", rows=1)
+    X = synth.sweep_rows("interactions", 1 << 16)
+    say("large interaction batch", X.shape)
+    inter, phi = run(torch, w.ensemble, X, "f32", both=True)
+    sel = sample_rows(X.shape[0], k=6, seed=5)
+    assert_parity(inter[sel], orc.interactions(w.ensemble, X[sel]), "f32", 2, "2^16 rows")
+    err = np.abs(inter.sum(-1) - phi)
+    bound = sum_tolerance(np.abs(inter), "f32", 1) + 1e-3 * np.abs(phi) + 1e-5 * np.abs(phi).sum(-1, keepdims=True)
+    assert np.all(err <= bound), float((err / bound).max())

@@ -156,3 +156,20 @@ def test_full_size_workloads(torch, orc, name, dtype):
     # oracle's block magnitude estimated by the kernel's own output
     bound = sum_tolerance(np.abs(got), dtype)
     assert np.all(err <= bound), float((err / bound).max())
+
+
+@pytest.mark.parametrize("name,rows", [("covtype_med", 1 << 20), ("deep", 1 << 16)])
+def test_large_row_counts(torch, orc, name, rows):
+    """The largest batches the rows sweep times (2^20 rows of the
+    covtype-shaped model): sampled rows against Algorithm 1, every row against
+    Eq. 1."""
+    w = synth.workload(name, rows=1)
+    X = synth.sweep_rows(name, rows)
+    say("large batch", name, X.shape)
+    got = run_shap(torch, w.ensemble, X, "f32")
+    sel = np.unique(np.concatenate([sample_rows(rows, k=16, seed=3), [rows // 2, rows - 65]]))
+    assert_parity(got[sel], orc.treeshap(w.ensemble, X[sel]), "f32", what=f"{name} {rows} rows")
+    f = orc.predict(w.ensemble, X)
+    err = np.abs(got.sum(-1) - f)
+    bound = sum_tolerance(np.abs(got), "f32")
+    assert np.all(err <= bound), float((err / bound).max())

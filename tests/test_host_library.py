@@ -385,3 +385,16 @@ def test_extract_workspace_and_device_argument_checks():
              None) == gts.GTS_EINVAL
     assert f(ctypes.byref(s), None, 0, ctypes.byref(n), ctypes.byref(p), None, None, 0,
              None) == gts.GTS_EBUFSIZE
+
+
+def test_feature_count_beyond_the_lds_is_rejected():
+    """A phi row of M + 1 entries that cannot fit a 4-row tile in a
+    workgroup's LDS is refused with GTS_EINVAL before any launch."""
+    ens = synth.ensemble_from_lists([[(1, 2, 3, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 4.0, 1.0),
+                                      (-1, -1, -1, 0, 6.0, 2.0)]], M=200000)
+    desc, blob, bias = gts.prepare_blob(ens, "f32")
+    L = gts.lib()
+    vp = ctypes.c_void_p
+    for fn in (L.gts_shap, L.gts_shap_interactions):
+        assert fn(ctypes.byref(desc), vp(1), vp(1), 4, 200000, vp(1), None) == gts.GTS_EINVAL
+        assert "LDS" in gts.last_error() or "too large" in gts.last_error()
