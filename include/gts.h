@@ -98,13 +98,16 @@ typedef struct gts_path_element {
  * Device-ready model produced by gts_model_layout.  The fields describe the
  * byte blob the caller copies to the device; treat them as read-only.
  */
+#define GTS_MODEL_SORTED_BINS 1
+
 typedef struct gts_model {
   uint32_t magic;
   int32_t dtype;           /* gts_dtype of zero fractions, leaf values, phi */
   int32_t num_features;    /* M */
   int32_t num_groups;      /* G */
   int32_t max_path_len;    /* longest path, root included */
-  int32_t reserved0;
+  int32_t flags;           /* GTS_MODEL_SORTED_BINS: inside every bin, paths
+                              are in non-increasing length order (BFD, FFD) */
   int64_t num_elements;
   int64_t num_paths;
   int64_t num_bins;

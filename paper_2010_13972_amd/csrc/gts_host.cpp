@@ -716,6 +716,40 @@ BlobPlan plan_blob(int64_t n, int64_t P, int64_t K, int32_t M, int32_t G, int32_
   return bp;
 }
 
+// GTS_MODEL_SORTED_BINS if the paths of every bin, in their order in the
+// bin, never grow in length; from packed elements (roots have feature -1)
+// and bin offsets (unusable offsets give 0).
+int32_t sorted_bins_flag(const gts_path_element* packed, int64_t n, const int64_t* bin_offsets,
+                         int64_t K) {
+  if (packed == nullptr || bin_offsets == nullptr) return 0;
+  for (int64_t b = 0; b < K; ++b) {
+    int64_t a = bin_offsets[b];
+    const int64_t e = bin_offsets[b + 1];
+    if (a < 0 || e > n || e < a) return 0;
+    int64_t prev = INT64_MAX;
+    while (a < e) {
+      int64_t m = a + 1;
+      while (m < e && packed[m].feature_idx != -1) ++m;
+      if (m - a > prev) return 0;
+      prev = m - a;
+      a = m;
+    }
+  }
+  return GTS_MODEL_SORTED_BINS;
+}
+
+// The same from a packing: sizes[p] of every path, visited in placement
+// order.
+int32_t sorted_bins_flag(const Packing& pk, const int32_t* size) {
+  std::vector<int32_t> last((size_t)pk.K, INT32_MAX);
+  for (int64_t p : pk.order) {
+    int32_t& l = last[(size_t)pk.bin_of[(size_t)p]];
+    if (size[p] > l) return 0;
+    l = size[p];
+  }
+  return GTS_MODEL_SORTED_BINS;
+}
+
 // Zero the alignment padding after each array (the arrays themselves are
 // written in full), so equal models give byte-identical blobs.
 void zero_padding(const BlobPlan& bp, char* blob) {
@@ -938,7 +972,8 @@ extern "C" gts_status gts_model_layout(const gts_path_element* packed, int64_t n
       }
       if (last >= 0) maxlen = std::max<int32_t>(maxlen, (int32_t)std::min<int64_t>(num_elements - last, INT32_MAX));
     }
-    const BlobPlan bp = plan_blob(num_elements, P, num_bins, num_features, num_groups, dtype, maxlen);
+    BlobPlan bp = plan_blob(num_elements, P, num_bins, num_features, num_groups, dtype, maxlen);
+    bp.m.flags = sorted_bins_flag(packed, num_elements, bin_offsets, num_bins);
     if (host_blob == nullptr) {
       *model = bp.m;
       return GTS_OK;
@@ -1155,7 +1190,8 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     // pack on sizes only
     Packing pk;
     assign_bins(size.data(), group.data(), P, bin_capacity, alg, pk, true);
-    const BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
+    BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
+    bp.m.flags = sorted_bins_flag(pk, size.data());
     *model = bp.m;
     if (sizes_only) return GTS_OK;
     if (host_blob != nullptr && blob_capacity < bp.m.bytes)

@@ -97,6 +97,7 @@ struct Launch {
   int32_t sp;        // LDS row stride of the phi tile (elements)
   int32_t width;     // phi entries per (row, group): M+1 or (M+1)^2
   int32_t accumulate;  // 1: atomically add the tile to phi (phi pre-zeroed)
+  int32_t sorted;      // 1: inside a bin, paths never grow in length
 };
 
 // Shapley weight of a coalition of size k among the other n-1 players:
@@ -632,7 +633,7 @@ __device__ __forceinline__ int wave_max_small(int v) {
 // RW < 64: rounds of up to P = 64/RW paths, lane (j, r) = (path j, row r).
 template <typename T, int RW, bool INTER, bool EXCL>
 __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>& b, int lane,
-                                            const float* xrow, T* prow, int stride) {
+                                            const float* xrow, T* prow, int stride, bool sorted) {
   const int nroots = stage_bin(st, b, lane);
   if constexpr (RW == 64) {
     for (int t = 0; t < nroots; ++t) {
@@ -650,7 +651,9 @@ __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>&
       const int info = valid ? st->path[t] : 0;
       const int my_s = info & 0xff;
       const int my_q = info >> 8;
-      const int qmax = wave_max_small(my_q);
+      // the round's longest path: its first when the bin's paths never grow
+      const int qmax = sorted ? __builtin_amdgcn_readfirstlane(st->path[base]) >> 8
+                              : wave_max_small(my_q);
       if (qmax > 0) dispatch<T, false, INTER, kPaired, true>(qmax, st, my_s, my_q, xrow, prow, stride);
     }
   }
@@ -725,7 +728,8 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
       Bin<T> nxt;
       const int bn = bi + WAVES;
       if (bn < b_hi) nxt = load_bin(d, bn, lane);
-      process_bin<T, RW, INTER, PRIV && RW == 64>(stages + wave, cur, lane, xrow, prow, stride);
+      process_bin<T, RW, INTER, PRIV && RW == 64>(stages + wave, cur, lane, xrow, prow, stride,
+                                                  L.sorted != 0);
       cur = nxt;
     }
   }
@@ -821,6 +825,7 @@ gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64
   L.sp = sp;
   L.width = width;
   L.accumulate = splits > 1 ? 1 : 0;
+  L.sorted = (m->flags & GTS_MODEL_SORTED_BINS) ? 1 : 0;
   const int64_t total = rows * (int64_t)m->num_groups * width;
   if (L.accumulate) {
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 65536);

@@ -49,7 +49,7 @@ class ModelDesc(ctypes.Structure):
     """gts_model"""
     _fields_ = [("magic", ctypes.c_uint32), ("dtype", ctypes.c_int32),
                 ("num_features", ctypes.c_int32), ("num_groups", ctypes.c_int32),
-                ("max_path_len", ctypes.c_int32), ("reserved0", ctypes.c_int32),
+                ("max_path_len", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("num_elements", ctypes.c_int64), ("num_paths", ctypes.c_int64),
                 ("num_bins", ctypes.c_int64), ("bytes", ctypes.c_int64),
                 ("off", ctypes.c_int64 * 16)]

@@ -398,3 +398,25 @@ def test_feature_count_beyond_the_lds_is_rejected():
     for fn in (L.gts_shap, L.gts_shap_interactions):
         assert fn(ctypes.byref(desc), vp(1), vp(1), 4, 200000, vp(1), None) == gts.GTS_EINVAL
         assert "LDS" in gts.last_error() or "too large" in gts.last_error()
+
+
+@pytest.mark.parametrize("alg", ["bfd", "ffd", "nf", "none"])
+def test_sorted_bins_flag(alg):
+    """GTS_MODEL_SORTED_BINS is set exactly when every bin's paths never grow
+    in length (always for the decreasing heuristics)."""
+    for name in ("covtype_med", "random3"):
+        w = _workload(name)
+        el, _, bias = gts.extract_paths(w.ensemble)
+        packed, offs = gts.pack_paths(el, 64, alg)
+        roots = np.flatnonzero(packed["feature_idx"] == -1)
+        ends = np.append(roots[1:], len(packed))
+        sorted_ = True
+        for b in range(len(offs) - 1):
+            sizes = [e - a for a, e in zip(roots, ends) if offs[b] <= a < offs[b + 1]]
+            sorted_ &= all(x >= y for x, y in zip(sizes, sizes[1:]))
+        desc, blob = gts.model_layout(packed, offs, w.ensemble.num_features,
+                                      w.ensemble.num_groups, bias, "f32")
+        assert bool(desc.flags & 1) == sorted_, (name, alg)
+        if alg in ("bfd", "ffd", "none"):
+            assert sorted_
+        assert gts.prepare_blob(w.ensemble, "f32", alg=alg)[0].flags == desc.flags
