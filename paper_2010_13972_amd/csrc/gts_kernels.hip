@@ -246,17 +246,13 @@ __device__ __forceinline__ Bin<T> load_bin(const DevModel<T>& d, int bi, int lan
 // e + (number of even-length paths before its path).  The gap after every
 // path of even length makes the distance between consecutive path starts
 // odd, so lanes reading the k-th elements of up to 8 paths of equal length at
-// once hit different LDS banks; aux entries are 16 bytes so that an element's
-// head and aux share one address register.  Slot kSlots holds a neutral
+// once hit different LDS banks.  Slot kSlots holds a neutral
 // element (feature 0, range (-inf, +inf), z = 1, w = 0): a player present
 // and absent alike, which changes no other player's Shapley value.  A lane
 // whose path is shorter than the wave's longest reads it in place of the
 // elements past its path's end.  Without GAPPED (one path per wave, every
 // read a broadcast) element e sits in slot e.
-template <typename T> struct Aux;
-template <> struct alignas(16) Aux<float> {
-  float w, pad0, pad1, pad2;
-};
+template <typename T> struct Aux;   // fp64 models; fp32 models keep w alone
 template <> struct alignas(16) Aux<double> {
   double z, w;
 };
@@ -264,10 +260,7 @@ template <> struct alignas(16) Aux<double> {
 template <typename T, bool GAPPED>
 struct Stage {
   static constexpr int kSlots = GAPPED ? 96 : 64;   // 64 elements + a gap per even-length path
-#ifndef GTS_WIDE_AUX
-#define GTS_WIDE_AUX 0
-#endif
-  using AuxT = std::conditional_t<sizeof(T) == 4 && !(GAPPED && GTS_WIDE_AUX), float, Aux<T>>;
+  using AuxT = std::conditional_t<sizeof(T) == 4, float, Aux<T>>;
   int4 head[kSlots + 1];
   AuxT aux[kSlots + 1];
   int path[64];
@@ -871,19 +864,14 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
   int RW = 0;
   int waves = 8;
   bool priv = false;
-#ifndef GTS_PRIV_LDS_MAX
-#define GTS_PRIV_LDS_MAX (64 * 1024)
-#endif
-  if ((int64_t)need(64, 4, true) <= std::min<int64_t>(GTS_PRIV_LDS_MAX, dev.lds_per_block)) {
+  constexpr int64_t kSmallTile = 64 * 1024;  // leaves room for several workgroups per CU
+  if ((int64_t)need(64, 4, true) <= std::min<int64_t>(kSmallTile, dev.lds_per_block)) {
     RW = 64;
     waves = 4;
     priv = true;
   } else {
-#ifndef GTS_SHARED_LDS_MAX
-#define GTS_SHARED_LDS_MAX (64 * 1024)
-#endif
     for (int cand : {64, 32, 16, 8}) {
-      if ((int64_t)need(cand, 8, false) <= std::min<int64_t>(GTS_SHARED_LDS_MAX, dev.lds_per_block)) {
+      if ((int64_t)need(cand, 8, false) <= std::min<int64_t>(kSmallTile, dev.lds_per_block)) {
         RW = cand;
         break;
       }
