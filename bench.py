@@ -69,16 +69,16 @@ SUITE = [
 # Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
 # of the kernel source the counters were taken on.
 TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 18740683, "write_bytes": 35200000,
-        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
-    ("interactions", "f32", True): {"fetch_bytes": 13808800, "write_bytes": 127751885,
-        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
-    ("deep", "f32", False): {"fetch_bytes": 43063521, "write_bytes": 11520000,
-        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
-    ("deep", "f64", False): {"fetch_bytes": 56777524, "write_bytes": 17280000,
-        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
-    ("wide", "f32", False): {"fetch_bytes": 5961550399, "write_bytes": 316800086,
-        "source": "9407f8ca3538ac48f4d701fbc24379ee0bf8f4d748dc199ae58d2476fe8f7332"},
+    ("covtype_med", "f32", False): {"fetch_bytes": 18728808, "write_bytes": 35200000,
+        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
+    ("interactions", "f32", True): {"fetch_bytes": 13816619, "write_bytes": 126568724,
+        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
+    ("deep", "f32", False): {"fetch_bytes": 43053779, "write_bytes": 11520000,
+        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
+    ("deep", "f64", False): {"fetch_bytes": 56750886, "write_bytes": 17280000,
+        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
+    ("wide", "f32", False): {"fetch_bytes": 5938586531, "write_bytes": 316800106,
+        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
 }
 
 
