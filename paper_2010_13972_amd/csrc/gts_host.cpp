@@ -7,6 +7,7 @@
 #include <condition_variable>
 #include <mutex>
 #include <pthread.h>
+#include <sched.h>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -96,6 +97,13 @@ gts_status validate_ensemble(const gts_ensemble* e) {
 // time; a caller that finds the pool busy runs body() alone.  The pool is
 // never destroyed (its threads end with the process) and a forked child
 // starts a fresh one.
+//
+// A region is published as one atomic word (generation << 16 | workers
+// wanted).  Workers that have just finished a region poll that word for a
+// while (first with a pause instruction, then yielding the core) before they
+// block on the condition variable, so back-to-back regions -- a model
+// preparation runs two, a few hundred microseconds apart -- start without a
+// wake-up through the kernel; the caller polls the pending count the same way.
 class Pool {
  public:
   static Pool& get() {
@@ -112,30 +120,40 @@ class Pool {
       body();
       return;
     }
+    n = std::min(n, kMaxWorkers + 1);
     std::function<void()> fn(std::ref(body));
+    bool wake;
     {
-      std::unique_lock<std::mutex> lock(mu_);
+      std::lock_guard<std::mutex> lock(mu_);
       while ((int)workers_.size() < n - 1) {
         const int id = (int)workers_.size();
         workers_.emplace_back([this, id] { loop(id); });
         workers_.back().detach();
       }
       job_ = &fn;
-      want_ = n - 1;
-      pending_ = n - 1;
-      ++gen_;
+      pending_.store(n - 1, std::memory_order_relaxed);
+      gen_ += 1;
+      state_.store(gen_ << 16 | (uint64_t)(n - 1), std::memory_order_release);
+      wake = sleepers_ > 0;
     }
-    cv_.notify_all();
+    if (wake) cv_.notify_all();
     body();
-    {
-      std::unique_lock<std::mutex> lock(mu_);
-      done_.wait(lock, [this] { return pending_ == 0; });
-      job_ = nullptr;
-    }
+    for (int i = 0; pending_.load(std::memory_order_acquire) != 0; ++i) relax(i);
     run_mu_.unlock();
   }
 
  private:
+  static constexpr int kMaxWorkers = 63;
+  static constexpr int kPauseRounds = 2048;     // ~ tens of microseconds
+  static constexpr int kYieldRounds = 4096;     // then yield the core, ~ a millisecond
+
+  static void relax(int i) {
+    if (i < kPauseRounds)
+      __builtin_ia32_pause();
+    else
+      std::this_thread::yield();
+  }
+
   static Pool*& instance() {
     static Pool* p = nullptr;
     return p;
@@ -147,26 +165,36 @@ class Pool {
 
   void loop(int id) {
     uint64_t seen = 0;
-    std::unique_lock<std::mutex> lock(mu_);
     for (;;) {
-      cv_.wait(lock, [&] { return gen_ != seen; });
-      seen = gen_;
-      if (id >= want_) continue;
-      const std::function<void()>* fn = job_;
-      lock.unlock();
-      (*fn)();
-      lock.lock();
-      if (--pending_ == 0) done_.notify_one();
+      uint64_t s = state_.load(std::memory_order_acquire);
+      for (int i = 0; (s >> 16) == seen && i < kPauseRounds + kYieldRounds; ++i) {
+        relax(i);
+        s = state_.load(std::memory_order_acquire);
+      }
+      if ((s >> 16) == seen) {
+        std::unique_lock<std::mutex> lock(mu_);
+        ++sleepers_;
+        cv_.wait(lock, [&] { return (state_.load(std::memory_order_relaxed) >> 16) != seen; });
+        --sleepers_;
+        s = state_.load(std::memory_order_relaxed);
+      }
+      seen = s >> 16;
+      // the region of generation `seen` cannot end (nor job_ change) before
+      // every worker it wants, this one included, has counted down
+      if (id >= (int)(s & 0xffff)) continue;
+      (*job_)();
+      pending_.fetch_sub(1, std::memory_order_release);
     }
   }
 
   std::mutex run_mu_, mu_;
-  std::condition_variable cv_, done_;
+  std::condition_variable cv_;
   std::vector<std::thread> workers_;
   const std::function<void()>* job_ = nullptr;
-  uint64_t gen_ = 0;
-  int want_ = 0;
-  int pending_ = 0;
+  uint64_t gen_ = 0;                  // under mu_
+  int sleepers_ = 0;                  // under mu_
+  std::atomic<uint64_t> state_{0};    // gen_ << 16 | workers wanted
+  std::atomic<int> pending_{0};
 };
 
 // Per-thread state for walking trees depth first.  The merged elements of the
@@ -335,11 +363,24 @@ void sum_bias(const gts_ensemble* e, const int64_t* tree_paths, const double* te
   }
 }
 
+// Cores this process may run on (its affinity mask, which a container's CPU
+// share narrows; hardware_concurrency() counts every online core).
+int usable_cores() {
+  static const int n = [] {
+    cpu_set_t set;
+    CPU_ZERO(&set);
+    if (sched_getaffinity(0, sizeof(set), &set) == 0 && CPU_COUNT(&set) > 0)
+      return (int)CPU_COUNT(&set);
+    const unsigned hw = std::thread::hardware_concurrency();
+    return hw == 0 ? 1 : (int)hw;
+  }();
+  return n;
+}
+
 int host_threads(int64_t work) {
-  unsigned hw = std::thread::hardware_concurrency();
-  if (hw == 0) hw = 1;
+  const int64_t hw = usable_cores();
   const int64_t by_work = (work + 1023) / 1024;  // at least ~1k nodes (or elements) a thread
-  return (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)hw, 16, by_work}));
+  return (int)std::max<int64_t>(1, std::min<int64_t>({hw, 16, by_work}));
 }
 
 // Runs fn(t, walker) for every tree on the pool (dynamic chunks of trees);
@@ -873,14 +914,16 @@ void rotate_bins(const gts_model& m, char* blob, const int64_t* bin_offsets) {
   float* hi = reinterpret_cast<float*>(blob + m.off[kUpper]);
   const int64_t K = m.num_bins;
   std::atomic<int64_t> next{0};
-  Pool::get().run(host_threads(m.num_elements), [&]() {
+  const int nthreads = host_threads(m.num_elements);
+  // about eight chunks a thread, at most 64 bins each
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(64, K / (8 * nthreads)));
+  Pool::get().run(nthreads, [&]() {
     std::vector<uint64_t> used((size_t)m.num_features, 0);
     std::vector<int32_t> touched;
-    constexpr int64_t kChunk = 64;
     for (;;) {
-      const int64_t b0 = next.fetch_add(kChunk);
+      const int64_t b0 = next.fetch_add(chunk);
       if (b0 >= K) break;
-      const int64_t b1 = std::min(K, b0 + kChunk);
+      const int64_t b1 = std::min(K, b0 + chunk);
       for (int64_t b = b0; b < b1; ++b) {
         if (m.dtype == GTS_F64)
           rotate_bin(feat, lo, hi, reinterpret_cast<double*>(blob + m.off[kZero]), bin_offsets[b],
@@ -1031,7 +1074,9 @@ namespace {
 // One tree's paths from a single walk: merged feature elements of every path
 // (concatenated, ascending feature order), with each path's length (root
 // included), leaf value and bias term v * prod(z).
-struct TreeOut {
+// (aligned to keep the vector headers of trees that different threads fill
+// at the same time on different cache lines)
+struct alignas(128) TreeOut {
   std::vector<Split> el;
   std::vector<int64_t> first;  // per path: its first element in el
   std::vector<int32_t> size;
@@ -1044,6 +1089,15 @@ struct TreeOut {
     v.clear();
     term.clear();
   }
+};
+
+// Working arrays of gts_prepare_model, kept per calling thread between calls
+// so that repeated preparations reuse their memory.
+struct PrepareScratch {
+  std::vector<TreeOut> trees;
+  std::vector<int64_t> tree_first, path_tree, bin_first, bin_paths;
+  std::vector<int32_t> size, group;
+  Packing pk;
 };
 
 // Writes the paths of bin b into the blob, rotating each path's features as
@@ -1134,11 +1188,11 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     const int64_t T = ens->num_trees;
     const bool sizes_only = host_blob == nullptr && bias == nullptr;
     // one walk: every path's merged elements (only their count for a size
-    // query), per tree
-    // (kept per calling thread between calls; the pool's workers write into
-    // the caller's copy)
-    static thread_local std::vector<TreeOut> tls_trees;
-    std::vector<TreeOut>& trees = tls_trees;
+    // query), per tree; the pool's workers write into the calling thread's
+    // scratch
+    static thread_local PrepareScratch tls;
+    PrepareScratch& sc = tls;
+    std::vector<TreeOut>& trees = sc.trees;
     if ((int64_t)trees.size() < T) trees.resize((size_t)T);
     std::vector<gts_status> status;
     for_each_tree(ens, status, [&](int64_t t, Walker& w) {
@@ -1163,12 +1217,17 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
         Walker w;
         return w.walk<false>(ens, t, [](int32_t, size_t) {});
       }
-    std::vector<int64_t> tree_first((size_t)T + 1, 0);
+    std::vector<int64_t>& tree_first = sc.tree_first;
+    tree_first.assign((size_t)T + 1, 0);
     for (int64_t t = 0; t < T; ++t)
       tree_first[(size_t)t + 1] = tree_first[(size_t)t] + (int64_t)trees[(size_t)t].size.size();
     const int64_t P = tree_first[(size_t)T];
-    std::vector<int32_t> size((size_t)P), group((size_t)P);
-    std::vector<int64_t> path_tree((size_t)P);
+    std::vector<int32_t>& size = sc.size;
+    std::vector<int32_t>& group = sc.group;
+    std::vector<int64_t>& path_tree = sc.path_tree;
+    size.resize((size_t)P);
+    group.resize((size_t)P);
+    path_tree.resize((size_t)P);
     int64_t n = 0;
     int32_t maxlen = 0;
     for (int64_t t = 0; t < T; ++t) {
@@ -1188,7 +1247,7 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     if (n >= std::numeric_limits<int32_t>::max())
       return fail(GTS_EINVAL, "too many path elements for 32-bit device indices");
     // pack on sizes only
-    Packing pk;
+    Packing& pk = sc.pk;
     assign_bins(size.data(), group.data(), P, bin_capacity, alg, pk, true);
     BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
     bp.m.flags = sorted_bins_flag(pk, size.data());
@@ -1211,21 +1270,25 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       zero_padding(bp, blob);
       // each bin's paths in placement order
       const int64_t K = pk.K;
-      std::vector<int64_t> bin_first((size_t)K + 1, 0);
+      std::vector<int64_t>& bin_first = sc.bin_first;
+      bin_first.assign((size_t)K + 1, 0);
       for (int64_t p = 0; p < P; ++p) ++bin_first[(size_t)pk.bin_of[(size_t)p] + 1];
       for (int64_t b = 0; b < K; ++b) bin_first[(size_t)b + 1] += bin_first[(size_t)b];
-      std::vector<int64_t> bin_paths((size_t)P);
+      std::vector<int64_t>& bin_paths = sc.bin_paths;
+      bin_paths.resize((size_t)P);
       for (int64_t p = 0; p < P; ++p)
         bin_paths[(size_t)(bin_first[(size_t)pk.bin_of[(size_t)p]] + pk.slot[(size_t)p])] = p;
       std::atomic<int64_t> next{0};
-      Pool::get().run(host_threads(n), [&]() {
+      const int nthreads = host_threads(n);
+      // about eight chunks a thread, at most 64 bins each
+      const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(64, K / (8 * nthreads)));
+      Pool::get().run(nthreads, [&]() {
         std::vector<uint64_t> used((size_t)ens->num_features, 0);
         std::vector<int32_t> touched;
-        constexpr int64_t kChunk = 64;
         for (;;) {
-          const int64_t b0 = next.fetch_add(kChunk);
+          const int64_t b0 = next.fetch_add(chunk);
           if (b0 >= K) break;
-          const int64_t b1 = std::min(K, b0 + kChunk);
+          const int64_t b1 = std::min(K, b0 + chunk);
           for (int64_t b = b0; b < b1; ++b) {
             if (dtype == GTS_F64)
               write_bin<double>(bp.m, blob, trees, path_tree.data(), tree_first.data(),

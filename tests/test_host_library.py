@@ -347,6 +347,38 @@ def test_prepare_model_equals_the_three_step_route(name, dtype, alg):
         assert bias.tobytes() == bias2.tobytes()
 
 
+def test_prepare_model_from_concurrent_threads():
+    """Preparations from several threads at once (ctypes releases the GIL;
+    the worker pool serves one caller at a time and the others run alone,
+    each in its own scratch) give the blobs of one-at-a-time calls, also when
+    one thread alternates between models of different sizes."""
+    import threading
+    names = ["covtype_med", "wide", "random0", "tiny"]
+    ens = {n: _workload(n).ensemble for n in names}
+    want = {}
+    for n in names:
+        d, b, bias = gts.prepare_blob(ens[n], "f32")
+        want[n] = (bytes(d), b.tobytes(), bias.tobytes())
+    errors = []
+
+    def work(k):
+        try:
+            for r in range(6):
+                n = names[(k + r) % len(names)]
+                d, b, bias = gts.prepare_blob(ens[n], "f32")
+                if (bytes(d), b.tobytes(), bias.tobytes()) != want[n]:
+                    errors.append((k, r, n))
+        except Exception as e:  # pragma: no cover - reported below
+            errors.append((k, repr(e)))
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(6)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert errors == []
+
+
 def test_prepare_model_errors():
     w = synth.workload("deep")
     with pytest.raises(gts.GtsError) as e:           # depth-16 paths do not fit 8 lanes
