@@ -436,8 +436,8 @@ def experiment_rows(torch, gts, synth, oracle, workloads, cpu_limit_s):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="covtype_med",
                     choices=["tiny", "covtype_med", "deep", "wide", "interactions"],
                     help="the batch one step explains (interactions: the interaction kernel "

@@ -589,133 +589,188 @@ struct FirstFitTree {
   }
 };
 
-// The outcome of packing: bin of every path, the placement order, the first
-// element of every path in the packed sequence and the bins' element ranges.
+// Processing order of Section 3.3: by group; then (BFD, FFD) non-increasing
+// size; ties by position.  The sort key of a path is
+//   rank of its group among the groups present * nsize + (cap - size),
+// nsize = cap + 1 for BFD and FFD; for Next-Fit and one-path-per-bin the
+// size part is dropped (nsize = 1).
+inline bool size_decreasing(int32_t alg) { return alg == GTS_PACK_BFD || alg == GTS_PACK_FFD; }
+inline int64_t keys_per_group(int32_t cap, int32_t alg) {
+  return size_decreasing(alg) ? (int64_t)cap + 1 : 1;
+}
+inline int32_t sort_key(int32_t grank, int32_t size, int32_t cap, int32_t alg) {
+  return size_decreasing(alg) ? grank * (cap + 1) + (cap - size) : grank;
+}
+
+// The outcome of packing.  Per placement k (the k-th path in processing
+// order, order[k]): its bin, its element offset inside the bin and its rank
+// among the bin's paths.  Per bin: group, elements, paths.  The bins'
+// element ranges, and the bins' path ranges for a list of placements by bin.
 struct Packing {
-  std::vector<int64_t> order;        // paths in placement order
-  std::vector<int64_t> bin_of;       // per path
-  std::vector<int64_t> dest;         // per path: packed element offset
-  std::vector<int32_t> slot;         // per path: its position among its bin's paths
-  std::vector<int64_t> bin_offsets;  // [K+1]
+  std::vector<int64_t> order;        // [P] paths in processing order
+  std::vector<int64_t> bin_at;       // [P] per placement
+  std::vector<uint8_t> within_at;    // [P] per placement: element offset inside the bin
+  std::vector<uint8_t> slot_at;      // [P] per placement: rank among the bin's paths
+  std::vector<int32_t> bin_used;     // [K] elements in the bin
+  std::vector<int32_t> bin_paths;    // [K] paths in the bin
   std::vector<int32_t> bin_group;    // [K]
+  std::vector<int64_t> bin_offsets;  // [K+1] element ranges
+  std::vector<int64_t> bin_first;    // [K+1] path ranges
+  std::vector<int64_t> dest;         // [P] per path: packed element offset (assign_bins)
   int64_t K = 0;
+  bool sorted = true;                // every bin's sizes non-increasing in placement order
 };
 
-// Section 3.3 on paths given by size and group (path order = input order).
-// Processing order: by group; then (BFD, FFD) non-increasing size; ties by
-// position -- a counting sort over (group rank, size) keys.
+// Runs the heuristic over the placements in processing order.  key_start
+// [ng * nsize + 1]: first placement of every sort key.  The size of a
+// placement is the one its key encodes for BFD and FFD, size_at[k] for the
+// others.  group_of_rank[r]: the group id of rank r.  The loop reads no
+// per-path array for BFD and FFD and writes the per-placement outputs in
+// order.
+void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_rank,
+                 const int32_t* size_at, int64_t P, int32_t cap, int32_t alg, Packing& pk) {
+  pk.bin_at.resize((size_t)P);
+  pk.within_at.resize((size_t)P);
+  pk.slot_at.resize((size_t)P);
+  pk.bin_used.clear();
+  pk.bin_paths.clear();
+  pk.bin_group.clear();
+  pk.sorted = true;
+  int64_t* const bin_at = pk.bin_at.data();
+  uint8_t* const within_at = pk.within_at.data();
+  uint8_t* const slot_at = pk.slot_at.data();
+  int64_t K = 0;
+  auto open_bin = [&](int32_t g) {
+    pk.bin_used.push_back(0);
+    pk.bin_paths.push_back(0);
+    pk.bin_group.push_back(g);
+    return K++;
+  };
+  // placement k (size s) goes into bin b at element offset w
+  auto put = [&](int64_t k, int64_t b, int32_t w, int32_t s) {
+    bin_at[k] = b;
+    within_at[k] = (uint8_t)w;
+    slot_at[k] = (uint8_t)pk.bin_paths[(size_t)b]++;
+    pk.bin_used[(size_t)b] = w + s;
+  };
+  const int64_t nsize = keys_per_group(cap, alg);
+  std::vector<int32_t> resid;
+  static thread_local std::vector<BinHeap> by_resid;
+  by_resid.resize((size_t)cap + 1);
+  for (int32_t r = 0; r < ng; ++r) {
+    const int32_t g = group_of_rank[r];
+    const int64_t i = key_start[r * nsize], j = key_start[(r + 1) * nsize];
+    if (alg == GTS_PACK_BFD) {
+      // open bins by residual in [1, cap]: a min-heap of bin numbers each,
+      // and bit (residual - 1) of `open` set when that heap is not empty
+      for (BinHeap& h : by_resid) h.clear();
+      uint64_t open = 0;
+      for (int64_t kk = 0; kk < nsize; ++kk) {
+        const int32_t s = cap - (int32_t)kk;
+        for (int64_t k = key_start[r * nsize + kk]; k < key_start[r * nsize + kk + 1]; ++k) {
+          int64_t b;
+          int32_t res;
+          const uint64_t fit = s >= 1 ? open >> (s - 1) : open;
+          if (fit != 0) {
+            res = s + __builtin_ctzll(fit);
+            b = heap_pop(by_resid[(size_t)res]);
+            if (by_resid[(size_t)res].empty()) open &= ~(1ull << (res - 1));
+          } else {
+            b = open_bin(g);
+            res = cap;
+          }
+          const int32_t left = res - s;
+          if (left > 0) {
+            heap_push(by_resid[(size_t)left], b);
+            open |= 1ull << (left - 1);
+          }
+          put(k, b, cap - res, s);
+        }
+      }
+    } else if (alg == GTS_PACK_FFD) {
+      const int64_t first_bin = K;
+      FirstFitTree tree(j - i);
+      resid.assign((size_t)(j - i), 0);
+      for (int64_t kk = 0; kk < nsize; ++kk) {
+        const int32_t s = cap - (int32_t)kk;
+        for (int64_t k = key_start[r * nsize + kk]; k < key_start[r * nsize + kk + 1]; ++k) {
+          int64_t local = tree.leftmost_at_least(s);
+          if (local < 0) {
+            local = open_bin(g) - first_bin;
+            resid[(size_t)local] = cap;
+          }
+          const int32_t res = resid[(size_t)local];
+          resid[(size_t)local] = res - s;
+          tree.set(local, res - s);
+          put(k, first_bin + local, cap - res, s);
+        }
+      }
+    } else if (alg == GTS_PACK_NF) {
+      const int64_t first_bin = K;
+      int32_t res = 0, last = INT32_MAX;
+      for (int64_t k = i; k < j; ++k) {
+        const int32_t s = size_at[k];
+        if (K == first_bin || res < s) {
+          open_bin(g);
+          res = cap;
+          last = INT32_MAX;
+        }
+        if (s > last) pk.sorted = false;
+        last = s;
+        put(k, K - 1, cap - res, s);
+        res -= s;
+      }
+    } else {
+      for (int64_t k = i; k < j; ++k) put(k, open_bin(g), 0, size_at[k]);
+    }
+  }
+  pk.K = K;
+  pk.bin_offsets.resize((size_t)K + 1);
+  pk.bin_first.resize((size_t)K + 1);
+  pk.bin_offsets[0] = 0;
+  pk.bin_first[0] = 0;
+  for (int64_t b = 0; b < K; ++b) {
+    pk.bin_offsets[(size_t)b + 1] = pk.bin_offsets[(size_t)b] + pk.bin_used[(size_t)b];
+    pk.bin_first[(size_t)b + 1] = pk.bin_first[(size_t)b] + pk.bin_paths[(size_t)b];
+  }
+}
+
+// Section 3.3 on paths given by size and group (path order = input order):
+// the processing order by a counting sort over the keys above, the
+// heuristic, and (with layout) every path's packed element offset.
 void assign_bins(const int32_t* size, const int32_t* group, int64_t P, int32_t cap, int32_t alg,
                  Packing& pk, bool layout) {
-  const bool decreasing = (alg == GTS_PACK_BFD || alg == GTS_PACK_FFD);
   std::vector<int32_t> groups;
   groups.reserve(16);
   for (int64_t i = 0; i < P; ++i)
     if (groups.empty() || groups.back() != group[i]) groups.push_back(group[i]);
   std::sort(groups.begin(), groups.end());
   groups.erase(std::unique(groups.begin(), groups.end()), groups.end());
-  const int64_t nsize = decreasing ? (int64_t)cap + 1 : 1;
-  std::vector<int64_t> count(groups.size() * (size_t)nsize + 1, 0);
+  const int64_t nkeys = (int64_t)groups.size() * keys_per_group(cap, alg);
+  std::vector<int64_t> start((size_t)nkeys + 1, 0);
   std::vector<int32_t> key((size_t)P);
   for (int64_t i = 0; i < P; ++i) {
-    const int64_t g = std::lower_bound(groups.begin(), groups.end(), group[i]) - groups.begin();
-    key[(size_t)i] = (int32_t)(g * nsize + (decreasing ? cap - size[i] : 0));
-    ++count[(size_t)key[(size_t)i] + 1];
+    const int32_t g =
+        (int32_t)(std::lower_bound(groups.begin(), groups.end(), group[i]) - groups.begin());
+    key[(size_t)i] = sort_key(g, size[i], cap, alg);
+    ++start[(size_t)key[(size_t)i] + 1];
   }
-  for (size_t k = 1; k < count.size(); ++k) count[k] += count[k - 1];
-  std::vector<int64_t>& order = pk.order;
-  order.resize((size_t)P);
-  for (int64_t i = 0; i < P; ++i) order[(size_t)count[(size_t)key[(size_t)i]]++] = i;
-
-  std::vector<int64_t>& bin_of = pk.bin_of;
-  bin_of.resize((size_t)P);
-  std::vector<int32_t> resid;
-  std::vector<BinHeap> by_resid((size_t)cap + 1);
-  int64_t K = 0;
-  size_t i = 0;
-  while (i < order.size()) {
-    const int32_t g = group[order[i]];
-    size_t j = i;
-    while (j < order.size() && group[order[j]] == g) ++j;
-    const int64_t first_bin = K;
-    if (alg == GTS_PACK_BFD) {
-      // open bins by residual r in [1, cap]: a min-heap of bin numbers each,
-      // and bit r-1 of `open` set when that heap is not empty
-      for (BinHeap& h : by_resid) h.clear();
-      uint64_t open = 0;
-      for (size_t k = i; k < j; ++k) {
-        const int32_t s = size[order[k]];
-        int64_t b;
-        int32_t r;
-        const uint64_t fit = s >= 1 ? open >> (s - 1) : open;
-        if (fit != 0) {
-          r = s + __builtin_ctzll(fit);
-          b = heap_pop(by_resid[(size_t)r]);
-          if (by_resid[(size_t)r].empty()) open &= ~(1ull << (r - 1));
-        } else {
-          b = K++;
-          r = cap;
-        }
-        const int32_t left = r - s;
-        if (left > 0) {
-          heap_push(by_resid[(size_t)left], b);
-          open |= 1ull << (left - 1);
-        }
-        bin_of[(size_t)order[k]] = b;
-      }
-    } else if (alg == GTS_PACK_FFD) {
-      FirstFitTree tree((int64_t)(j - i));
-      int64_t opened = 0;
-      resid.assign((size_t)(j - i), 0);
-      for (size_t k = i; k < j; ++k) {
-        const int32_t s = size[order[k]];
-        int64_t local = tree.leftmost_at_least(s);
-        if (local < 0) {
-          local = opened++;
-          resid[(size_t)local] = cap;
-        }
-        resid[(size_t)local] -= s;
-        tree.set(local, resid[(size_t)local]);
-        bin_of[(size_t)order[k]] = first_bin + local;
-      }
-      K = first_bin + opened;
-    } else if (alg == GTS_PACK_NF) {
-      int32_t r = 0;
-      for (size_t k = i; k < j; ++k) {
-        const int32_t s = size[order[k]];
-        if (K == first_bin || r < s) {
-          ++K;
-          r = cap;
-        }
-        r -= s;
-        bin_of[(size_t)order[k]] = K - 1;
-      }
-    } else {
-      for (size_t k = i; k < j; ++k) bin_of[(size_t)order[k]] = K++;
-    }
-    i = j;
+  for (size_t k = 1; k < start.size(); ++k) start[k] += start[k - 1];
+  std::vector<int64_t> pos(start.begin(), start.end() - 1);
+  pk.order.resize((size_t)P);
+  std::vector<int32_t> size_at((size_t)P);
+  for (int64_t i = 0; i < P; ++i) {
+    const int64_t k = pos[(size_t)key[(size_t)i]]++;
+    pk.order[(size_t)k] = i;
+    size_at[(size_t)k] = size[i];
   }
-  pk.K = K;
+  place_paths(start.data(), (int32_t)groups.size(), groups.data(), size_at.data(), P, cap, alg,
+              pk);
   if (!layout) return;
-  // bins in order; inside a bin, paths in placement order
-  std::vector<int64_t>& off = pk.bin_offsets;
-  off.assign((size_t)K + 1, 0);
-  pk.bin_group.assign((size_t)K, 0);
-  for (int64_t p = 0; p < P; ++p) {
-    off[(size_t)bin_of[(size_t)p] + 1] += size[p];
-    pk.bin_group[(size_t)bin_of[(size_t)p]] = group[p];
-  }
-  for (int64_t b = 0; b < K; ++b) off[(size_t)b + 1] += off[(size_t)b];
-  std::vector<int64_t> cursor(off.begin(), off.end() - 1);
-  std::vector<int32_t> filled((size_t)K, 0);
   pk.dest.resize((size_t)P);
-  pk.slot.resize((size_t)P);
-  for (size_t k = 0; k < order.size(); ++k) {
-    const int64_t p = order[k];
-    const int64_t b = bin_of[(size_t)p];
-    pk.dest[(size_t)p] = cursor[(size_t)b];
-    pk.slot[(size_t)p] = filled[(size_t)b]++;
-    cursor[(size_t)b] += size[p];
-  }
+  for (int64_t k = 0; k < P; ++k)
+    pk.dest[(size_t)pk.order[(size_t)k]] =
+        pk.bin_offsets[(size_t)pk.bin_at[(size_t)k]] + pk.within_at[(size_t)k];
 }
 
 // ---------------------------------------------------------------------------
@@ -775,18 +830,6 @@ int32_t sorted_bins_flag(const gts_path_element* packed, int64_t n, const int64_
       prev = m - a;
       a = m;
     }
-  }
-  return GTS_MODEL_SORTED_BINS;
-}
-
-// The same from a packing: sizes[p] of every path, visited in placement
-// order.
-int32_t sorted_bins_flag(const Packing& pk, const int32_t* size) {
-  std::vector<int32_t> last((size_t)pk.K, INT32_MAX);
-  for (int64_t p : pk.order) {
-    int32_t& l = last[(size_t)pk.bin_of[(size_t)p]];
-    if (size[p] > l) return 0;
-    l = size[p];
   }
   return GTS_MODEL_SORTED_BINS;
 }
@@ -1073,7 +1116,7 @@ namespace {
 
 // One tree's paths from a single walk: merged feature elements of every path
 // (concatenated, ascending feature order), with each path's length (root
-// included), leaf value and bias term v * prod(z).
+// included) and leaf value, and the tree's part of the bias.
 // (aligned to keep the vector headers of trees that different threads fill
 // at the same time on different cache lines)
 struct alignas(128) TreeOut {
@@ -1081,13 +1124,17 @@ struct alignas(128) TreeOut {
   std::vector<int64_t> first;  // per path: its first element in el
   std::vector<int32_t> size;
   std::vector<double> v;
-  std::vector<double> term;
+  double term_sum = 0.0;       // the terms v * prod(z) summed in path order
+  int32_t max_size = 0;
+  int64_t elements = 0;        // sum of size
   void clear() {
     el.clear();
     first.clear();
     size.clear();
     v.clear();
-    term.clear();
+    term_sum = 0.0;
+    max_size = 0;
+    elements = 0;
   }
 };
 
@@ -1095,17 +1142,18 @@ struct alignas(128) TreeOut {
 // so that repeated preparations reuse their memory.
 struct PrepareScratch {
   std::vector<TreeOut> trees;
-  std::vector<int64_t> tree_first, path_tree, bin_first, bin_paths;
-  std::vector<int32_t> size, group;
+  std::vector<int64_t> tree_first, path_tree, chunk_start, key_start, by_bin;
+  std::vector<int32_t> size_at, key, grank, group_of_rank;
   Packing pk;
 };
 
 // Writes the paths of bin b into the blob, rotating each path's features as
 // rotate_bin does (same choices, taken from the feature-sorted source).
+// by_bin[bin_first[b] ..]: the placements of bin b in placement order.
 template <typename Z>
 void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees,
-               const int64_t* path_tree, const int64_t* tree_first, const int64_t* bin_paths,
-               int64_t p0, int64_t p1, const int64_t* dest, std::vector<uint64_t>& used,
+               const int64_t* path_tree, const int64_t* tree_first, const Packing& pk,
+               const int64_t* by_bin, int64_t b, std::vector<uint64_t>& used,
                std::vector<int32_t>& touched) {
   const float inf = std::numeric_limits<float>::infinity();
   int32_t* const feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]);
@@ -1114,14 +1162,16 @@ void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees
   Z* const zero = reinterpret_cast<Z*>(blob + m.off[kZero]);
   uint64_t* const u = used.data();
   int32_t t_in_bin = 0;
-  for (int64_t i = p0; i < p1; ++i, ++t_in_bin) {
-    const int64_t p = bin_paths[i];
+  const int64_t base = pk.bin_offsets[(size_t)b];
+  for (int64_t i = pk.bin_first[(size_t)b]; i < pk.bin_first[(size_t)b + 1]; ++i, ++t_in_bin) {
+    const int64_t k = by_bin[i];
+    const int64_t p = pk.order[(size_t)k];
     const int64_t t = path_tree[p];
     const TreeOut& tr = trees[(size_t)t];
     const size_t j = (size_t)(p - tree_first[t]);
     const Split* src = tr.el.data() + tr.first[j];
     const int32_t q = tr.size[j] - 1;
-    const int64_t d = dest[p];
+    const int64_t d = base + pk.within_at[(size_t)k];
     feat[d] = -1;
     lower[d] = -inf;
     upper[d] = inf;
@@ -1199,7 +1249,11 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       TreeOut& out = trees[(size_t)t];
       out.clear();
       if (sizes_only)
-        return w.walk<false>(ens, t, [&](int32_t, size_t m) { out.size.push_back((int32_t)m + 1); });
+        return w.walk<false>(ens, t, [&](int32_t, size_t m) {
+          out.size.push_back((int32_t)m + 1);
+          out.max_size = std::max(out.max_size, (int32_t)m + 1);
+          out.elements += (int64_t)m + 1;
+        });
       const int64_t base = ens->tree_node_offsets[t];
       return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
@@ -1209,7 +1263,9 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
         out.el.insert(out.el.end(), w.merged.begin(), w.merged.begin() + (std::ptrdiff_t)m);
         out.size.push_back((int32_t)m + 1);
         out.v.push_back(v);
-        out.term.push_back(v * prod);
+        out.term_sum = out.term_sum + v * prod;
+        out.max_size = std::max(out.max_size, (int32_t)m + 1);
+        out.elements += (int64_t)m + 1;
       });
     });
     for (int64_t t = 0; t < T; ++t)
@@ -1219,67 +1275,148 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       }
     std::vector<int64_t>& tree_first = sc.tree_first;
     tree_first.assign((size_t)T + 1, 0);
-    for (int64_t t = 0; t < T; ++t)
-      tree_first[(size_t)t + 1] = tree_first[(size_t)t] + (int64_t)trees[(size_t)t].size.size();
-    const int64_t P = tree_first[(size_t)T];
-    std::vector<int32_t>& size = sc.size;
-    std::vector<int32_t>& group = sc.group;
-    std::vector<int64_t>& path_tree = sc.path_tree;
-    size.resize((size_t)P);
-    group.resize((size_t)P);
-    path_tree.resize((size_t)P);
     int64_t n = 0;
     int32_t maxlen = 0;
     for (int64_t t = 0; t < T; ++t) {
-      const std::vector<int32_t>& sz = trees[(size_t)t].size;
-      for (size_t k = 0; k < sz.size(); ++k) {
-        const int64_t p = tree_first[(size_t)t] + (int64_t)k;
-        size[(size_t)p] = sz[k];
-        group[(size_t)p] = ens->tree_group[t];
-        path_tree[(size_t)p] = t;
-        n += sz[k];
-        maxlen = std::max(maxlen, sz[k]);
-      }
+      const TreeOut& tr = trees[(size_t)t];
+      tree_first[(size_t)t + 1] = tree_first[(size_t)t] + (int64_t)tr.size.size();
+      n += tr.elements;
+      maxlen = std::max(maxlen, tr.max_size);
     }
+    const int64_t P = tree_first[(size_t)T];
     if (maxlen > bin_capacity)
       return fail(GTS_EPATHLEN, "a merged path has length %d > bin capacity %d", maxlen,
                   bin_capacity);
     if (n >= std::numeric_limits<int32_t>::max())
       return fail(GTS_EINVAL, "too many path elements for 32-bit device indices");
-    // pack on sizes only
+
+    // processing order (a counting sort on the keys of sort_key), over
+    // chunks of consecutive trees on the pool: each chunk counts its keys,
+    // then places its paths after those of every smaller key and of the
+    // same key in earlier chunks -- the order of the serial sort
+    std::vector<int32_t>& grank = sc.grank;
+    std::vector<int32_t>& group_of_rank = sc.group_of_rank;
+    grank.assign((size_t)ens->num_groups, -1);
+    group_of_rank.clear();
+    for (int64_t t = 0; t < T; ++t) grank[(size_t)ens->tree_group[t]] = 0;
+    for (int32_t g = 0; g < ens->num_groups; ++g)
+      if (grank[(size_t)g] == 0) {
+        grank[(size_t)g] = (int32_t)group_of_rank.size();
+        group_of_rank.push_back(g);
+      }
+    const int32_t ng = (int32_t)group_of_rank.size();
+    const int64_t nkeys = (int64_t)ng * keys_per_group(bin_capacity, alg);
+    const int nthreads = host_threads(n);
+    const int64_t chunks = std::max<int64_t>(
+        1, std::min<int64_t>({T, 4 * (int64_t)nthreads, P / std::max<int64_t>(1, 4 * nkeys)}));
+    const bool need_size = !size_decreasing(alg);
+    std::vector<int32_t>& key = sc.key;
+    std::vector<int32_t>& size_at = sc.size_at;
+    std::vector<int64_t>& path_tree = sc.path_tree;
+    std::vector<int64_t>& start = sc.chunk_start;
+    std::vector<int64_t>& key_start = sc.key_start;
+    key.resize((size_t)P);
+    path_tree.resize((size_t)P);
+    if (need_size) size_at.resize((size_t)P);
+    start.assign((size_t)(chunks * nkeys), 0);
+    key_start.resize((size_t)nkeys + 1);
+    auto chunk_trees = [&](int64_t c, int64_t& t0, int64_t& t1) {
+      t0 = T * c / chunks;
+      t1 = T * (c + 1) / chunks;
+    };
+    const int sort_threads = (int)std::min<int64_t>(nthreads, chunks);
+    {
+      std::atomic<int64_t> next{0};
+      Pool::get().run(sort_threads, [&]() {
+        for (int64_t c; (c = next.fetch_add(1)) < chunks;) {
+          int64_t t0, t1;
+          chunk_trees(c, t0, t1);
+          int64_t* cnt = start.data() + c * nkeys;
+          for (int64_t t = t0; t < t1; ++t) {
+            const std::vector<int32_t>& sz = trees[(size_t)t].size;
+            const int32_t r = grank[(size_t)ens->tree_group[t]];
+            int64_t p = tree_first[(size_t)t];
+            for (size_t k = 0; k < sz.size(); ++k, ++p) {
+              path_tree[(size_t)p] = t;
+              const int32_t kk = sort_key(r, sz[k], bin_capacity, alg);
+              key[(size_t)p] = kk;
+              ++cnt[kk];
+            }
+          }
+        }
+      });
+    }
+    {
+      int64_t run = 0;
+      for (int64_t k = 0; k < nkeys; ++k) {
+        key_start[(size_t)k] = run;
+        for (int64_t c = 0; c < chunks; ++c) {
+          int64_t& x = start[(size_t)(c * nkeys + k)];
+          const int64_t cnt = x;
+          x = run;
+          run += cnt;
+        }
+      }
+      key_start[(size_t)nkeys] = run;
+    }
     Packing& pk = sc.pk;
-    assign_bins(size.data(), group.data(), P, bin_capacity, alg, pk, true);
+    pk.order.resize((size_t)P);
+    {
+      std::atomic<int64_t> next{0};
+      Pool::get().run(sort_threads, [&]() {
+        for (int64_t c; (c = next.fetch_add(1)) < chunks;) {
+          int64_t t0, t1;
+          chunk_trees(c, t0, t1);
+          int64_t* pos = start.data() + c * nkeys;
+          for (int64_t t = t0; t < t1; ++t) {
+            const std::vector<int32_t>& sz = trees[(size_t)t].size;
+            int64_t p = tree_first[(size_t)t];
+            for (size_t j = 0; j < sz.size(); ++j, ++p) {
+              const int64_t k = pos[key[(size_t)p]]++;
+              pk.order[(size_t)k] = p;
+              if (need_size) size_at[(size_t)k] = sz[j];
+            }
+          }
+        }
+      });
+    }
+    place_paths(key_start.data(), ng, group_of_rank.data(), need_size ? size_at.data() : nullptr,
+                P, bin_capacity, alg, pk);
     BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
-    bp.m.flags = sorted_bins_flag(pk, size.data());
+    bp.m.flags = pk.sorted ? GTS_MODEL_SORTED_BINS : 0;
     *model = bp.m;
     if (sizes_only) return GTS_OK;
     if (host_blob != nullptr && blob_capacity < bp.m.bytes)
       return fail(GTS_EBUFSIZE, "blob_capacity %lld < %lld bytes", (long long)blob_capacity,
                   (long long)bp.m.bytes);
-    // bias: per-tree sums of the terms in path order, then per group
+    // bias: per-tree sums of the terms in path order, then per group in tree
+    // order
     std::vector<double> bsum((size_t)ens->num_groups, 0.0);
-    for (int64_t t = 0; t < T; ++t) {
-      double acc = 0.0;
-      for (double x : trees[(size_t)t].term) acc = acc + x;
-      bsum[(size_t)ens->tree_group[t]] = bsum[(size_t)ens->tree_group[t]] + acc;
-    }
+    for (int64_t t = 0; t < T; ++t)
+      bsum[(size_t)ens->tree_group[t]] = bsum[(size_t)ens->tree_group[t]] +
+                                         trees[(size_t)t].term_sum;
     if (bias)
       for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = bsum[(size_t)g];
     char* blob = static_cast<char*>(host_blob);
     if (blob) {
       zero_padding(bp, blob);
-      // each bin's paths in placement order
       const int64_t K = pk.K;
-      std::vector<int64_t>& bin_first = sc.bin_first;
-      bin_first.assign((size_t)K + 1, 0);
-      for (int64_t p = 0; p < P; ++p) ++bin_first[(size_t)pk.bin_of[(size_t)p] + 1];
-      for (int64_t b = 0; b < K; ++b) bin_first[(size_t)b + 1] += bin_first[(size_t)b];
-      std::vector<int64_t>& bin_paths = sc.bin_paths;
-      bin_paths.resize((size_t)P);
-      for (int64_t p = 0; p < P; ++p)
-        bin_paths[(size_t)(bin_first[(size_t)pk.bin_of[(size_t)p]] + pk.slot[(size_t)p])] = p;
+      // each bin's placements in placement order
+      std::vector<int64_t>& by_bin = sc.by_bin;
+      by_bin.resize((size_t)P);
+      {
+        std::atomic<int64_t> next{0};
+        const int64_t step = std::max<int64_t>(4096, P / (4 * nthreads) + 1);
+        Pool::get().run(nthreads, [&]() {
+          for (int64_t k0; (k0 = next.fetch_add(step)) < P;) {
+            const int64_t k1 = std::min(P, k0 + step);
+            for (int64_t k = k0; k < k1; ++k)
+              by_bin[(size_t)(pk.bin_first[(size_t)pk.bin_at[(size_t)k]] + pk.slot_at[(size_t)k])] =
+                  k;
+          }
+        });
+      }
       std::atomic<int64_t> next{0};
-      const int nthreads = host_threads(n);
       // about eight chunks a thread, at most 64 bins each
       const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(64, K / (8 * nthreads)));
       Pool::get().run(nthreads, [&]() {
@@ -1291,13 +1428,11 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
           const int64_t b1 = std::min(K, b0 + chunk);
           for (int64_t b = b0; b < b1; ++b) {
             if (dtype == GTS_F64)
-              write_bin<double>(bp.m, blob, trees, path_tree.data(), tree_first.data(),
-                                bin_paths.data(), bin_first[(size_t)b], bin_first[(size_t)b + 1],
-                                pk.dest.data(), used, touched);
+              write_bin<double>(bp.m, blob, trees, path_tree.data(), tree_first.data(), pk,
+                                by_bin.data(), b, used, touched);
             else
-              write_bin<float>(bp.m, blob, trees, path_tree.data(), tree_first.data(),
-                               bin_paths.data(), bin_first[(size_t)b], bin_first[(size_t)b + 1],
-                               pk.dest.data(), used, touched);
+              write_bin<float>(bp.m, blob, trees, path_tree.data(), tree_first.data(), pk,
+                               by_bin.data(), b, used, touched);
           }
         }
       });
