@@ -69,15 +69,15 @@ SUITE = [
 # Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
 # of the kernel source the counters were taken on.
 TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 18728808, "write_bytes": 35200000,
+    ("covtype_med", "f32", False): {"fetch_bytes": 18729325, "write_bytes": 35200000,
         "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("interactions", "f32", True): {"fetch_bytes": 13816619, "write_bytes": 126568724,
+    ("interactions", "f32", True): {"fetch_bytes": 13814513, "write_bytes": 126538132,
         "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("deep", "f32", False): {"fetch_bytes": 43053779, "write_bytes": 11520000,
+    ("deep", "f32", False): {"fetch_bytes": 43053437, "write_bytes": 11520000,
         "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("deep", "f64", False): {"fetch_bytes": 56750886, "write_bytes": 17280000,
+    ("deep", "f64", False): {"fetch_bytes": 56754384, "write_bytes": 17280000,
         "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("wide", "f32", False): {"fetch_bytes": 5938586531, "write_bytes": 316800106,
+    ("wide", "f32", False): {"fetch_bytes": 5896037931, "write_bytes": 316800106,
         "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
 }
 
