@@ -205,7 +205,10 @@ class Pool {
 struct Walker {
   struct Frame {
     int32_t node;
-    int32_t stage;  // 0: not entered yet, 1: in its left subtree, 2: in its right subtree
+    int32_t depth;    // undo depth of the parent's path
+    int32_t feature;  // the split into this node (-1 at the root)
+    float lo, hi;
+    double ratio;
   };
   struct Undo {
     int32_t feature;
@@ -279,70 +282,62 @@ struct Walker {
   // Depth-first walk of tree t, left child (x < t) first, validating every
   // node it reaches.  Calls leaf(node, m) with m merged elements; with EMIT
   // they are in merged[0..m), in ascending feature order (without EMIT only
-  // m is computed).
+  // m is computed).  The stack holds nodes still to visit, each with the
+  // split that leads to it and the undo depth of its parent's path: a visit
+  // first unwinds the path to that depth, then enters the split.
   template <bool EMIT, typename LeafFn>
   gts_status walk(const gts_ensemble* e, int64_t t, LeafFn&& leaf) {
     const int64_t base = e->tree_node_offsets[t];
     const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
     reset(e->num_features);
     seen.assign((size_t)n, 0);
-    stack.push_back(Frame{0, 0});
     const float inf = std::numeric_limits<float>::infinity();
+    stack.push_back(Frame{0, 0, -1, 0.0f, 0.0f, 0.0});
     while (!stack.empty()) {
-      Frame& fr = stack.back();
+      const Frame fr = stack.back();
+      stack.pop_back();
+      while ((int32_t)undo.size() > fr.depth) pop<EMIT>();
+      if (fr.feature >= 0) push<EMIT>(fr.feature, fr.lo, fr.hi, fr.ratio);
       const int32_t node = fr.node;
       const int64_t gi = base + node;
-      if (fr.stage == 0) {
-        if (seen[(size_t)node])
-          return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
-                      (long long)t, node);
-        seen[(size_t)node] = 1;
-        const double r = e->cover[gi];
-        if (!(r >= 0.0) || !std::isfinite(r))
-          return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
-                      (long long)t, node);
-        const int32_t a = e->left[gi], b = e->right[gi];
-        if (a < 0 && b < 0) {
-          if (!std::isfinite(e->value[gi]))
-            return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t,
-                        node);
-          const size_t m = active.size();
-          if (EMIT) {
-            merged.resize(m);
-            for (size_t i = 0; i < m; ++i) {
-              const size_t f = (size_t)active[i];
-              merged[i] = Split{active[i], lower[f], upper[f], zf[f]};
-            }
+      if (seen[(size_t)node])
+        return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
+                    (long long)t, node);
+      seen[(size_t)node] = 1;
+      const double r = e->cover[gi];
+      if (!(r >= 0.0) || !std::isfinite(r))
+        return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
+                    (long long)t, node);
+      const int32_t a = e->left[gi], b = e->right[gi];
+      if (a < 0 && b < 0) {
+        if (!std::isfinite(e->value[gi]))
+          return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
+        const size_t m = active.size();
+        if (EMIT) {
+          merged.resize(m);
+          for (size_t i = 0; i < m; ++i) {
+            const size_t f = (size_t)active[i];
+            merged[i] = Split{active[i], lower[f], upper[f], zf[f]};
           }
-          stack.pop_back();
-          leaf(node, m);
-          continue;
         }
-        if (a < 0 || b < 0 || a >= n || b >= n)
-          return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
-                      node);
-        const int32_t d = e->feature[gi];
-        if (d < 0 || d >= e->num_features)
-          return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)",
-                      (long long)t, node, d, e->num_features);
-        const float th = e->threshold[gi];
-        if (std::isnan(th))
-          return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
-        fr.stage = 1;
-        push<EMIT>(d, -inf, th, EMIT ? cover_ratio(e->cover[base + a], r) : 0.0);
-        stack.push_back(Frame{a, 0});
-      } else if (fr.stage == 1) {
-        pop<EMIT>();
-        fr.stage = 2;
-        const int32_t b = e->right[gi];
-        push<EMIT>(e->feature[gi], e->threshold[gi], inf,
-                   EMIT ? cover_ratio(e->cover[base + b], e->cover[gi]) : 0.0);
-        stack.push_back(Frame{b, 0});
-      } else {
-        pop<EMIT>();
-        stack.pop_back();
+        leaf(node, m);
+        continue;
       }
+      if (a < 0 || b < 0 || a >= n || b >= n)
+        return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
+                    node);
+      const int32_t d = e->feature[gi];
+      if (d < 0 || d >= e->num_features)
+        return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)",
+                    (long long)t, node, d, e->num_features);
+      const float th = e->threshold[gi];
+      if (std::isnan(th))
+        return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
+      const int32_t depth = (int32_t)undo.size();
+      stack.push_back(Frame{b, depth, d, th, inf, EMIT ? cover_ratio(e->cover[base + b], r) : 0.0});
+      stack.push_back(Frame{a, depth, d, -inf, th, EMIT ? cover_ratio(e->cover[base + a], r) : 0.0});
     }
+    while (!undo.empty()) pop<EMIT>();
     clean = true;
     return GTS_OK;
   }
