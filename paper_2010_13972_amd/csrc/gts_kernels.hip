@@ -897,19 +897,30 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
   }
   if (RW == 0) return fail(GTS_EINVAL, "M = %d needs more LDS than a workgroup has", M);
   const size_t lds = need(RW, waves, priv);
-  // enough workgroups for two rounds of every CU at the occupancy the LDS
-  // allows; (group, slice) units a multiple of the 8 XCDs when split
+  // Bin slices per (row tile, group) when there are too few tiles to fill
+  // the GPU.  Every slice adds its tile to phi atomically, so a slice costs
+  // rows x width atomic adds.  SHAP values (short phi rows): enough
+  // workgroups for two rounds of every CU at the occupancy the LDS allows,
+  // (group, slice) units a multiple of the 8 XCDs; the extra workgroups
+  // balance the load.  Interaction values ((M+1)^2 per row): at most one
+  // round, since there the adds outweigh the balance.
   const int64_t tiles = (rows + RW - 1) / RW;
   const int64_t base = tiles * G;
   const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, dev.lds_per_cu / (int64_t)lds));
-  const int64_t target = 2 * per_cu * dev.cus;
   const int64_t bins_per_group = std::max<int64_t>(1, m->num_bins / G);
   int splits = 1;
-  if (base < target) {
-    int64_t want = (target + base - 1) / base;
-    const int64_t step = 8 / std::gcd(G, 8);
-    want = (want + step - 1) / step * step;
-    splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
+  if constexpr (INTER) {
+    const int64_t round = per_cu * dev.cus;
+    if (2 * base <= round)
+      splits = (int)std::max<int64_t>(1, std::min<int64_t>(round / base, bins_per_group));
+  } else {
+    const int64_t target = 2 * per_cu * dev.cus;
+    if (base < target) {
+      int64_t want = (target + base - 1) / base;
+      const int64_t step = 8 / std::gcd(G, 8);
+      want = (want + step - 1) / step * step;
+      splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
+    }
   }
 #define GTS_LAUNCH(rw, w)                                                                 \
   return launch_rw<T, rw, INTER, w, false>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, \
