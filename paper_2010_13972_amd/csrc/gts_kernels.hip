@@ -901,9 +901,10 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
   // the GPU.  Every slice adds its tile to phi atomically, so a slice costs
   // rows x width atomic adds.  SHAP values (short phi rows): enough
   // workgroups for two rounds of every CU at the occupancy the LDS allows,
-  // (group, slice) units a multiple of the 8 XCDs; the extra workgroups
-  // balance the load.  Interaction values ((M+1)^2 per row): at most one
-  // round, since there the adds outweigh the balance.
+  // or more, up to 128 slices, while every wave still gets 8 bins or more
+  // (finer slices even out the last rounds); (group, slice) units a multiple
+  // of the 8 XCDs.  Interaction values ((M+1)^2 per row): at most one round,
+  // since there the adds outweigh the balance.
   const int64_t tiles = (rows + RW - 1) / RW;
   const int64_t base = tiles * G;
   const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, dev.lds_per_cu / (int64_t)lds));
@@ -919,6 +920,8 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
       int64_t want = (target + base - 1) / base;
       const int64_t step = 8 / std::gcd(G, 8);
       want = (want + step - 1) / step * step;
+      const int64_t fine = std::min<int64_t>(128, bins_per_group / (8 * waves)) / step * step;
+      want = std::max(want, fine);
       splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
     }
   }
