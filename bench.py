@@ -69,16 +69,16 @@ SUITE = [
 # Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
 # of the kernel source the counters were taken on.
 TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 18729325, "write_bytes": 35200000,
-        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("interactions", "f32", True): {"fetch_bytes": 13814513, "write_bytes": 126538132,
-        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("deep", "f32", False): {"fetch_bytes": 43053437, "write_bytes": 11520000,
-        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("deep", "f64", False): {"fetch_bytes": 56754384, "write_bytes": 17280000,
-        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
-    ("wide", "f32", False): {"fetch_bytes": 5896037931, "write_bytes": 316800106,
-        "source": "44531f682e008fdac2fb02f9712ba53c6b54cb49155f698ac4866bde12549079"},
+    ("covtype_med", "f32", False): {"fetch_bytes": 18728829, "write_bytes": 35200000,
+        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
+    ("interactions", "f32", True): {"fetch_bytes": 16043622, "write_bytes": 46142754,
+        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
+    ("deep", "f32", False): {"fetch_bytes": 43108669, "write_bytes": 46080000,
+        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
+    ("deep", "f64", False): {"fetch_bytes": 53145216, "write_bytes": 92160000,
+        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
+    ("wide", "f32", False): {"fetch_bytes": 5909935492, "write_bytes": 316800108,
+        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
 }
 
 
