@@ -36,13 +36,15 @@ def assert_parity(got, want, dtype: str, block_axes: int = 1, what: str = ""):
     err = np.abs(got - want)
     tol = tolerance(want, dtype, block_axes)
     bad = err > tol
+    # err / tol, where a zero tolerance (an all-zero fp32 block) allows no error
+    ratio = np.divide(err, tol, out=np.where(err > 0, np.inf, 0.0), where=tol > 0)
     if bad.any():
         idx = np.argwhere(bad)[:5]
         detail = ", ".join(f"{tuple(i)}: got {got[tuple(i)]:.9g} want {want[tuple(i)]:.9g}"
                            for i in idx)
         raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} outside tolerance "
-                             f"(max err/tol {float((err / tol).max()):.3g}); {detail}")
-    return float((err / tol).max())
+                             f"(max err/tol {float(ratio.max()):.3g}); {detail}")
+    return float(ratio.max()) if ratio.size else 0.0
 
 
 def sum_tolerance(want_block: np.ndarray, dtype: str, block_axes: int = 1) -> np.ndarray:

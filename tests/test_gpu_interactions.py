@@ -11,7 +11,7 @@ import pytest
 
 from paper_2010_13972_amd import gts, synth
 from parity import assert_parity, sum_tolerance
-from test_gpu_shap import chain_tree, sample_rows, say
+from test_gpu_shap import chain_tree, empty_ensemble, sample_rows, say
 
 pytestmark = pytest.mark.gpu
 
@@ -99,3 +99,22 @@ def test_large_row_count_interactions(torch, orc):
     err = np.abs(inter.sum(-1) - phi)
     bound = sum_tolerance(np.abs(inter), "f32", 1) + 1e-3 * np.abs(phi) + 1e-5 * np.abs(phi).sum(-1, keepdims=True)
     assert np.all(err <= bound), float((err / bound).max())
+
+
+def test_empty_model_and_unfed_groups(torch, orc):
+    """No trees, and an output group that no tree feeds: the interaction
+    tile is exactly 0 there; the fed groups match the conditioning route."""
+    X = np.random.default_rng(2).uniform(0, 1, size=(40, 3)).astype(np.float32)
+    for dtype in ("f64", "f32"):
+        say("interactions empty model", dtype)
+        got = run(torch, empty_ensemble(3, 2), X, dtype)
+        assert got.shape == (40, 2, 4, 4) and np.all(got == 0.0)
+    stump = [(1, 2, 1, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 3.0, -1.0), (-1, -1, -1, 0, 7.0, 4.0)]
+    two = [(1, 2, 0, 0.25, 8.0, 0.0), (3, 4, 2, 0.5, 2.0, 0.0), (-1, -1, -1, 0, 6.0, -0.5),
+           (-1, -1, -1, 0, 1.0, 1.5), (-1, -1, -1, 0, 1.0, 0.5)]
+    ens = synth.ensemble_from_lists([stump, two], M=3, num_groups=3, tree_group=[2, 0])
+    for dtype in ("f64", "f32"):
+        say("interactions unfed group", dtype)
+        got = run(torch, ens, X, dtype)
+        assert_parity(got, orc.interactions(ens, X), dtype, 2, "unfed group")
+        assert np.all(got[:, 1] == 0.0)

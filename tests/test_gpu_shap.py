@@ -126,6 +126,35 @@ def test_special_models(torch, orc):
         assert np.all(got[:, 0, 2] == 0.0)  # feature 2 never used
 
 
+def empty_ensemble(M, G):
+    return synth.Ensemble(
+        num_features=M, num_groups=G, tree_node_offsets=np.zeros(1, np.int64),
+        tree_group=np.zeros(0, np.int32), left=np.zeros(0, np.int32),
+        right=np.zeros(0, np.int32), feature=np.zeros(0, np.int32),
+        threshold=np.zeros(0, np.float32), cover=np.zeros(0), value=np.zeros(0))
+
+
+def test_empty_model_and_unfed_groups(torch, orc):
+    """A model without trees, and a model whose middle output group no tree
+    feeds: phi is exactly 0 there (no path, bias 0); the fed groups match
+    Algorithm 1."""
+    X = np.random.default_rng(1).uniform(0, 1, size=(70, 3)).astype(np.float32)
+    for dtype in ("f64", "f32"):
+        say("empty model", dtype)
+        got = run_shap(torch, empty_ensemble(3, 2), X, dtype)
+        assert got.shape == (70, 2, 4) and np.all(got == 0.0)
+    stump = [(1, 2, 1, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 3.0, -1.0), (-1, -1, -1, 0, 7.0, 4.0)]
+    stump0 = [(1, 2, 0, 0.25, 8.0, 0.0), (-1, -1, -1, 0, 2.0, 1.5), (-1, -1, -1, 0, 6.0, -0.5)]
+    leaf = [(-1, -1, -1, 0.0, 10.0, 2.5)]
+    ens = synth.ensemble_from_lists([stump, leaf, stump0], M=3, num_groups=3,
+                                    tree_group=[0, 2, 0])
+    for dtype in ("f64", "f32"):
+        say("unfed group", dtype)
+        got = run_shap(torch, ens, X, dtype)
+        assert_parity(got, orc.treeshap(ens, X), dtype, what="unfed group")
+        assert np.all(got[:, 1, :] == 0.0)
+
+
 # --------------------------------------------------------------------------
 # full-size workloads: sampled rows against Algorithm 1, all rows against Eq. 1
 # --------------------------------------------------------------------------
