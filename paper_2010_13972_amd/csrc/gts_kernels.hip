@@ -14,7 +14,7 @@
 // RW == 64 all lanes share one path and read its elements from the staging
 // area at the same address (an LDS broadcast); with fewer rows per wave each
 // group of RW lanes reads its own path's elements.  Trip counts are
-// compile-time constants (one variant per path length up to 16 features, 8
+// compile-time constants (one variant per path length up to 12 features, 8
 // for interactions), so a wave never diverges on path length.  This does the
 // q^2 work of a path once per row instead of spreading it over q lanes that
 // then need q shuffles each.
