@@ -11,6 +11,7 @@
  *   gts_prepare_model   host   the three steps above in one pass
  *   gts_shap            device SHAP values              phi[rows][G][M+1]
  *   gts_shap_interactions device SHAP interaction values phi[rows][G][M+1][M+1]
+ *   gts_launch_config   host   the launch shape the two calls above choose
  *
  * Conventions shared by every call:
  *   - All memory is owned by the caller.  The library allocates nothing on the
@@ -289,6 +290,38 @@ gts_status gts_shap(const gts_model *model, const void *d_model,
 gts_status gts_shap_interactions(const gts_model *model, const void *d_model,
                                  const float *d_X, int64_t rows, int64_t ld_x,
                                  void *d_phi, void *stream);
+
+/*
+ * gts_launch_config -- the launch that gts_shap (interactions == 0) or
+ * gts_shap_interactions (interactions != 0) makes for this model and row
+ * count on the calling thread's current device, without launching anything.
+ * For tuning and tests.  The decomposition it reports is the work split of
+ * Sections 3.3-3.4: bins of paths as work units, a tile of rows per
+ * workgroup.
+ *
+ * rows_per_tile  rows of a workgroup's phi tile (64, 32, 16, 8 or 4); below
+ *                64, a wave runs 64 / rows_per_tile paths at once
+ * waves          waves (64 lanes) per workgroup
+ * private_tiles  1 if every wave has a phi tile of its own (no LDS atomics)
+ * slices         bin slices per (row tile, output group); above 1 the
+ *                slices add their tiles to phi atomically after a clearing
+ *                pass
+ * workgroups     grid size (0 for rows == 0)
+ * lds_bytes      LDS per workgroup
+ * Errors: GTS_EINVAL as gts_shap, for out == NULL, or when a phi row does
+ * not fit in a workgroup's LDS; GTS_EDEVICE without a HIP device.
+ */
+typedef struct gts_launch {
+  int32_t rows_per_tile;
+  int32_t waves;
+  int32_t private_tiles;
+  int32_t slices;
+  int64_t workgroups;
+  int64_t lds_bytes;
+} gts_launch;
+
+gts_status gts_launch_config(const gts_model *model, int64_t rows, int32_t interactions,
+                             gts_launch *out);
 
 /* Message describing the calling thread's most recent failure ("" if none). */
 const char *gts_last_error(void);

@@ -838,10 +838,20 @@ gts_status launch_rw(const gts_model* m, const void* blob, const float* X, int64
   return GTS_OK;
 }
 
+// The launch shape of a model and row count: rows per tile, waves, private
+// tiles, LDS strides and bytes, and bin slices.
+struct Plan {
+  int RW = 0;
+  int waves = 8;
+  bool priv = false;
+  int32_t sx = 0, sp = 0, width = 0;
+  size_t lds = 0;
+  int splits = 1;
+  int64_t tiles = 0;
+};
+
 template <typename T, bool INTER>
-gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t rows, int64_t ld,
-                  void* phi, hipStream_t stream) {
-  const DeviceInfo dev = device_info();
+gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, Plan& plan) {
   const int M = m->num_features;
   const int G = m->num_groups;
   const int64_t width64 = INTER ? (int64_t)(M + 1) * (M + 1) : (int64_t)(M + 1);
@@ -925,10 +935,31 @@ gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t 
       splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
     }
   }
+  plan.RW = RW;
+  plan.waves = waves;
+  plan.priv = priv;
+  plan.sx = sx;
+  plan.sp = sp;
+  plan.width = width;
+  plan.lds = lds;
+  plan.splits = splits;
+  plan.tiles = tiles;
+  return GTS_OK;
+}
+
+template <typename T, bool INTER>
+gts_status launch(const gts_model* m, const void* blob, const float* X, int64_t rows, int64_t ld,
+                  void* phi, hipStream_t stream) {
+  Plan plan;
+  const gts_status st = plan_launch<T, INTER>(m, rows, device_info(), plan);
+  if (st != GTS_OK) return st;
+  const int RW = plan.RW, waves = plan.waves, splits = plan.splits;
+  const int32_t sx = plan.sx, sp = plan.sp, width = plan.width;
+  const size_t lds = plan.lds;
 #define GTS_LAUNCH(rw, w)                                                                 \
   return launch_rw<T, rw, INTER, w, false>(m, blob, X, rows, ld, phi, stream, splits, sx, sp, \
                                            width, lds)
-  if (priv)
+  if (plan.priv)
     return launch_rw<T, 64, INTER, 4, true>(m, blob, X, rows, ld, phi, stream, splits, sx, sp,
                                             width, lds);
   switch (RW) {
@@ -970,6 +1001,35 @@ gts_status entry(const gts_model* model, const void* d_model, const float* d_X, 
 
 }  // namespace
 }  // namespace gts
+
+extern "C" gts_status gts_launch_config(const gts_model* model, int64_t rows,
+                                        int32_t interactions, gts_launch* out) {
+  using namespace gts;
+  clear_error();
+  if (out == nullptr) return fail(GTS_EINVAL, "out must not be NULL");
+  gts_status st = check_model(model);
+  if (st != GTS_OK) return st;
+  if (rows < 0) return fail(GTS_EINVAL, "rows must be >= 0");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(GTS_EDEVICE, "no HIP device");
+  Plan plan;
+  const DeviceInfo info = device_info();
+  const int64_t r = rows > 0 ? rows : 1;
+  if (model->dtype == GTS_F64)
+    st = interactions ? plan_launch<double, true>(model, r, info, plan)
+                      : plan_launch<double, false>(model, r, info, plan);
+  else
+    st = interactions ? plan_launch<float, true>(model, r, info, plan)
+                      : plan_launch<float, false>(model, r, info, plan);
+  if (st != GTS_OK) return st;
+  out->rows_per_tile = plan.RW;
+  out->waves = plan.waves;
+  out->private_tiles = plan.priv ? 1 : 0;
+  out->slices = plan.splits;
+  out->workgroups = rows > 0 ? plan.tiles * model->num_groups * plan.splits : 0;
+  out->lds_bytes = (int64_t)plan.lds;
+  return GTS_OK;
+}
 
 extern "C" gts_status gts_shap(const gts_model* model, const void* d_model, const float* d_X,
                                int64_t rows, int64_t ld_x, void* d_phi, void* stream) {

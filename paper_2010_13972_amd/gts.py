@@ -58,6 +58,13 @@ class ModelDesc(ctypes.Structure):
 _lib = None
 
 
+class LaunchInfo(ctypes.Structure):
+    """gts_launch (include/gts.h)."""
+    _fields_ = [("rows_per_tile", ctypes.c_int32), ("waves", ctypes.c_int32),
+                ("private_tiles", ctypes.c_int32), ("slices", ctypes.c_int32),
+                ("workgroups", ctypes.c_int64), ("lds_bytes", ctypes.c_int64)]
+
+
 def lib() -> ctypes.CDLL:
     """The loaded libgts.so; raises if it has not been built."""
     global _lib
@@ -87,6 +94,9 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.argtypes = [ctypes.POINTER(ModelDesc), vp, vp, i64, i64, vp, vp]
             f.restype = st
+        L.gts_launch_config.argtypes = [ctypes.POINTER(ModelDesc), i64, i32,
+                                        ctypes.POINTER(LaunchInfo)]
+        L.gts_launch_config.restype = st
         L.gts_last_error.restype = ctypes.c_char_p
         L.gts_version.restype = ctypes.c_char_p
         _lib = L
@@ -362,3 +372,12 @@ def shap_interactions(model: DeviceModel, X, out=None, stream=None):
                                        ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)),
            "gts_shap_interactions")
     return out
+
+
+def launch_config(model: DeviceModel, rows: int, interactions: bool = False) -> dict:
+    """gts_launch_config: the launch shape gts_shap (or gts_shap_interactions)
+    uses for this model and row count on the current device."""
+    info = LaunchInfo()
+    _check(lib().gts_launch_config(ctypes.byref(model.desc), int(rows), 1 if interactions else 0,
+                                   ctypes.byref(info)), "gts_launch_config")
+    return {name: int(getattr(info, name)) for name, _ in LaunchInfo._fields_}

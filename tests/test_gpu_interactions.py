@@ -118,3 +118,18 @@ def test_empty_model_and_unfed_groups(torch, orc):
         got = run(torch, ens, X, dtype)
         assert_parity(got, orc.interactions(ens, X), dtype, 2, "unfed group")
         assert np.all(got[:, 1] == 0.0)
+
+
+@pytest.mark.parametrize("M,rw", [(8, 64), (24, 16), (55, 8)])
+def test_launch_shapes(torch, orc, M, rw):
+    """Tile heights of the interaction launches (gts_launch_config), against
+    the conditioning route."""
+    w = synth.random_workload(30 + M, num_trees=8, max_depth=6, M=M, num_groups=2, n_bg=40,
+                              rows=37)
+    model = gts.prepare(w.ensemble, "f32")
+    cfg = gts.launch_config(model, 37, interactions=True)
+    say("interactions launch shape", M, cfg)
+    assert cfg["rows_per_tile"] == rw and cfg["private_tiles"] == 0
+    assert cfg["workgroups"] == -(-37 // rw) * 2 * cfg["slices"]
+    got = run(torch, w.ensemble, w.X, "f32")
+    assert_parity(got, orc.interactions(w.ensemble, w.X), "f32", 2, f"M={M}")

@@ -155,6 +155,29 @@ def test_empty_model_and_unfed_groups(torch, orc):
         assert np.all(got[:, 1, :] == 0.0)
 
 
+# (M, dtype, rows per tile the launch policy picks): a private tile per wave,
+# and shared tiles of 64, 32, 16 and 4 rows (8 is the wide workload's)
+SHAPES = [(8, "f32", 64), (63, "f32", 64), (150, "f32", 32), (250, "f32", 16),
+          (150, "f64", 16), (3000, "f32", 4)]
+
+
+@pytest.mark.parametrize("M,dtype,rw", SHAPES, ids=[f"M{m}-{d}" for m, d, _ in SHAPES])
+def test_launch_shapes(torch, orc, M, dtype, rw):
+    """Every tile height of the launch policy, checked through
+    gts_launch_config, against Algorithm 1 on a ragged row count."""
+    w = synth.random_workload(7 + M, num_trees=10, max_depth=6, M=M, num_groups=2, n_bg=40,
+                              rows=70)
+    model = gts.prepare(w.ensemble, dtype)
+    cfg = gts.launch_config(model, 70)
+    say("launch shape", M, dtype, cfg)
+    assert cfg["rows_per_tile"] == rw
+    assert cfg["private_tiles"] == (1 if M == 8 else 0)
+    assert cfg["lds_bytes"] <= 160 * 1024
+    assert cfg["workgroups"] == -(-70 // rw) * 2 * cfg["slices"]
+    got = run_shap(torch, w.ensemble, w.X, dtype)
+    assert_parity(got, orc.treeshap(w.ensemble, w.X), dtype, what=f"M={M} {dtype}")
+
+
 # --------------------------------------------------------------------------
 # full-size workloads: sampled rows against Algorithm 1, all rows against Eq. 1
 # --------------------------------------------------------------------------

@@ -327,6 +327,10 @@ def test_device_calls_reject_bad_arguments_without_touching_the_gpu():
         forged = gts.ModelDesc.from_buffer_copy(desc)
         forged.magic = 0
         assert fn(ctypes.byref(forged), vp(1), vp(1), 4, 8, vp(1), None) == gts.GTS_EINVAL
+    info = gts.LaunchInfo()
+    assert L.gts_launch_config(ctypes.byref(desc), 10, 0, None) == gts.GTS_EINVAL
+    assert L.gts_launch_config(None, 10, 0, ctypes.byref(info)) == gts.GTS_EINVAL
+    assert L.gts_launch_config(ctypes.byref(desc), -1, 1, ctypes.byref(info)) == gts.GTS_EINVAL
 
 
 @pytest.mark.parametrize("name", ["tiny", "covtype_med", "wide", "random0", "random2"])
