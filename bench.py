@@ -245,6 +245,7 @@ def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
         "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
                    + (f", {ens.num_features + 1}]" if interactions else "]")),
         "paths": int(len(q)), "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
+        "launch": gts.launch_config(model, rows, interactions),
         "host_prepare_ms": host_ms, "upload_ms": upload_ms, "model_bytes": blob_bytes,
         "extract_ms_device": dev_extract_ms, "extract_ms_host": host_extract_ms,
         "kernel_ms_median": med, "kernel_ms_mean": float(k.mean()),
@@ -528,6 +529,7 @@ def main():
                      "modelled_gflop_per_launch": flops / 1e9,
                      "note": "peak is the packed-FP32 vendor figure; FP32 code that is "
                              "not packed issues at half of it"},
+        "launch": gts.launch_config(model, rows, inter),
         "kernel": {"rows_per_s": rows / (float(np.median(k_only)) * 1e-3),
                    "ms_median": float(np.median(k_only)), "ms_mean": float(k_only.mean()),
                    "ms_std": float(k_only.std()), "runs": len(k_only)},
