@@ -69,16 +69,16 @@ SUITE = [
 # Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
 # of the kernel source the counters were taken on.
 TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 18728829, "write_bytes": 35200000,
-        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
-    ("interactions", "f32", True): {"fetch_bytes": 16043622, "write_bytes": 46142754,
-        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
-    ("deep", "f32", False): {"fetch_bytes": 43108669, "write_bytes": 46080000,
-        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
-    ("deep", "f64", False): {"fetch_bytes": 53145216, "write_bytes": 92160000,
-        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
-    ("wide", "f32", False): {"fetch_bytes": 5909935492, "write_bytes": 316800108,
-        "source": "eca01ab33d7b850d871e0f42d221932cadd68d6de4752e23400421b00ead13a3"},
+    ("covtype_med", "f32", False): {"fetch_bytes": 18729416, "write_bytes": 35200000,
+        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
+    ("interactions", "f32", True): {"fetch_bytes": 16043835, "write_bytes": 45533780,
+        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
+    ("deep", "f32", False): {"fetch_bytes": 43109209, "write_bytes": 46080000,
+        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
+    ("deep", "f64", False): {"fetch_bytes": 53145483, "write_bytes": 92160000,
+        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
+    ("wide", "f32", False): {"fetch_bytes": 5857592682, "write_bytes": 316800062,
+        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
 }
 
 
