@@ -423,7 +423,9 @@ __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q],
 //   (1,0): (o_c - z_c) S_ic = -sum_k c'_k D^i_k         (D^i = E / (z_i + t))
 //   (0,0): (o_i - z_i)(o_c - z_c) S_ic = sum_k c'_k E_k
 // and phi_ii = phi_i - sum_{c != i} Delta_ic (Eq. 6).  Each pair is added to
-// the entry [f_i][f_c] only; the tile write adds the mirror entries.
+// the entry [f_i][f_c] only; the tile write adds the mirror entries.  The
+// lone-element values and v/2 (1 - z) are formed once per element, not once
+// per pair.
 template <typename T, int Q, AddMode MODE>
 __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
                                            const T (&w)[Q], const bool (&on)[Q], T v,
@@ -439,8 +441,16 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
     for (int k = 0; k < Q - 1; ++k) t_pair = fma(T(shapley_weight(Q - 1, k)), E[k], t_pair);
   }
   const T half_v = T(0.5) * v;
-  T tp[Q];    // sum_k c'_k D^c_k for each element c
+  const T k00 = half_v * t_pair;   // (o_i, o_c) = (0, 0)
+  T hw[Q];    // v (1 - z_i) / 2
+  T zc1[Q];   // 1 - z_c
+  T lone[Q];  // -v (1 - z_c) tp[c] / 2: the pair value when only c is present
   T diag[Q];  // running phi_cc
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    hw[i] = T(0.5) * w[i];
+    zc1[i] = T(1) - z[i];
+  }
 #pragma unroll
   for (int c = 0; c < Q; ++c) {
     T D[Q];
@@ -449,12 +459,27 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
 #pragma unroll
     for (int k = 0; k < Q; ++k) s = fma(T(shapley_weight(Q, k)), D[k], s);
     diag[c] = o[c] ? w[c] * s : -v * t_all;
-    tp[c] = T(0);
+    T tpc = T(0);
     if constexpr (Q >= 2) {
 #pragma unroll
-      for (int k = 0; k < Q - 1; ++k) tp[c] = fma(T(shapley_weight(Q - 1, k)), D[k], tp[c]);
+      for (int k = 0; k < Q - 1; ++k) tpc = fma(T(shapley_weight(Q - 1, k)), D[k], tpc);
     }
+    lone[c] = -hw[c] * tpc;
     if (c == 0) continue;
+    // S_ic for every i < c: the Shapley-weighted sum (q-1 players) of
+    // D / (z_i + t).  For many i, as a polynomial in -z_i with coefficients
+    // H_m = sum_k c'_k D_{k+m+1}; for few, by synthetic division.
+    constexpr int kHorner = Q / 2 + 1;
+    T H[Q];
+    if (c > kHorner) {
+#pragma unroll
+      for (int m = 0; m + 1 < Q; ++m) {
+        H[m] = T(shapley_weight(Q - 1, 0)) * D[m + 1];
+#pragma unroll
+        for (int k = 1; k + m + 1 < Q; ++k) H[m] = fma(T(shapley_weight(Q - 1, k)), D[k + m + 1], H[m]);
+      }
+    }
+    const T cw = hw[c];   // v (1 - z_c) / 2, times (1 - z_i) below
     T* p[Q];
     T val[Q];
     bool pon[Q];
@@ -468,18 +493,21 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
     for (int i = 0; i < c; ++i) {
       T s11 = T(0);
       if constexpr (Q >= 2) {
-        T DD[Q];
-        DD[Q - 2] = D[Q - 1];
+        if (c > kHorner) {
+          s11 = H[Q - 2];
 #pragma unroll
-        for (int k = Q - 2; k >= 1; --k) DD[k - 1] = fma(-z[i], DD[k], D[k]);
+          for (int m = Q - 3; m >= 0; --m) s11 = fma(-z[i], s11, H[m]);
+        } else {
+          T DD[Q];
+          DD[Q - 2] = D[Q - 1];
 #pragma unroll
-        for (int k = 0; k < Q - 1; ++k) s11 = fma(T(shapley_weight(Q - 1, k)), DD[k], s11);
+          for (int k = Q - 2; k >= 1; --k) DD[k - 1] = fma(-z[i], DD[k], D[k]);
+#pragma unroll
+          for (int k = 0; k < Q - 1; ++k) s11 = fma(T(shapley_weight(Q - 1, k)), DD[k], s11);
+        }
       }
-      T delta;
-      if (o[i] && o[c]) delta = T(0.5) * w[i] * (T(1) - z[c]) * s11;
-      else if (o[i]) delta = T(-0.5) * w[i] * tp[i];
-      else if (o[c]) delta = T(-0.5) * w[c] * tp[c];
-      else delta = half_v * t_pair;
+      const T both = (cw * zc1[i]) * s11;
+      const T delta = o[i] ? (o[c] ? both : lone[i]) : (o[c] ? lone[c] : k00);
       diag[c] -= delta;
       diag[i] -= delta;
       pon[i] = on[i] && on[c];
