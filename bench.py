@@ -69,16 +69,16 @@ SUITE = [
 # Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
 # of the kernel source the counters were taken on.
 TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 18729416, "write_bytes": 35200000,
-        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
-    ("interactions", "f32", True): {"fetch_bytes": 16043835, "write_bytes": 45533780,
-        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
-    ("deep", "f32", False): {"fetch_bytes": 43109209, "write_bytes": 46080000,
-        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
-    ("deep", "f64", False): {"fetch_bytes": 53145483, "write_bytes": 92160000,
-        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
-    ("wide", "f32", False): {"fetch_bytes": 5857592682, "write_bytes": 316800062,
-        "source": "2e881409368748cfd1ad89270ae0b58e6f8a0ae64b20ed312b2e3b1af3ffe410"},
+    ("covtype_med", "f32", False): {"fetch_bytes": 18727386, "write_bytes": 35200000,
+        "source": "7758b45fc5a3d0d01ce621a79425605526c68543cbd8c652d35a90a651d50030"},
+    ("interactions", "f32", True): {"fetch_bytes": 21103722, "write_bytes": 72099077,
+        "source": "7758b45fc5a3d0d01ce621a79425605526c68543cbd8c652d35a90a651d50030"},
+    ("deep", "f32", False): {"fetch_bytes": 43117213, "write_bytes": 46080000,
+        "source": "7758b45fc5a3d0d01ce621a79425605526c68543cbd8c652d35a90a651d50030"},
+    ("deep", "f64", False): {"fetch_bytes": 53143983, "write_bytes": 92160000,
+        "source": "7758b45fc5a3d0d01ce621a79425605526c68543cbd8c652d35a90a651d50030"},
+    ("wide", "f32", False): {"fetch_bytes": 5890174327, "write_bytes": 316800158,
+        "source": "7758b45fc5a3d0d01ce621a79425605526c68543cbd8c652d35a90a651d50030"},
 }
 
 
