@@ -15,7 +15,9 @@
  *
  * Conventions shared by every call:
  *   - All memory is owned by the caller.  The library allocates nothing on the
- *     device, keeps no state between calls and never frees caller memory.
+ *     device and never frees caller memory.  No result depends on an earlier
+ *     call; the host calls reuse a pool of worker threads (up to 16, started
+ *     on first use) and gts_prepare_model reuses per-thread working memory.
  *   - Every call returns a gts_status; on failure gts_last_error() returns a
  *     message for the calling thread (valid until that thread's next call).
  *   - A split sends x to the left child iff x < threshold; a path element
@@ -241,10 +243,12 @@ gts_status gts_model_layout(const gts_path_element *packed, int64_t num_elements
 /*
  * gts_prepare_model -- Sections 3.1-3.3 in one host pass: extract and merge
  * the paths of `ens`, pack them (bin_capacity, alg as gts_pack_paths) and
- * write the device blob, without materialising the intermediate
- * path-element lists; trees are walked on several host threads.  The blob
- * and descriptor are byte for byte those of
- * gts_model_layout(gts_pack_paths(gts_extract_paths(ens))).
+ * write the device blob, without building the intermediate
+ * gts_path_element arrays; trees are walked, sorted and written on several
+ * host threads.  The blob and descriptor are byte for byte those of
+ * gts_model_layout(gts_pack_paths(gts_extract_paths(ens))).  Its working
+ * memory (about 35 bytes per path element) stays with the calling thread and
+ * is reused by that thread's next call.
  *
  * host_blob host buffer of blob_capacity bytes, or NULL to size only (then
  *           model->bytes gives the size).  bias (out, may be NULL) double[G].

@@ -148,10 +148,13 @@ class Pool {
   static constexpr int kYieldRounds = 4096;     // then yield the core, ~ a millisecond
 
   static void relax(int i) {
-    if (i < kPauseRounds)
+#if defined(__x86_64__) || defined(__i386__)
+    if (i < kPauseRounds) {
       __builtin_ia32_pause();
-    else
-      std::this_thread::yield();
+      return;
+    }
+#endif
+    std::this_thread::yield();
   }
 
   static Pool*& instance() {
