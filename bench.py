@@ -139,12 +139,16 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
           for _ in range(steps)]
     out = None
     model = None
+    host_ms = []   # gts_prepare_model inside each timed step, host clock
 
     def step(k, timed):
         nonlocal out, model
         i = k % 2
         copied[i].synchronize()        # the upload of step k-2 has read pinned[i]
+        h0 = time.perf_counter()
         desc, _, bias = gts.prepare_blob(ens, dtype, out=pinned[i].numpy())
+        if timed:
+            host_ms.append(1e3 * (time.perf_counter() - h0))
         with torch.cuda.stream(copy):
             copy.wait_event(consumed[i])   # the kernel of step k-2 is done with dev[i]
             dev[i].copy_(pinned[i], non_blocking=True)
@@ -170,7 +174,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     kern = np.array([a.elapsed_time(b) for a, b in ev])
     # a model that stays valid after the steps, for the kernel-only timing
     model = gts.prepare(ens, dtype)
-    return wall, kern, out, model
+    return wall, kern, out, model, np.array(host_ms)
 
 
 def time_kernel(torch, gts, model, Xd, reps, interactions):
@@ -495,7 +499,7 @@ def main():
     Xd = torch.from_numpy(w.X).cuda()
     q = path_features(gts, ens)
 
-    wall, kern, out, model = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
+    wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
                                            args.warmup, inter)
     # The roofline takes the kernel's mean launch duration from back-to-back
     # launches (each bracketed by HIP events on its stream).  Inside the
@@ -526,6 +530,7 @@ def main():
                      "kernel": "shap_kernel" + (" (interactions)" if inter else ""),
                      "kernel_ms": kern_ms,
                      "kernel_ms_in_steps": float(kern.mean()),
+                     "host_prepare_ms_in_steps": float(np.median(step_host)),
                      "modelled_gflop_per_launch": flops / 1e9,
                      "note": "peak is the packed-FP32 vendor figure; FP32 code that is "
                              "not packed issues at half of it"},
