@@ -78,6 +78,34 @@ def test_zero_rows_is_a_no_op(torch):
     assert tuple(out.shape) == (0, 1, 9)
 
 
+def test_side_streams_and_concurrent_models(torch):
+    """Launches on two non-default streams at once (two models, one of them
+    with interaction values) give the default stream's results: no result
+    depends on an earlier call.  (Not bit for bit: the order in which waves
+    add to a tile entry varies from run to run.)"""
+    wa, wb = synth.workload("covtype_med"), synth.workload("tiny")
+    ma, mb = gts.prepare(wa.ensemble, "f32"), gts.prepare(wb.ensemble, "f64")
+    Xa = torch.from_numpy(wa.X[:3000]).cuda()
+    Xb = torch.from_numpy(wb.X).cuda()
+    ref_a = gts.shap(ma, Xa)
+    ref_b = gts.shap_interactions(mb, Xb)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            oa = gts.shap(ma, Xa)
+        with torch.cuda.stream(s2):
+            ob = gts.shap_interactions(mb, Xb)
+        outs.append((oa, ob))
+    torch.cuda.synchronize()
+    ra = ref_a.cpu().numpy().astype(np.float64)
+    rb = ref_b.cpu().numpy().astype(np.float64)
+    for oa, ob in outs:
+        assert_parity(oa.cpu().numpy(), ra, "f32", what="side stream, SHAP")
+        assert_parity(ob.cpu().numpy(), rb, "f64", 2, what="side stream, interactions")
+
+
 def chain_tree(depth, M, rng):
     """A spine of `depth` splits on distinct features (the left child
     continues the spine), so the deepest path has `depth` features."""
