@@ -124,41 +124,58 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     """Whole-path steps, pipelined: the host prepares the model of step k+1
     (gts_prepare_model into one of two pinned buffers) and a copy stream
     uploads it into one of two device buffers while the kernel of step k
-    runs.  Timed on the host clock; the kernel is bracketed by HIP events on
-    its stream."""
-    fn = kernel_fn(gts, interactions)
+    runs.  The loop calls the C ABI with arguments marshalled once (the
+    ensemble struct, descriptors, buffer pointers), so the step measures the
+    library rather than Python wrappers.  Timed on the host clock; the kernel
+    is bracketed by HIP events on its stream."""
+    import ctypes
+    L = gts.lib()
+    launch = L.gts_shap_interactions if interactions else L.gts_shap
     compute = torch.cuda.current_stream()
     copy = torch.cuda.Stream()
-    desc, blob, bias = gts.prepare_blob(ens, dtype)
-    nbytes = int(desc.bytes)
+    desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
+    nbytes = int(desc0.bytes)
     pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(2)]
     dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
-    copied = [torch.cuda.Event() for _ in range(2)]    # upload into dev[i] done
+    copied = [torch.cuda.Event() for _ in range(2)]    # upload from pinned[i] done
     consumed = [torch.cuda.Event() for _ in range(2)]  # kernel reading dev[i] done
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
-    out = None
-    model = None
+    ens_struct, keep = gts._ensemble_struct(ens)
+    descs = [gts.ModelDesc() for _ in range(2)]
+    biases = [np.zeros(ens.num_groups, np.float64) for _ in range(2)]
+    rows, M, G = Xd.shape[0], ens.num_features, ens.num_groups
+    shape = (rows, G, M + 1, M + 1) if interactions else (rows, G, M + 1)
+    out = torch.empty(shape, dtype=torch.float64 if dtype == "f64" else torch.float32,
+                      device="cuda")
+    prep_args = [(ctypes.byref(ens_struct), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
+                  ctypes.byref(descs[i]), ctypes.c_void_p(pinned[i].data_ptr()), nbytes,
+                  biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(2)]
+    run_args = [(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
+                 ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
+                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(compute.cuda_stream))
+                for i in range(2)]
     host_ms = []   # gts_prepare_model inside each timed step, host clock
 
     def step(k, timed):
-        nonlocal out, model
         i = k % 2
         copied[i].synchronize()        # the upload of step k-2 has read pinned[i]
         h0 = time.perf_counter()
-        desc, _, bias = gts.prepare_blob(ens, dtype, out=pinned[i].numpy())
+        st = L.gts_prepare_model(*prep_args[i])
         if timed:
             host_ms.append(1e3 * (time.perf_counter() - h0))
+        if st != gts.GTS_OK:
+            raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
         with torch.cuda.stream(copy):
             copy.wait_event(consumed[i])   # the kernel of step k-2 is done with dev[i]
             dev[i].copy_(pinned[i], non_blocking=True)
             copied[i].record(copy)
         compute.wait_event(copied[i])
-        model = gts.DeviceModel(desc, dev[i], ens.num_features, ens.num_groups, dtype,
-                                desc.num_paths, desc.num_bins, bias)
         if timed:
             ev[k][0].record(compute)
-        out = fn(model, Xd, out=out)
+        st = launch(*run_args[i])
+        if st != gts.GTS_OK:
+            raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
         if timed:
             ev[k][1].record(compute)
         consumed[i].record(compute)
@@ -172,7 +189,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     kern = np.array([a.elapsed_time(b) for a, b in ev])
-    # a model that stays valid after the steps, for the kernel-only timing
+    # the last step's output against a model prepared the ordinary way
     model = gts.prepare(ens, dtype)
     return wall, kern, out, model, np.array(host_ms)
 
@@ -500,7 +517,14 @@ def main():
     q = path_features(gts, ens)
 
     wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                           args.warmup, inter)
+                                                      args.warmup, inter)
+    # the steps' last output against the Python binding's call on the same
+    # model (up to the order of the tile additions)
+    ref = kernel_fn(gts, inter)(model, Xd)
+    torch.cuda.synchronize()
+    rel = float((out - ref).abs().max() / (ref.abs().max() + 1e-30))
+    if not rel < 1e-4:
+        raise SystemExit(f"pipelined steps disagree with gts.shap: relative difference {rel:.3g}")
     # The roofline takes the kernel's mean launch duration from back-to-back
     # launches (each bracketed by HIP events on its stream), a timed region of
     # its own right after the steps.  Inside the whole-path steps the GPU
@@ -533,6 +557,8 @@ def main():
                      "kernel_ms": kern_ms,
                      "kernel_ms_in_steps": float(kern.mean()),
                      "host_prepare_ms_in_steps": float(np.median(step_host)),
+                     "host_prepare_ms_in_steps_mean": float(step_host.mean()),
+                     "host_prepare_ms_in_steps_p90": float(np.percentile(step_host, 90)),
                      "modelled_gflop_per_launch": flops / 1e9,
                      "note": "peak is the packed-FP32 vendor figure; FP32 code that is "
                              "not packed issues at half of it"},
