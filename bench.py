@@ -120,14 +120,21 @@ def kernel_fn(gts, interactions):
     return gts.shap_interactions if interactions else gts.shap
 
 
+NBUF = 3   # model buffers in flight in the pipelined steps
+
+
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
-    """Whole-path steps, pipelined: the host prepares the model of step k+1
-    (gts_prepare_model into one of two pinned buffers) and a copy stream
-    uploads it into one of two device buffers while the kernel of step k
-    runs.  The loop calls the C ABI with arguments marshalled once (the
-    ensemble struct, descriptors, buffer pointers), so the step measures the
-    library rather than Python wrappers.  Timed on the host clock; the kernel
-    is bracketed by HIP events on its stream."""
+    """Whole-path steps, pipelined.  Step k prepares its model on the host
+    (gts_prepare_model into pinned buffer k mod 3) and a copy stream uploads
+    it into device buffer k mod 3; its kernel is launched after step k+1's
+    model has been prepared and its upload issued.  The host orders buffer
+    reuse (it waits for the upload that last read a pinned buffer, and for
+    the kernel that last read a device buffer), so the compute stream holds
+    only kernels and no cross-stream waits.  The loop calls the C ABI with
+    arguments marshalled once (the ensemble struct, descriptors, buffer
+    pointers), so the step measures the library rather than Python wrappers.
+    Timed on the host clock; each kernel is bracketed by HIP events on its
+    stream."""
     import ctypes
     L = gts.lib()
     launch = L.gts_shap_interactions if interactions else L.gts_shap
@@ -135,42 +142,45 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     copy = torch.cuda.Stream()
     desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
     nbytes = int(desc0.bytes)
-    pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(2)]
-    dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
-    copied = [torch.cuda.Event() for _ in range(2)]    # upload from pinned[i] done
-    consumed = [torch.cuda.Event() for _ in range(2)]  # kernel reading dev[i] done
+    pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(NBUF)]
+    dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(NBUF)]
+    copied = [torch.cuda.Event() for _ in range(NBUF)]    # upload from pinned[i] done
+    consumed = [torch.cuda.Event() for _ in range(NBUF)]  # kernel reading dev[i] done
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     ens_struct, keep = gts._ensemble_struct(ens)
-    descs = [gts.ModelDesc() for _ in range(2)]
-    biases = [np.zeros(ens.num_groups, np.float64) for _ in range(2)]
+    descs = [gts.ModelDesc() for _ in range(NBUF)]
+    biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NBUF)]
     rows, M, G = Xd.shape[0], ens.num_features, ens.num_groups
     shape = (rows, G, M + 1, M + 1) if interactions else (rows, G, M + 1)
     out = torch.empty(shape, dtype=torch.float64 if dtype == "f64" else torch.float32,
                       device="cuda")
     prep_args = [(ctypes.byref(ens_struct), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
                   ctypes.byref(descs[i]), ctypes.c_void_p(pinned[i].data_ptr()), nbytes,
-                  biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(2)]
+                  biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NBUF)]
     run_args = [(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
                  ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
                  ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(compute.cuda_stream))
-                for i in range(2)]
+                for i in range(NBUF)]
     host_ms = []   # gts_prepare_model inside each timed step, host clock
 
-    def step(k, timed):
-        i = k % 2
-        copied[i].synchronize()        # the upload of step k-2 has read pinned[i]
+    def prepare_and_upload(k, timed):
+        i = k % NBUF
+        copied[i].synchronize()        # the upload of step k-3 has read pinned[i]
         h0 = time.perf_counter()
         st = L.gts_prepare_model(*prep_args[i])
         if timed:
             host_ms.append(1e3 * (time.perf_counter() - h0))
         if st != gts.GTS_OK:
             raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
+        consumed[i].synchronize()      # the kernel of step k-3 is done with dev[i]
         with torch.cuda.stream(copy):
-            copy.wait_event(consumed[i])   # the kernel of step k-2 is done with dev[i]
             dev[i].copy_(pinned[i], non_blocking=True)
             copied[i].record(copy)
-        compute.wait_event(copied[i])
+
+    def launch_kernel(k, timed):
+        i = k % NBUF
+        copied[i].synchronize()        # step k's model is in dev[i]
         if timed:
             ev[k][0].record(compute)
         st = launch(*run_args[i])
@@ -180,12 +190,19 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
             ev[k][1].record(compute)
         consumed[i].record(compute)
 
-    for k in range(warmup):
-        step(k, False)
+    def run_steps(n, timed):
+        if n == 0:
+            return
+        for k in range(n):
+            prepare_and_upload(k, timed)
+            if k > 0:
+                launch_kernel(k - 1, timed)
+        launch_kernel(n - 1, timed)
+
+    run_steps(warmup, False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(steps):
-        step(k, True)
+    run_steps(steps, True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     kern = np.array([a.elapsed_time(b) for a, b in ev])
@@ -481,6 +498,8 @@ def main():
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be at least 1 and --warmup at least 0")
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; the row-sharded "
