@@ -52,11 +52,12 @@ def test_random_edge_case_ensembles(torch, orc, seed, dtype):
     assert_parity(got, orc.interactions(w.ensemble, w.X), dtype, 2, f"random{seed}")
 
 
-@pytest.mark.parametrize("depth", [2, 8, 9, 13, 20])
+@pytest.mark.parametrize("depth", [2, 8, 9, 13, 20, 31, 63])
 def test_long_paths(torch, orc, depth):
-    """Around the unrolled-variant boundary (8 features) and beyond."""
+    """Around the unrolled-variant boundary (8 features), beyond it, and at
+    the wave64 maximum (63 features + root = 64 elements)."""
     rng = np.random.default_rng(100 + depth)
-    M = 24
+    M = 24 if depth <= 24 else 63
     ens = synth.ensemble_from_lists([chain_tree(depth, M, rng), chain_tree(depth // 2 + 1, M, rng)],
                                     M=M)
     X = rng.uniform(0.4, 0.8, size=(40, M)).astype(np.float32)
