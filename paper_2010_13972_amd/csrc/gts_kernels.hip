@@ -683,13 +683,13 @@ __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>&
 }
 
 // One workgroup: rows [tile*RW, tile*RW + RW) of output group g, bins of
-// slice s of that group.  PRIV: every wave accumulates into a phi tile of its
+// slice s of that group (every splits-th bin, starting at bin s).  PRIV: every wave accumulates into a phi tile of its
 // own (summed when the tile is written), so waves never contend; with one
 // path per wave (RW == 64) the accumulation then needs no atomics.
 // Workgroups are dealt to the 8 XCDs round-robin; when the (group, slice)
 // units divide evenly among the XCDs, consecutive workgroups on an XCD take
 // the same unit for successive row tiles, so each XCD's L2 holds only its own
-// part of the model.
+// share of the model's bins.
 template <typename T, int RW, bool INTER, int WAVES, bool PRIV>
 __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const float* __restrict__ X,
                                                          T* __restrict__ phi, Launch L) {
@@ -733,22 +733,23 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   const int lane = threadIdx.x & 63;
   const int r = lane % RW;
   init_stage(stages + wave, lane);
-  const int gb0 = d.group_bins[g], gb1 = d.group_bins[g + 1];
-  const int nb = gb1 - gb0;
-  const int chunk = (nb + L.splits - 1) / L.splits;
-  const int b_lo = gb0 + min(nb, s * chunk);
-  const int b_hi = gb0 + min(nb, (s + 1) * chunk);
+  // Slice s takes every splits-th bin of the group.  Bins come longest paths
+  // first, so contiguous runs would give the first slices the most work;
+  // strided, every slice gets bins of every size.
+  const int gb1 = d.group_bins[g + 1];
+  const int b_lo = d.group_bins[g] + s;
+  const int b_step = L.splits;
   const float* xrow = xs + r * L.sx;
   T* prow = ps + (PRIV ? wave * tile_elems : 0) + r * L.sp;
   const int stride = M + 1;
 
-  int bi = b_lo + wave;
-  if (bi < b_hi) {
+  int bi = b_lo + wave * b_step;
+  if (bi < gb1) {
     Bin<T> cur = load_bin(d, bi, lane);
-    for (; bi < b_hi; bi += WAVES) {
+    for (; bi < gb1; bi += WAVES * b_step) {
       Bin<T> nxt;
-      const int bn = bi + WAVES;
-      if (bn < b_hi) nxt = load_bin(d, bn, lane);
+      const int bn = bi + WAVES * b_step;
+      if (bn < gb1) nxt = load_bin(d, bn, lane);
       process_bin<T, RW, INTER, PRIV && RW == 64>(stages + wave, cur, lane, xrow, prow, stride,
                                                   L.sorted != 0);
       cur = nxt;
