@@ -120,25 +120,29 @@ def kernel_fn(gts, interactions):
     return gts.shap_interactions if interactions else gts.shap
 
 
-NBUF = 3   # model buffers in flight in the pipelined steps
+NBUF = 3      # model buffers in flight in the pipelined steps
+NSTREAMS = 2  # compute streams the steps alternate between
 
 
-def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
+def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=NSTREAMS):
     """Whole-path steps, pipelined.  Step k prepares its model on the host
     (gts_prepare_model into pinned buffer k mod 3) and a copy stream uploads
     it into device buffer k mod 3; its kernel is launched after step k+1's
-    model has been prepared and its upload issued.  The host orders buffer
-    reuse (it waits for the upload that last read a pinned buffer, and for
-    the kernel that last read a device buffer), so the compute stream holds
-    only kernels and no cross-stream waits.  The loop calls the C ABI with
-    arguments marshalled once (the ensemble struct, descriptors, buffer
-    pointers), so the step measures the library rather than Python wrappers.
-    Timed on the host clock; each kernel is bracketed by HIP events on its
-    stream."""
+    model has been prepared and its upload issued, on compute stream k mod 2
+    into output buffer k mod 2.  Consecutive steps are independent batches,
+    so one step's kernel can fill the CUs that the previous one's last
+    workgroups leave idle.  The host orders buffer reuse (it waits for the
+    upload that last read a pinned buffer, and for the kernel that last read
+    a device buffer), so the compute streams hold only kernels and no
+    cross-stream waits.  The loop calls the C ABI with arguments marshalled
+    once (the ensemble struct, descriptors, buffer pointers), so the step
+    measures the library rather than Python wrappers.  Timed on the host
+    clock; each kernel is bracketed by HIP events on its stream."""
     import ctypes
     L = gts.lib()
     launch = L.gts_shap_interactions if interactions else L.gts_shap
-    compute = torch.cuda.current_stream()
+    computes = [torch.cuda.current_stream()] + [torch.cuda.Stream()
+                                                for _ in range(nstreams - 1)]
     copy = torch.cuda.Stream()
     desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
     nbytes = int(desc0.bytes)
@@ -153,15 +157,15 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NBUF)]
     rows, M, G = Xd.shape[0], ens.num_features, ens.num_groups
     shape = (rows, G, M + 1, M + 1) if interactions else (rows, G, M + 1)
-    out = torch.empty(shape, dtype=torch.float64 if dtype == "f64" else torch.float32,
-                      device="cuda")
+    outs = [torch.empty(shape, dtype=torch.float64 if dtype == "f64" else torch.float32,
+                        device="cuda") for _ in range(nstreams)]
     prep_args = [(ctypes.byref(ens_struct), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
                   ctypes.byref(descs[i]), ctypes.c_void_p(pinned[i].data_ptr()), nbytes,
                   biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NBUF)]
-    run_args = [(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
-                 ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
-                 ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(compute.cuda_stream))
-                for i in range(NBUF)]
+    run_args = [[(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
+                  ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
+                  ctypes.c_void_p(outs[j].data_ptr()), ctypes.c_void_p(computes[j].cuda_stream))
+                 for j in range(nstreams)] for i in range(NBUF)]
     host_ms = []   # gts_prepare_model inside each timed step, host clock
 
     def prepare_and_upload(k, timed):
@@ -179,16 +183,17 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
             copied[i].record(copy)
 
     def launch_kernel(k, timed):
-        i = k % NBUF
+        i, j = k % NBUF, k % nstreams
+        stream = computes[j]
         copied[i].synchronize()        # step k's model is in dev[i]
         if timed:
-            ev[k][0].record(compute)
-        st = launch(*run_args[i])
+            ev[k][0].record(stream)
+        st = launch(*run_args[i][j])
         if st != gts.GTS_OK:
             raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
         if timed:
-            ev[k][1].record(compute)
-        consumed[i].record(compute)
+            ev[k][1].record(stream)
+        consumed[i].record(stream)
 
     def run_steps(n, timed):
         if n == 0:
@@ -208,7 +213,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions):
     kern = np.array([a.elapsed_time(b) for a, b in ev])
     # the last step's output against a model prepared the ordinary way
     model = gts.prepare(ens, dtype)
-    return wall, kern, out, model, np.array(host_ms)
+    return wall, kern, outs[(steps - 1) % nstreams], model, np.array(host_ms)
 
 
 def time_kernel(torch, gts, model, Xd, reps, interactions):
@@ -495,11 +500,13 @@ def main():
                          "sweep (Fig. 4)")
     ap.add_argument("--sweep-workloads", default="covtype_med,deep,interactions")
     ap.add_argument("--cpu-limit", type=float, default=4.0)
+    ap.add_argument("--streams", type=int, default=NSTREAMS,
+                    help="compute streams the pipelined steps alternate between")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     args = ap.parse_args()
-    if args.steps < 1 or args.warmup < 0:
-        ap.error("--steps must be at least 1 and --warmup at least 0")
+    if args.steps < 1 or args.warmup < 0 or args.streams < 1:
+        ap.error("--steps and --streams must be at least 1, --warmup at least 0")
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; the row-sharded "
@@ -536,7 +543,7 @@ def main():
     q = path_features(gts, ens)
 
     wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                                      args.warmup, inter)
+                                                      args.warmup, inter, args.streams)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)
