@@ -274,8 +274,11 @@ gts_status gts_prepare_model(const gts_ensemble *ens, int32_t bin_capacity, int3
  * stream   hipStream_t (NULL = default stream).  The call only enqueues work
  *          and returns; results are ready when the stream reaches them.
  * rows == 0 is a no-op.  Errors: GTS_EINVAL for NULL pointers, a descriptor
- * that is not from gts_model_layout, rows < 0, ld_x < M; GTS_EDEVICE if a
- * launch fails.
+ * that is not from gts_model_layout, rows < 0, ld_x < M, or an M whose phi
+ * and X rows do not fit in a workgroup's LDS at 4 rows per tile (on a
+ * 160 KB-LDS device: M <= 4567 in fp32, M <= 2852 in fp64; for
+ * gts_shap_interactions M <= 94 in fp32, M <= 64 in fp64), checked before
+ * any launch; GTS_EDEVICE if a launch fails.
  */
 gts_status gts_shap(const gts_model *model, const void *d_model,
                     const float *d_X, int64_t rows, int64_t ld_x, void *d_phi,

@@ -253,3 +253,46 @@ def test_large_row_counts(torch, orc, name, rows):
     err = np.abs(got.sum(-1) - f)
     bound = sum_tolerance(np.abs(got), "f32")
     assert np.all(err <= bound), float((err / bound).max())
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+@pytest.mark.parametrize("inter", [False, True])
+def test_largest_feature_count(torch, orc, dtype, inter):
+    """The widest phi row a workgroup's LDS holds (4 rows per tile): the
+    largest M that gts_launch_config accepts runs and matches the oracle;
+    one more feature is GTS_EINVAL from the launch call, before any launch."""
+    def stump(M):
+        return [(1, 2, M - 1, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 3.0, -1.0), (-1, -1, -1, 0, 7.0, 4.0)]
+
+    def fits(M):
+        model = gts.prepare(synth.ensemble_from_lists([stump(M)], M=M), dtype)
+        try:
+            gts.launch_config(model, 8, inter)
+            return True
+        except gts.GtsError as e:
+            assert e.status == gts.GTS_EINVAL
+            return False
+
+    lo, hi = 2, 1 << 14
+    assert fits(lo) and not fits(hi)
+    while lo + 1 < hi:
+        mid = (lo + hi) // 2
+        lo, hi = (mid, hi) if fits(mid) else (lo, mid)
+    say("largest M", dtype, inter, lo)
+    rng = np.random.default_rng(lo)
+    fn = gts.shap_interactions if inter else gts.shap
+    want = orc.interactions if inter else orc.treeshap
+    for M, good in ((lo, True), (lo + 1, False)):
+        ens = synth.ensemble_from_lists([stump(M), [(-1, -1, -1, 0.0, 5.0, 0.25)]], M=M)
+        X = rng.uniform(0, 1, size=(9, M)).astype(np.float32)
+        model = gts.prepare(ens, dtype)
+        Xd = torch.from_numpy(X).cuda()
+        if good:
+            got = fn(model, Xd)
+            torch.cuda.synchronize()
+            assert_parity(got.cpu().numpy().astype(np.float64), want(ens, X), dtype,
+                          2 if inter else 1, f"M={M}")
+        else:
+            with pytest.raises(gts.GtsError) as err:
+                fn(model, Xd)
+            assert err.value.status == gts.GTS_EINVAL
