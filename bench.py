@@ -575,7 +575,8 @@ def main():
                               + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": "extract + merge + bias + BFD pack (B=64) + layout (host) + upload "
                            + ("+ interaction kernel" if inter else "+ SHAP kernel")
-                           + "; host work of step k+1 and its upload overlap the kernel of step k"},
+                           + "; host work of step k+1 and its upload overlap the kernel of step k",
+                   "compute_streams": args.streams},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": traffic_for((args.workload, dtype, inter)),
@@ -587,7 +588,10 @@ def main():
                      "host_prepare_ms_in_steps_p90": float(np.percentile(step_host, 90)),
                      "modelled_gflop_per_launch": flops / 1e9,
                      "note": "peak is the packed-FP32 vendor figure; non-packed FP32 FMAs "
-                             "measured about 129 TFLOP/s on this chip"},
+                             "measured about 129 TFLOP/s on this chip. kernel_ms: back-to-back "
+                             "launches on one stream; kernel_ms_in_steps: event spans of the "
+                             "pipelined steps' launches, which on two streams overlap the "
+                             "other stream's kernel"},
         "launch": gts.launch_config(model, rows, inter),
         "kernel": {"rows_per_s": rows / (float(np.median(k_only)) * 1e-3),
                    "ms_median": float(np.median(k_only)), "ms_mean": float(k_only.mean()),
