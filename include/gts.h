@@ -16,8 +16,9 @@
  * Conventions shared by every call:
  *   - All memory is owned by the caller.  The library allocates nothing on the
  *     device and never frees caller memory.  No result depends on an earlier
- *     call; the host calls reuse a pool of worker threads (up to 16, started
- *     on first use) and gts_prepare_model reuses per-thread working memory.
+ *     call; the host calls reuse a pool of worker threads (up to 16, two
+ *     fewer than the process's cores when it has 8 or more, started on first
+ *     use) and gts_prepare_model reuses per-thread working memory.
  *   - Every call returns a gts_status; on failure gts_last_error() returns a
  *     message for the calling thread (valid until that thread's next call).
  *   - A split sends x to the left child iff x < threshold; a path element
