@@ -72,6 +72,13 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                               "or python -m paper_2010_13972_amd.build")
+        # torch carries its own copy of the HIP runtime.  Loaded first, it is
+        # the copy libgts binds to; loaded after libgts had brought in the
+        # system one, the process held two runtimes and torch found no device.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         st = ctypes.c_int
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
