@@ -668,9 +668,16 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
       // and bit (residual - 1) of `open` set when that heap is not empty
       for (BinHeap& h : by_resid) h.clear();
       uint64_t open = 0;
+      // Items of one size come in a run.  Once an item has gone into bin b
+      // (the smallest residual that fits, every other fitting residual being
+      // at least as large), b's new residual, if it still fits, is strictly
+      // the smallest: the next items of the run go into b until it no longer
+      // fits.  So a bin takes residual / s items of the run at once, the
+      // placements item-by-item Best-Fit-Decreasing makes.
       for (int64_t kk = 0; kk < nsize; ++kk) {
         const int32_t s = cap - (int32_t)kk;
-        for (int64_t k = key_start[r * nsize + kk]; k < key_start[r * nsize + kk + 1]; ++k) {
+        const int64_t k1 = key_start[r * nsize + kk + 1];
+        for (int64_t k = key_start[r * nsize + kk]; k < k1;) {
           int64_t b;
           int32_t res;
           const uint64_t fit = s >= 1 ? open >> (s - 1) : open;
@@ -682,12 +689,15 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
             b = open_bin(g);
             res = cap;
           }
-          const int32_t left = res - s;
-          if (left > 0) {
-            heap_push(by_resid[(size_t)left], b);
-            open |= 1ull << (left - 1);
+          const int64_t n = std::min<int64_t>(res / s, k1 - k);
+          for (int64_t t = 0; t < n; ++t, ++k) {
+            put(k, b, cap - res, s);
+            res -= s;
           }
-          put(k, b, cap - res, s);
+          if (res > 0) {
+            heap_push(by_resid[(size_t)res], b);
+            open |= 1ull << (res - 1);
+          }
         }
       }
     } else if (alg == GTS_PACK_FFD) {
