@@ -704,18 +704,26 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
       const int64_t first_bin = K;
       FirstFitTree tree(j - i);
       resid.assign((size_t)(j - i), 0);
+      // As for BFD, a run of equal-size items fills the chosen bin: every
+      // bin left of it is too full for this size, so it stays the leftmost
+      // fit while it fits.
       for (int64_t kk = 0; kk < nsize; ++kk) {
         const int32_t s = cap - (int32_t)kk;
-        for (int64_t k = key_start[r * nsize + kk]; k < key_start[r * nsize + kk + 1]; ++k) {
+        const int64_t k1 = key_start[r * nsize + kk + 1];
+        for (int64_t k = key_start[r * nsize + kk]; k < k1;) {
           int64_t local = tree.leftmost_at_least(s);
           if (local < 0) {
             local = open_bin(g) - first_bin;
             resid[(size_t)local] = cap;
           }
-          const int32_t res = resid[(size_t)local];
-          resid[(size_t)local] = res - s;
-          tree.set(local, res - s);
-          put(k, first_bin + local, cap - res, s);
+          int32_t res = resid[(size_t)local];
+          const int64_t n = std::min<int64_t>(res / s, k1 - k);
+          for (int64_t t = 0; t < n; ++t, ++k) {
+            put(k, first_bin + local, cap - res, s);
+            res -= s;
+          }
+          resid[(size_t)local] = res;
+          tree.set(local, res);
         }
       }
     } else if (alg == GTS_PACK_NF) {
