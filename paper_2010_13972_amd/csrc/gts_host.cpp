@@ -894,74 +894,104 @@ inline void put_element(const gts_model& m, char* blob, int64_t i, int32_t feat,
   else reinterpret_cast<float*>(blob + m.off[kZero])[i] = (float)z_or_v;
 }
 
-// Device order of a path's feature elements.  The kernels may run several
-// paths of a bin side by side, one per group of lanes, stepping through their
-// elements together; paths that share a feature (often the same tree's upper
-// splits) would then update the same phi-tile entry in the same step, which
-// the kernels' compare-and-swap accumulation resolves by retrying.  SHAP
+// Device order of a path's feature elements.
+//
+// Zero-fraction elements come first, in feature order, and the root's feature
+// slot holds -1 - (their count).  A row outside the range of such an element
+// meets the factor z + o t = 0 of the path's weight polynomial, so the
+// (row, path) contributes nothing; the kernels test these elements first and
+// skip a path that no row of their tile reaches.
+//
+// The other elements are rotated.  The kernels may run several paths of a
+// bin side by side, one per group of lanes, stepping through their elements
+// together; paths that share a feature (often the same tree's upper splits)
+// would then update the same phi-tile entry in the same step, which the
+// kernels' compare-and-swap accumulation resolves by retrying.  SHAP
 // arithmetic does not depend on the element order, so each path's
-// feature-sorted elements are rotated: paths are taken in their order in the
-// bin, and each gets the rotation (tried from t mod q for the t-th path) that
-// puts the fewest of its features at a position where an earlier path of
-// the bin already has the same feature.
+// feature-sorted remaining elements are rotated: paths are taken in their
+// order in the bin, and each gets the rotation (tried from t mod q' for the
+// t-th path, q' the number of elements rotated) that puts the fewest of its
+// features at a position where an earlier path of the bin already has the
+// same feature.
+//
+// f, z: the path's q feature elements in ascending feature order (z in the
+// blob's precision); used[f] has bit k set when an earlier path of the bin
+// stores feature f at position k.  Writes order[k] = the source index stored
+// at position k and returns the number of zero-fraction elements.
+template <typename Z>
+int32_t device_order(const int32_t* f, const Z* z, int32_t q, int32_t t_in_bin,
+                     const uint64_t* used, int32_t* order) {
+  int32_t n0 = 0;
+  for (int32_t j = 0; j < q; ++j)
+    if (z[j] == Z(0)) order[n0++] = j;
+  int32_t rest[kMaxPathLen];
+  int32_t nr = 0;
+  for (int32_t j = 0; j < q; ++j)
+    if (z[j] != Z(0)) rest[nr++] = j;
+  int32_t best = 0;
+  if (nr > 1) {
+    // cost[rho]: collisions if rest element i goes to position
+    // n0 + (i - rho) mod nr
+    int32_t cost[kMaxPathLen];
+    for (int32_t k = 0; k < nr; ++k) cost[k] = 0;
+    const uint64_t in_q = q >= 64 ? ~0ull : (1ull << q) - 1;
+    const uint64_t below = n0 >= 64 ? ~0ull : (1ull << n0) - 1;
+    for (int32_t i = 0; i < nr; ++i) {
+      uint64_t bits = used[(size_t)f[rest[i]]] & in_q & ~below;
+      while (bits) {
+        const int32_t kk = __builtin_ctzll(bits) - n0;
+        bits &= bits - 1;
+        ++cost[i >= kk ? i - kk : i - kk + nr];
+      }
+    }
+    int32_t rho = t_in_bin % nr, best_cost = INT32_MAX;
+    for (int32_t c = 0; c < nr; ++c) {
+      if (cost[rho] < best_cost) {
+        best_cost = cost[rho];
+        best = rho;
+        if (best_cost == 0) break;
+      }
+      if (++rho == nr) rho = 0;
+    }
+  }
+  int32_t src = best;
+  for (int32_t k = 0; k < nr; ++k, ++src) {
+    if (src == nr) src = 0;
+    order[n0 + k] = rest[src];
+  }
+  return n0;
+}
+
+// Applies device_order to the paths of one bin of a blob written in packed
+// order (root first, features ascending), in place.
 template <typename Z>
 void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t a1,
                 std::vector<uint64_t>& used, std::vector<int32_t>& touched) {
   Z zbuf[kMaxPathLen];
   float lbuf[kMaxPathLen], hbuf[kMaxPathLen];
-  int32_t fbuf[kMaxPathLen];
+  int32_t fbuf[kMaxPathLen], order[kMaxPathLen];
   int32_t t = 0;
   int64_t a = a0;
   while (a < a1) {
     int64_t e = a + 1;
-    while (e < a1 && feat[e] != -1) ++e;
+    while (e < a1 && feat[e] >= 0) ++e;
     const int32_t q = (int32_t)(e - a - 1);
-    if (q > 1) {
-      const int32_t* f = feat + a + 1;
-      int32_t best = 0, best_cost = INT32_MAX;
-      // cost[rho]: collisions if element j goes to position (j - rho) mod q;
-      // only features an earlier path of the bin has at some position < q
-      // contribute
-      int32_t cost[kMaxPathLen];
-      for (int32_t k = 0; k < q; ++k) cost[k] = 0;
-      const uint64_t in_q = q >= 64 ? ~0ull : (1ull << q) - 1;
-      for (int32_t j = 0; j < q; ++j) {
-        uint64_t bits = used[(size_t)f[j]] & in_q;
-        while (bits) {
-          const int32_t k = __builtin_ctzll(bits);
-          bits &= bits - 1;
-          const int32_t rho = j >= k ? j - k : j - k + q;
-          ++cost[rho];
-        }
-      }
-      int32_t rho = t % q;
-      for (int32_t i = 0; i < q; ++i) {
-        if (cost[rho] < best_cost) {
-          best_cost = cost[rho];
-          best = rho;
-          if (best_cost == 0) break;
-        }
-        if (++rho == q) rho = 0;
-      }
-      int32_t src_k = best;
-      for (int32_t k = 0; k < q; ++k, ++src_k) {
-        if (src_k == q) src_k = 0;
-        const int64_t src = a + 1 + src_k;
-        fbuf[k] = feat[src];
-        lbuf[k] = lo[src];
-        hbuf[k] = hi[src];
-        zbuf[k] = zf[src];
-      }
-      for (int32_t k = 0; k < q; ++k) {
-        feat[a + 1 + k] = fbuf[k];
-        lo[a + 1 + k] = lbuf[k];
-        hi[a + 1 + k] = hbuf[k];
-        zf[a + 1 + k] = zbuf[k];
-      }
-    }
+    const int32_t n0 = device_order(feat + a + 1, zf + a + 1, q, t, used.data(), order);
     for (int32_t k = 0; k < q; ++k) {
-      uint64_t& m = used[(size_t)feat[a + 1 + k]];
-      if (m == 0) touched.push_back(feat[a + 1 + k]);
+      const int64_t src = a + 1 + order[k];
+      fbuf[k] = feat[src];
+      lbuf[k] = lo[src];
+      hbuf[k] = hi[src];
+      zbuf[k] = zf[src];
+    }
+    feat[a] = -1 - n0;
+    for (int32_t k = 0; k < q; ++k) {
+      feat[a + 1 + k] = fbuf[k];
+      lo[a + 1 + k] = lbuf[k];
+      hi[a + 1 + k] = hbuf[k];
+      zf[a + 1 + k] = zbuf[k];
+      uint64_t& m = used[(size_t)fbuf[k]];
+      if (m == 0) touched.push_back(fbuf[k]);
       m |= 1ull << k;
     }
     ++t;
@@ -1168,9 +1198,10 @@ struct PrepareScratch {
   Packing pk;
 };
 
-// Writes the paths of bin b into the blob, rotating each path's features as
-// rotate_bin does (same choices, taken from the feature-sorted source).
-// by_bin[bin_first[b] ..]: the placements of bin b in placement order.
+// Writes the paths of bin b into the blob, in the device order of
+// device_order (the choices rotate_bin makes, taken from the feature-sorted
+// source).  by_bin[bin_first[b] ..]: the placements of bin b in placement
+// order.
 template <typename Z>
 void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees,
                const int64_t* path_tree, const int64_t* tree_first, const Packing& pk,
@@ -1182,6 +1213,8 @@ void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees
   float* const upper = reinterpret_cast<float*>(blob + m.off[kUpper]);
   Z* const zero = reinterpret_cast<Z*>(blob + m.off[kZero]);
   uint64_t* const u = used.data();
+  int32_t fs[kMaxPathLen], order[kMaxPathLen];
+  Z zs[kMaxPathLen];
   int32_t t_in_bin = 0;
   const int64_t base = pk.bin_offsets[(size_t)b];
   for (int64_t i = pk.bin_first[(size_t)b]; i < pk.bin_first[(size_t)b + 1]; ++i, ++t_in_bin) {
@@ -1193,45 +1226,25 @@ void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees
     const Split* src = tr.el.data() + tr.first[j];
     const int32_t q = tr.size[j] - 1;
     const int64_t d = base + pk.within_at[(size_t)k];
-    feat[d] = -1;
+    for (int32_t jj = 0; jj < q; ++jj) {
+      fs[jj] = src[jj].feature;
+      zs[jj] = (Z)src[jj].zero_fraction;
+    }
+    const int32_t n0 = device_order(fs, zs, q, t_in_bin, u, order);
+    feat[d] = -1 - n0;
     lower[d] = -inf;
     upper[d] = inf;
     zero[d] = (Z)tr.v[j];
-    int32_t best = 0;
-    if (q > 1) {
-      int32_t cost[kMaxPathLen];
-      for (int32_t k = 0; k < q; ++k) cost[k] = 0;
-      const uint64_t in_q = q >= 64 ? ~0ull : (1ull << q) - 1;
-      for (int32_t jj = 0; jj < q; ++jj) {
-        uint64_t bits = u[src[jj].feature] & in_q;
-        while (bits) {
-          const int32_t k = __builtin_ctzll(bits);
-          bits &= bits - 1;
-          ++cost[jj >= k ? jj - k : jj - k + q];
-        }
-      }
-      int32_t rho = t_in_bin % q, best_cost = INT32_MAX;
-      for (int32_t c = 0; c < q; ++c) {
-        if (cost[rho] < best_cost) {
-          best_cost = cost[rho];
-          best = rho;
-          if (best_cost == 0) break;
-        }
-        if (++rho == q) rho = 0;
-      }
-    }
-    int32_t sk = best;
-    for (int32_t k = 0; k < q; ++k, ++sk) {
-      if (sk == q) sk = 0;
-      const Split& e = src[sk];
-      const int64_t o = d + 1 + k;
+    for (int32_t kk = 0; kk < q; ++kk) {
+      const Split& e = src[order[kk]];
+      const int64_t o = d + 1 + kk;
       feat[o] = e.feature;
       lower[o] = e.lower;
       upper[o] = e.upper;
-      zero[o] = (Z)e.zero_fraction;
+      zero[o] = zs[order[kk]];
       uint64_t& bits = u[e.feature];
       if (bits == 0) touched.push_back(e.feature);
-      bits |= 1ull << k;
+      bits |= 1ull << kk;
     }
   }
   for (int32_t f : touched) used[(size_t)f] = 0;

@@ -14,10 +14,12 @@ namespace gts {
 // never mix output groups and are ordered by group.  A path is a root element
 // followed by its feature elements; the root's zero-fraction slot holds the
 // path's leaf value v (a root's own zero fraction is always 1 and unused).
-// Within a bin, each path's feature-sorted elements are stored rotated (see
-// rotate_bin in the host code); roots stay first.
+// Within a bin, each path's zero-fraction elements come first (feature
+// order), then its other elements rotated (see device_order in the host
+// code); roots stay first.
 enum BlobArray : int {
-  kFeat = 0,       // int32[num_elements]   split feature, -1 on root elements
+  kFeat = 0,       // int32[num_elements]   split feature; on a root -1 - (the
+                   //                       path's zero-fraction elements)
   kLower = 1,      // float[num_elements]   range [lower, upper)
   kUpper = 2,      // float[num_elements]
   kZero = 3,       // T[num_elements]       zero fraction (leaf value on roots)

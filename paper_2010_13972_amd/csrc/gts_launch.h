@@ -1,0 +1,56 @@
+// Launch plan shared by the planner (gts_kernels.hip) and the translation
+// units that instantiate the SHAP kernels (gts_shap_f32.hip and friends).
+// Not part of the public ABI.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include "gts_internal.h"
+
+namespace gts {
+
+// Longest path (features) with fully unrolled per-path code.  Longer paths
+// run the runtime-loop code, in fp64, which keeps its per-path arrays in
+// per-lane private memory; only the long-path kernel variants contain it.
+constexpr int kMaxUnrolledShap = 12;
+constexpr int kMaxUnrolledInter = 8;
+
+// Kernel variant by the model's longest path: every path has at most 8
+// features, at most 12, or any length up to a full bin (63).
+constexpr int kQShort = 8;
+constexpr int kQMid = 12;
+constexpr int kQLong = 64;
+
+// The launch shape of a model and row count: rows per tile, waves, private
+// tiles, LDS strides and bytes, bin slices, and the kernel variant.
+struct Plan {
+  int RW = 0;
+  int waves = 8;
+  bool priv = false;
+  int32_t sx = 0, sp = 0, width = 0;
+  size_t lds = 0;
+  int splits = 1;
+  int64_t tiles = 0;
+  int qmax = kQLong;
+};
+
+// Arguments of one gts_shap / gts_shap_interactions call.
+struct KernelArgs {
+  const gts_model* m;
+  const void* blob;
+  const float* X;
+  int64_t rows;
+  int64_t ld;
+  void* phi;
+  void* stream;   // hipStream_t
+};
+
+// One launcher per (dtype, kind); each lives in its own translation unit so
+// the kernel variants compile in parallel.
+gts_status launch_shap_f32(const KernelArgs& a, const Plan& p);
+gts_status launch_shap_f64(const KernelArgs& a, const Plan& p);
+gts_status launch_inter_f32(const KernelArgs& a, const Plan& p);
+gts_status launch_inter_f64(const KernelArgs& a, const Plan& p);
+
+}  // namespace gts
