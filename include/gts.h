@@ -6,6 +6,7 @@
  * Pipeline (Section 3, steps 1-4):
  *   gts_extract_paths   host   ensemble -> merged unique root-to-leaf paths
  *   gts_extract_paths_device  the same on the GPU, bit for bit
+ *   gts_extract_paths_device_noalloc  the same without a caller workspace
  *   gts_pack_paths      host   paths -> bins of <= 64 path elements
  *   gts_model_layout    host   packed paths -> one device-ready byte blob
  *   gts_prepare_model   host   the three steps above in one pass
@@ -14,8 +15,9 @@
  *   gts_launch_config   host   the launch shape the two calls above choose
  *
  * Conventions shared by every call:
- *   - All memory is owned by the caller.  The library allocates nothing on the
- *     device and never frees caller memory.  No result depends on an earlier
+ *   - All memory is owned by the caller.  The library calls no device
+ *     allocator and never frees caller memory; its only device memory of its
+ *     own is the fixed workspace array of gts_extract_paths_device_noalloc.  No result depends on an earlier
  *     call; the host calls reuse a pool of worker threads (up to 16, two
  *     fewer than the process's cores when it has 8 or more, started on first
  *     use) and gts_prepare_model reuses per-thread working memory.
@@ -190,6 +192,29 @@ gts_status gts_extract_paths_device(const gts_ensemble *ens, gts_path_element *d
                                     int64_t capacity, int64_t *num_elements,
                                     int64_t *num_paths, double *d_bias, void *d_workspace,
                                     int64_t workspace_bytes, void *stream);
+
+/*
+ * gts_extract_paths_device_noalloc -- gts_extract_paths_device for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation).  Same arguments, output,
+ * order and errors as gts_extract_paths_device, without d_workspace: the
+ * workspace is a fixed array of GTS_EXTRACT_NOALLOC_BYTES bytes in the
+ * library's device code, one per device, held from module load until the
+ * process ends.  The call itself allocates nothing (no hipMalloc, no
+ * allocating library routine).
+ *
+ * Limit: an ensemble whose workspace (gts_extract_workspace_bytes) exceeds
+ * GTS_EXTRACT_NOALLOC_BYTES (64 MiB, about 1.2 million nodes) gets GTS_EINVAL
+ * before any device work.  Every call on a device shares that device's array
+ * and leaves its contents behind (each call initialises what it reads):
+ * calls that overlap on one device -- on different streams or from different
+ * threads -- race and are not supported; serialise them.
+ */
+#define GTS_EXTRACT_NOALLOC_BYTES (64LL << 20)
+
+gts_status gts_extract_paths_device_noalloc(const gts_ensemble *ens, gts_path_element *d_out,
+                                            int64_t capacity, int64_t *num_elements,
+                                            int64_t *num_paths, double *d_bias, void *stream);
 
 /*
  * gts_pack_paths -- Section 3.3 (bin packing for work allocation).

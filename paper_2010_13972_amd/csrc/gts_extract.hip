@@ -24,6 +24,8 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
+#include <vector>
 
 #include "gts_internal.h"
 
@@ -441,12 +443,12 @@ extern "C" gts_status gts_extract_workspace_bytes(int64_t num_trees, int64_t num
   return GTS_OK;
 }
 
-extern "C" gts_status gts_extract_paths_device(const gts_ensemble* ens, gts_path_element* d_out,
-                                               int64_t capacity, int64_t* num_elements,
-                                               int64_t* num_paths, double* d_bias,
-                                               void* d_workspace, int64_t workspace_bytes,
-                                               void* stream) {
-  clear_error();
+namespace gts {
+namespace {
+
+gts_status extract_device(const gts_ensemble* ens, gts_path_element* d_out, int64_t capacity,
+                          int64_t* num_elements, int64_t* num_paths, double* d_bias,
+                          void* d_workspace, int64_t workspace_bytes, void* stream) {
   if (ens == nullptr || num_elements == nullptr || num_paths == nullptr)
     return fail(GTS_EINVAL, "ensemble, num_elements and num_paths must not be NULL");
   if (ens->num_features < 1 || ens->num_groups < 1 || ens->num_trees < 0 || ens->num_nodes < 0)
@@ -530,4 +532,78 @@ extern "C" gts_status gts_extract_paths_device(const gts_ensemble* ens, gts_path
   }
   if (hipGetLastError() != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed");
   return GTS_OK;
+}
+
+}  // namespace
+}  // namespace gts
+
+extern "C" gts_status gts_extract_paths_device(const gts_ensemble* ens, gts_path_element* d_out,
+                                               int64_t capacity, int64_t* num_elements,
+                                               int64_t* num_paths, double* d_bias,
+                                               void* d_workspace, int64_t workspace_bytes,
+                                               void* stream) {
+  clear_error();
+  return extract_device(ens, d_out, capacity, num_elements, num_paths, d_bias, d_workspace,
+                        workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// allocation-free variant: the workspace is a fixed device array
+// ---------------------------------------------------------------------------
+
+// Workspace of gts_extract_paths_device_noalloc on every device the library
+// runs on (each device holds its own copy, from module load to process exit).
+// Host code never uses this name as an address: the device address comes
+// from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[GTS_EXTRACT_NOALLOC_BYTES];
+
+namespace gts {
+namespace {
+
+// The device address of `scratch` on the current device, looked up on the
+// first call on that device (with it current) and kept.
+gts_status scratch_address(void** out) {
+  static std::mutex mu;
+  static std::vector<void*> addr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(GTS_EDEVICE, "no HIP device");
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)addr.size() <= dev) addr.resize((size_t)dev + 1, nullptr);
+  if (addr[(size_t)dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess || p == nullptr)
+      return fail(GTS_EDEVICE, "hipGetSymbolAddress of the extraction workspace failed: %s",
+                  hipGetErrorString(err));
+    addr[(size_t)dev] = p;
+  }
+  *out = addr[(size_t)dev];
+  return GTS_OK;
+}
+
+}  // namespace
+}  // namespace gts
+
+extern "C" gts_status gts_extract_paths_device_noalloc(const gts_ensemble* ens,
+                                                       gts_path_element* d_out, int64_t capacity,
+                                                       int64_t* num_elements, int64_t* num_paths,
+                                                       double* d_bias, void* stream) {
+  clear_error();
+  if (ens == nullptr) return fail(GTS_EINVAL, "ensemble must not be NULL");
+  if (ens->num_trees < 0 || ens->num_nodes < 0)
+    return fail(GTS_EINVAL, "ensemble sizes out of range");
+  int64_t o[kArrays];
+  size_t scan_bytes = 0;
+  const int64_t need = plan(ens->num_trees, ens->num_nodes, o, &scan_bytes);
+  if (need > GTS_EXTRACT_NOALLOC_BYTES)
+    return fail(GTS_EINVAL,
+                "ensemble of %lld trees and %lld nodes needs %lld bytes of workspace; "
+                "gts_extract_paths_device_noalloc holds %lld (use gts_extract_paths_device)",
+                (long long)ens->num_trees, (long long)ens->num_nodes, (long long)need,
+                (long long)GTS_EXTRACT_NOALLOC_BYTES);
+  void* ws = nullptr;
+  const gts_status st = scratch_address(&ws);
+  if (st != GTS_OK) return st;
+  return extract_device(ens, d_out, capacity, num_elements, num_paths, d_bias, ws,
+                        GTS_EXTRACT_NOALLOC_BYTES, stream);
 }

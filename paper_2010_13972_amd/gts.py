@@ -97,6 +97,9 @@ def lib() -> ctypes.CDLL:
         L.gts_extract_paths_device.argtypes = [ctypes.POINTER(_Ensemble), vp, i64, vp, vp, vp,
                                                vp, i64, vp]
         L.gts_extract_paths_device.restype = st
+        L.gts_extract_paths_device_noalloc.argtypes = [ctypes.POINTER(_Ensemble), vp, i64, vp,
+                                                       vp, vp, vp]
+        L.gts_extract_paths_device_noalloc.restype = st
         for name in ("gts_shap", "gts_shap_interactions"):
             f = getattr(L, name)
             f.argtypes = [ctypes.POINTER(ModelDesc), vp, vp, i64, i64, vp, vp]
@@ -207,6 +210,27 @@ def extract_paths_device(dens: DeviceEnsemble, stream=None, workspace=None):
                                           ctypes.c_void_p(bias.data_ptr()),
                                           ctypes.c_void_p(workspace.data_ptr()),
                                           workspace.numel(), h), "gts_extract_paths_device")
+    return out[:n.value * PATH_ELEMENT.itemsize], int(npaths.value), bias
+
+
+def extract_paths_device_noalloc(dens: DeviceEnsemble, stream=None):
+    """gts_extract_paths_device_noalloc: as extract_paths_device, with the
+    library's fixed device workspace instead of a caller's."""
+    import torch
+    dev = dens.tensors["left"].device
+    n = ctypes.c_int64(0)
+    npaths = ctypes.c_int64(0)
+    h = _stream_handle(stream)
+    _check(lib().gts_extract_paths_device_noalloc(ctypes.byref(dens.struct), None, 0,
+                                                  ctypes.byref(n), ctypes.byref(npaths), None, h),
+           "gts_extract_paths_device_noalloc")
+    out = torch.empty(max(1, n.value) * PATH_ELEMENT.itemsize, dtype=torch.uint8, device=dev)
+    bias = torch.empty(dens.num_groups, dtype=torch.float64, device=dev)
+    _check(lib().gts_extract_paths_device_noalloc(ctypes.byref(dens.struct),
+                                                  ctypes.c_void_p(out.data_ptr()), n.value,
+                                                  ctypes.byref(n), ctypes.byref(npaths),
+                                                  ctypes.c_void_p(bias.data_ptr()), h),
+           "gts_extract_paths_device_noalloc")
     return out[:n.value * PATH_ELEMENT.itemsize], int(npaths.value), bias
 
 
