@@ -1,28 +1,33 @@
 """Benchmark: exact TreeShap rows/s on one MI355X.
 
-One step is one pass of the whole path over one batch of rows of the
-covtype-shaped workload (100 trees, depth <= 8, split probability 0.85,
-M = 54, 10 000 rows, fp32): path extraction with duplicate merging and the
-bias, Best-Fit-Decreasing packing into 64-element bins, device layout and
-upload of the model (host), then the SHAP kernel over the batch (device).
-The rows X are resident in HBM before timing starts.  `value` is rows
-explained per second over the timed steps.
+One step is one pass of the whole path over one batch of rows of the deep
+regression workload (1000 trees, depth <= 16, split probability 0.7, at most
+1024 leaves per tree, M = 8, 10 000 rows, fp32): path extraction with
+duplicate merging and the bias, Best-Fit-Decreasing packing into 64-element
+bins, device layout and upload of the model (host), then the SHAP kernel over
+the batch (device).  The rows X are resident in HBM before timing starts.
+`value` is rows explained per second over the timed steps.
 
 The same JSON line carries:
-  roofline      the SHAP kernel's modelled VALU rate against the MI355X
-                vector peak (op model per (row, path) with q path features:
-                10 q^2 + 8 q flops; interactions add q (q-1)(10 q + 4)),
-                its mean duration from HIP events on the launch stream over
-                back-to-back launches, and its HBM traffic from rocprofv3
-                FETCH_SIZE / WRITE_SIZE, scaled by the same counters' reading
-                of a plain device copy (null when the kernel source differs
-                from the one the counters were taken on);
-  kernel        kernel-only rows/s (median, mean and std of the launches);
+  roofline      the SHAP kernel against the MI355X FP32 vector peak.  Its
+                algorithmic flops are the op model (10 q^2 + 8 q per
+                (row, path) with q path features; interactions add
+                q (q-1)(10 q + 4)) summed over the live (row, path) pairs --
+                a pair with a zero-cover element whose range misses the row
+                contributes exactly nothing and is not work the method needs
+                -- counted exactly on the device; its duration is the mean
+                of HIP events around its launches inside the timed steps, on
+                the launch stream.  HBM traffic and executed VALU
+                instructions come from rocprofv3 counters of the same kernel
+                code (null when the kernel sources differ from the ones the
+                counters were taken on);
+  kernel        kernel-only rows/s over back-to-back launches;
   configs       every workload of the suite (tiny, covtype-shaped, deep fp32
-                and fp64, wide multiclass, interactions): host preparation
-                time, kernel time and rows/s, modelled rate and fraction;
+                and fp64, wide multiclass, interactions): host preparation,
+                kernel time and rows/s, live pairs, modelled rate and
+                fraction, and the CPU oracle's rate on a row prefix;
   cpu_baseline  the fp64 CPU oracle (Algorithm 1, OpenMP over rows) on a row
-                prefix of the same batch, on the host's cores, and on one
+                prefix of the headline batch, on the host's cores, and on one
                 thread.
 """
 from __future__ import annotations
@@ -41,8 +46,18 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_TFLOPS = 157.3   # MI355X FP32 vector, vendor figure
 PEAK_FP64_TFLOPS = 78.6    # MI355X FP64 vector
+PEAK_HBM_GBPS = 8000.0     # MI355X HBM3E
+# Non-packed FP32 wave64 VALU instructions issued per SIMD per cycle, measured
+# with standalone FMA streams on this chip (about 129 TFLOP/s of FMAs over 1024
+# SIMDs at 2.4 GHz): the ceiling for code built without packed FP32.
+VALU_ISSUE_CEILING = 0.41
+SIMDS = 256 * 4
+CLOCK_HZ = 2.4e9
 METRIC = "rows/sec for SHAP values and SHAP interaction values; % FP32 VALU peak"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2010_13972_amd", "csrc", "gts_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2010_13972_amd", "csrc")
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in (
+    "gts_shap_kernel.h", "gts_launch.h", "gts_kernels.hip", "gts_shap_f32.hip",
+    "gts_shap_f64.hip", "gts_inter_f32.hip", "gts_inter_f64.hip")]
 
 WORKLOAD_TEXT = {
     "tiny": "tiny: 10 full depth-3 trees, M=8, X~U[0,1), 256 rows",
@@ -63,51 +78,72 @@ SUITE = [
     ("interactions_f32", "interactions", "f32", True),
 ]
 
-# HBM traffic of the SHAP kernel per launch, from rocprofv3 --pmc FETCH_SIZE
-# and --pmc WRITE_SIZE runs of `bench.py --copy-probe`, each scaled by the
-# ratio of a plain 256 MiB copy's true bytes to the counter's reading of it.
-# Keyed by (workload, dtype, interactions); `source` is kernel_source_hash()
-# of the kernel source the counters were taken on.
-TRAFFIC = {
-    ("covtype_med", "f32", False): {"fetch_bytes": 19415185, "write_bytes": 35200000,
-        "source": "0ba3e6c82051609eb77578e2217aa7bac2fc7b1466dfadea0b59a752aaed02e4"},
-    ("interactions", "f32", True): {"fetch_bytes": 22601788, "write_bytes": 61987758,
-        "source": "0ba3e6c82051609eb77578e2217aa7bac2fc7b1466dfadea0b59a752aaed02e4"},
-    ("deep", "f32", False): {"fetch_bytes": 63880290, "write_bytes": 46080000,
-        "source": "0ba3e6c82051609eb77578e2217aa7bac2fc7b1466dfadea0b59a752aaed02e4"},
-    ("deep", "f64", False): {"fetch_bytes": 73830175, "write_bytes": 92160000,
-        "source": "0ba3e6c82051609eb77578e2217aa7bac2fc7b1466dfadea0b59a752aaed02e4"},
-    ("wide", "f32", False): {"fetch_bytes": 5945953179, "write_bytes": 316800082,
-        "source": "0ba3e6c82051609eb77578e2217aa7bac2fc7b1466dfadea0b59a752aaed02e4"},
-}
+# rocprofv3 counters of the SHAP kernel per launch, keyed by (workload, dtype,
+# interactions); `source` is kernel_source_hash() of the kernel sources the
+# counters were taken on.  fetch_bytes / write_bytes: FETCH_SIZE and
+# WRITE_SIZE, each scaled by the ratio of a plain 256 MiB copy's true bytes to
+# the counter's reading of it.  valu_insts / salu_insts / lds_insts:
+# SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
+# summaries and the commands that made them are in profiles/.
+COUNTERS = {}
 
 
 def kernel_source_hash() -> str:
-    """SHA-256 of the kernel source's code: line comments and blank lines are
-    dropped, so editing a comment keeps the measured traffic."""
+    """SHA-256 of the kernel sources' code: line comments and blank lines are
+    dropped, so editing a comment keeps the measured counters."""
     code = []
-    with open(KERNEL_SOURCE) as f:
-        for line in f:
-            c = line.split("//", 1)[0].rstrip()
-            if c.strip():
-                code.append(c)
+    for path in KERNEL_SOURCES:
+        with open(path) as f:
+            for line in f:
+                c = line.split("//", 1)[0].rstrip()
+                if c.strip():
+                    code.append(c)
     return hashlib.sha256("\n".join(code).encode()).hexdigest()
 
 
-def traffic_for(key):
-    t = TRAFFIC.get(key)
-    if t is None or t["source"] != kernel_source_hash():
+def counters_for(key):
+    c = COUNTERS.get(key)
+    if c is None or c["source"] != kernel_source_hash():
         return None
-    return t["fetch_bytes"] + t["write_bytes"]
+    return c
 
 
-def modelled_flops(q: np.ndarray, interactions: bool) -> float:
-    """Per row: the op model summed over the extracted paths."""
+def traffic_for(key):
+    c = counters_for(key)
+    return None if c is None else c["fetch_bytes"] + c["write_bytes"]
+
+
+def executed(key, kernel_ms: float):
+    """Counter-derived rates of the kernel: HBM GB/s from FETCH_SIZE +
+    WRITE_SIZE, VALU lane operations (instructions x 64) and the VALU issue
+    rate per SIMD-cycle, also as a fraction of the measured non-packed
+    ceiling."""
+    c = counters_for(key)
+    if c is None:
+        return None
+    s = kernel_ms * 1e-3
+    issue = c["valu_insts"] / (s * SIMDS * CLOCK_HZ)
+    return {"hbm_gbps": (c["fetch_bytes"] + c["write_bytes"]) / s / 1e9,
+            "hbm_frac": (c["fetch_bytes"] + c["write_bytes"]) / s / 1e9 / PEAK_HBM_GBPS,
+            "valu_lane_ops_per_launch": 64 * c["valu_insts"],
+            "valu_issue_per_simd_cycle": issue,
+            "valu_issue_frac_of_ceiling": issue / VALU_ISSUE_CEILING,
+            "salu_insts_per_launch": c["salu_insts"], "lds_insts_per_launch": c["lds_insts"],
+            "counters_source": c["source"][:16]}
+
+
+def op_model(q: np.ndarray, interactions: bool) -> np.ndarray:
+    """Flops per (row, path) for paths of q features."""
     q = q.astype(np.float64)
     f = 10 * q * q + 8 * q
     if interactions:
         f = f + q * (q - 1) * (10 * q + 4)
-    return float(f.sum())
+    return f
+
+
+def modelled_flops(q: np.ndarray, interactions: bool) -> float:
+    """Per row: the op model summed over the extracted paths."""
+    return float(op_model(q, interactions).sum())
 
 
 def path_features(gts, ens) -> np.ndarray:
@@ -116,28 +152,88 @@ def path_features(gts, ens) -> np.ndarray:
     return np.diff(np.append(roots, len(el))) - 1
 
 
+def live_pairs(torch, gts, ens, X: np.ndarray, dtype: str, tile: int = 64, dev: str = "cuda"):
+    """Exact count of the live (row, path) pairs: a pair is dead when the path
+    has an element whose zero fraction is 0 (in the model's precision) and
+    whose range [lower, upper) misses the row -- its weight polynomial has a
+    factor z + o t = 0 and it contributes exactly nothing.  Counted on the
+    device (torch), per path: live rows, and live tiles of `tile` rows.
+    Returns (q per path, live rows per path, live tiles per path)."""
+    el, _, _ = gts.extract_paths(ens)
+    roots = np.flatnonzero(el["feature_idx"] == -1)
+    P = len(roots)
+    q = np.diff(np.append(roots, len(el))) - 1
+    rows = X.shape[0]
+    ntiles = (rows + tile - 1) // tile
+    live_rows = np.full(P, rows, np.int64)
+    live_tiles = np.full(P, ntiles, np.int64)
+    z = el["zero_fraction"].astype(np.float32 if dtype == "f32" else np.float64)
+    zero = (z == 0) & (el["feature_idx"] >= 0)
+    if not zero.any() or rows == 0:
+        return q, live_rows, live_tiles
+    path_of = np.cumsum(el["feature_idx"] == -1) - 1
+    zi = np.flatnonzero(zero)
+    zp = path_of[zi]
+    counts = np.bincount(zp, minlength=P)
+    K = int(counts.max())
+    # [P, K] padded with an always-true element
+    rank = np.arange(len(zi)) - np.searchsorted(zp, zp)   # zi is sorted by path
+    F = np.zeros((P, K), np.int64)
+    Lo = np.full((P, K), -np.inf, np.float32)
+    Hi = np.full((P, K), np.inf, np.float32)
+    F[zp, rank] = el["feature_idx"][zi]
+    Lo[zp, rank] = el["lower"][zi]
+    Hi[zp, rank] = el["upper"][zi]
+    has = np.flatnonzero(counts > 0)
+    Xt = torch.from_numpy(np.ascontiguousarray(X.T, np.float32)).to(dev)   # [M, rows]
+    pad = ntiles * tile - rows
+    chunk = max(1, (1 << 28) // max(1, K * rows))
+    for a in range(0, len(has), chunk):
+        idx = has[a:a + chunk]
+        f = torch.from_numpy(F[idx]).to(dev)
+        lo = torch.from_numpy(Lo[idx]).to(dev)[..., None]
+        hi = torch.from_numpy(Hi[idx]).to(dev)[..., None]
+        vals = Xt[f]                                              # [C, K, rows]
+        ok = ((lo <= vals) & (vals < hi)).all(dim=1)              # [C, rows]
+        live_rows[idx] = ok.sum(dim=1).cpu().numpy()
+        if pad:
+            ok = torch.nn.functional.pad(ok, (0, pad))
+        live_tiles[idx] = ok.view(len(idx), ntiles, tile).any(dim=2).sum(dim=1).cpu().numpy()
+    return q, live_rows, live_tiles
+
+
+def work_model(torch, gts, ens, X, dtype, interactions):
+    """Algorithmic flops of one launch over X: the op model over the live
+    (row, path) pairs, and over all pairs (dense equivalent)."""
+    q, lr, lt = live_pairs(torch, gts, ens, X, dtype)
+    f = op_model(q, interactions)
+    rows = X.shape[0]
+    return {"flops_live": float((f * lr).sum()), "flops_dense": float(f.sum() * rows),
+            "pairs": int(len(q)) * rows, "live_pairs": int(lr.sum()),
+            "tile_pairs": int(len(q)) * int(-(-rows // 64)), "live_tile_pairs": int(lt.sum()),
+            "paths": int(len(q)), "path_elements": int((q + 1).sum())}
+
+
 def kernel_fn(gts, interactions):
     return gts.shap_interactions if interactions else gts.shap
 
 
 NBUF = 3      # model buffers in flight in the pipelined steps
-NSTREAMS = 2  # compute streams the steps alternate between
 
 
-def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=NSTREAMS):
+def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1):
     """Whole-path steps, pipelined.  Step k prepares its model on the host
     (gts_prepare_model into pinned buffer k mod 3) and a copy stream uploads
     it into device buffer k mod 3; its kernel is launched after step k+1's
-    model has been prepared and its upload issued, on compute stream k mod 2
-    into output buffer k mod 2.  Consecutive steps are independent batches,
-    so one step's kernel can fill the CUs that the previous one's last
-    workgroups leave idle.  The host orders buffer reuse (it waits for the
-    upload that last read a pinned buffer, and for the kernel that last read
-    a device buffer), so the compute streams hold only kernels and no
-    cross-stream waits.  The loop calls the C ABI with arguments marshalled
-    once (the ensemble struct, descriptors, buffer pointers), so the step
-    measures the library rather than Python wrappers.  Timed on the host
-    clock; each kernel is bracketed by HIP events on its stream."""
+    model has been prepared and its upload issued, on compute stream
+    k mod nstreams into output buffer k mod nstreams.  The host orders buffer
+    reuse (it waits for the upload that last read a pinned buffer, and for the
+    kernel that last read a device buffer), so the compute streams hold only
+    kernels and no cross-stream waits.  The loop calls the C ABI with
+    arguments marshalled once (the ensemble struct, descriptors, buffer
+    pointers), so the step measures the library rather than Python wrappers.
+    Timed on the host clock; each kernel is bracketed by HIP events on its
+    stream."""
     import ctypes
     L = gts.lib()
     launch = L.gts_shap_interactions if interactions else L.gts_shap
@@ -204,6 +300,15 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                 launch_kernel(k - 1, timed)
         launch_kernel(n - 1, timed)
 
+    # untimed: a few preparations and back-to-back launches bring the host
+    # threads and the GPU clocks up before the warm-up steps
+    for _ in range(2):
+        L.gts_prepare_model(*prep_args[0])
+    ref_model = gts.prepare(ens, dtype)
+    fn = kernel_fn(gts, interactions)
+    for _ in range(5):
+        fn(ref_model, Xd, out=outs[0])
+    torch.cuda.synchronize()
     run_steps(warmup, False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -211,9 +316,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     kern = np.array([a.elapsed_time(b) for a, b in ev])
-    # the last step's output against a model prepared the ordinary way
-    model = gts.prepare(ens, dtype)
-    return wall, kern, outs[(steps - 1) % nstreams], model, np.array(host_ms)
+    return wall, kern, outs[(steps - 1) % nstreams], ref_model, np.array(host_ms)
 
 
 def time_kernel(torch, gts, model, Xd, reps, interactions):
@@ -255,7 +358,7 @@ def time_device_extract(torch, gts, ens, reps=5):
     node arrays), wall clock per call including its two count read-backs;
     gts_extract_paths on the host for comparison."""
     dens = gts.DeviceEnsemble(ens)
-    raw, _, _ = gts.extract_paths_device(dens)
+    gts.extract_paths_device(dens)
     torch.cuda.synchronize()
     dev, host = [], []
     for _ in range(reps):
@@ -269,25 +372,71 @@ def time_device_extract(torch, gts, ens, reps=5):
     return 1e3 * float(np.median(dev)), 1e3 * float(np.median(host))
 
 
-def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
+def cpu_threads() -> int:
+    threads = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS")
+    if env and env.isdigit():
+        threads = min(threads, int(env))
+    return threads
+
+
+def oracle_rate(oracle, ens, X, budget_s: float, interactions: bool, nthreads: int):
+    """The oracle on a row prefix grown until one call takes about budget_s,
+    or the whole batch repeated until that much time has passed: (rows per
+    second, rows in the prefix, passes, seconds)."""
+    fn = oracle.interactions if interactions else oracle.treeshap
+    n = 4 if interactions else 16
+    while True:
+        n = min(n, X.shape[0])
+        t0 = time.perf_counter()
+        fn(ens, X[:n], nthreads=nthreads)
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or n == X.shape[0]:
+            break
+        n = min(X.shape[0], max(n + 1, int(n * 1.05 * budget_s / max(dt, 1e-3))))
+    passes = 1
+    if dt < budget_s:
+        passes = max(1, int(np.ceil(budget_s / max(dt, 1e-3))))
+        t0 = time.perf_counter()
+        for _ in range(passes):
+            fn(ens, X[:n], nthreads=nthreads)
+        dt = time.perf_counter() - t0
+    return n * passes / dt, n, passes, dt
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def suite_entry(torch, gts, synth, oracle, workload, dtype, interactions, reps, oracle_s):
     w = synth.workload(workload)
     ens = w.ensemble
     rows = w.X.shape[0]
     Xd = torch.from_numpy(w.X).cuda()
-    q = path_features(gts, ens)
     host_ms, upload_ms, blob_bytes = time_prepare(gts, ens, dtype)
     dev_extract_ms, host_extract_ms = time_device_extract(torch, gts, ens)
     model = gts.prepare(ens, dtype)
     k = time_kernel(torch, gts, model, Xd, reps, interactions)
     med = float(np.median(k))
-    flops = modelled_flops(q, interactions) * rows
+    wm = work_model(torch, gts, ens, w.X, dtype, interactions)
     peak = PEAK_FP64_TFLOPS if dtype == "f64" else PEAK_FP32_TFLOPS
-    achieved = flops / (med * 1e-3) / 1e12
-    return {
+    achieved = wm["flops_live"] / (med * 1e-3) / 1e12
+    dense = wm["flops_dense"] / (med * 1e-3) / 1e12
+    entry = {
         "workload": WORKLOAD_TEXT[workload], "dtype": dtype, "rows": rows,
         "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
                    + (f", {ens.num_features + 1}]" if interactions else "]")),
-        "paths": int(len(q)), "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
+        "paths": wm["paths"], "path_elements": wm["path_elements"],
+        "bins": int(model.num_bins),
+        "live_pair_fraction": wm["live_pairs"] / max(1, wm["pairs"]),
+        "live_tile_fraction": wm["live_tile_pairs"] / max(1, wm["tile_pairs"]),
         "launch": gts.launch_config(model, rows, interactions),
         "host_prepare_ms": host_ms, "upload_ms": upload_ms, "model_bytes": blob_bytes,
         "extract_ms_device": dev_extract_ms, "extract_ms_host": host_extract_ms,
@@ -296,58 +445,32 @@ def suite_entry(torch, gts, synth, workload, dtype, interactions, reps):
         "kernel_rows_per_s": rows / (med * 1e-3),
         "end_to_end_rows_per_s": rows / ((host_ms + upload_ms + med) * 1e-3),
         "modelled_tflops": achieved, "peak_tflops": peak, "frac": achieved / peak,
+        "dense_equivalent_tflops": dense,
         "traffic_bytes": traffic_for((workload, dtype, interactions)),
+        "executed": executed((workload, dtype, interactions), med),
     }
+    if oracle is not None and oracle_s > 0:
+        threads = cpu_threads()
+        rate, n, passes, dt = oracle_rate(oracle, ens, w.X, oracle_s, interactions, threads)
+        entry["oracle_rows_per_s"] = rate
+        entry["oracle"] = {"cores": threads, "sample": f"first {n} of {rows} rows x {passes} "
+                           f"pass(es) in {dt:.2f} s, fp64, OpenMP over rows"}
+    return entry
 
 
 def cpu_baseline(oracle, ens, X, budget_s: float, interactions: bool):
     """The oracle as it stands, on all usable cores, on a bounded sample of
-    the batch: a row prefix grown until one call takes about budget_s / 2, or
-    the whole batch repeated until that much time has passed; then on one
-    thread for about budget_s / 4."""
-    threads = len(os.sched_getaffinity(0))
-    env = os.environ.get("OMP_NUM_THREADS")
-    if env and env.isdigit():
-        threads = min(threads, int(env))
-    fn = oracle.interactions if interactions else oracle.treeshap
-
-    def run(nthreads, target):
-        n = 8 if interactions else 64
-        while True:
-            n = min(n, X.shape[0])
-            t0 = time.perf_counter()
-            fn(ens, X[:n], nthreads=nthreads)
-            dt = time.perf_counter() - t0
-            if dt >= target or n == X.shape[0]:
-                break
-            n = min(X.shape[0], max(n + 1, int(n * 1.05 * target / max(dt, 1e-3))))
-        passes = 1
-        if dt < target:
-            passes = max(1, int(np.ceil(target / max(dt, 1e-3))))
-            t0 = time.perf_counter()
-            for _ in range(passes):
-                fn(ens, X[:n], nthreads=nthreads)
-            dt = time.perf_counter() - t0
-        return n, passes, dt
-
-    n, passes, dt = run(threads, budget_s / 2)
-    n1, passes1, dt1 = run(1, budget_s / 4)
-    cpu = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    cpu = line.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
+    the batch (about budget_s / 2), then on one thread (about budget_s / 4)."""
+    threads = cpu_threads()
+    rate, n, passes, dt = oracle_rate(oracle, ens, X, budget_s / 2, interactions, threads)
+    rate1, n1, passes1, dt1 = oracle_rate(oracle, ens, X, budget_s / 4, interactions, 1)
     what = "conditioning interactions" if interactions else "Algorithm 1"
-    return {"value": n * passes / dt, "unit": "rows/s", "cores": threads, "kind": "oracle",
+    return {"value": rate, "unit": "rows/s", "cores": threads, "kind": "oracle",
             "sample": f"first {n} of {X.shape[0]} rows x {passes} pass(es) in {dt:.2f} s, fp64 "
                       f"{what}, OpenMP over rows",
-            "one_thread_value": n1 * passes1 / dt1,
+            "one_thread_value": rate1,
             "one_thread_sample": f"first {n1} rows x {passes1} pass(es) in {dt1:.2f} s",
-            "cpu": cpu}
+            "cpu": cpu_model()}
 
 
 def copy_probe(torch):
@@ -360,6 +483,21 @@ def copy_probe(torch):
     torch.neg(src, out=dst)
     torch.cuda.synchronize()
     return n * 4
+
+
+def profile_launches(torch, gts, synth, workload, dtype, launches):
+    """Only the kernel of one workload, `launches` times back to back (for
+    rocprofv3 counter and trace runs)."""
+    w = synth.workload(workload)
+    inter = workload == "interactions"
+    model = gts.prepare(w.ensemble, dtype)
+    Xd = torch.from_numpy(w.X).cuda()
+    fn = kernel_fn(gts, inter)
+    out = fn(model, Xd)
+    for _ in range(launches - 1):
+        fn(model, Xd, out=out)
+    torch.cuda.synchronize()
+    print(json.dumps({"profiled": workload, "dtype": dtype, "launches": launches}), flush=True)
 
 
 # ---------------------------------------------------------------------------
@@ -416,10 +554,7 @@ def experiment_rows(torch, gts, synth, oracle, workloads, cpu_limit_s):
     device-resident rows (HIP events), and host to host (upload of X from
     pinned memory, kernel, download of phi), median of several calls.  CPU: the
     oracle on all cores while one call stays under cpu_limit_s."""
-    threads = len(os.sched_getaffinity(0))
-    env = os.environ.get("OMP_NUM_THREADS")
-    if env and env.isdigit():
-        threads = min(threads, int(env))
+    threads = cpu_threads()
     out = {"experiment": "rows", "cpu_threads": threads, "sweeps": []}
     for wl in workloads:
         w = synth.workload(wl)
@@ -480,9 +615,9 @@ def experiment_rows(torch, gts, synth, oracle, workloads, cpu_limit_s):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="covtype_med",
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="deep",
                     choices=["tiny", "covtype_med", "deep", "wide", "interactions"],
                     help="the batch one step explains (interactions: the interaction kernel "
                          "on the covtype-shaped model)")
@@ -491,6 +626,8 @@ def main():
     ap.add_argument("--no-suite", action="store_true",
                     help="skip the per-workload suite (kernel and preparation of every workload)")
     ap.add_argument("--suite-reps", type=int, default=10)
+    ap.add_argument("--suite-oracle-s", type=float, default=2.0,
+                    help="seconds of oracle time per suite workload (0: none)")
     ap.add_argument("--cpu-budget", type=float, default=16.0,
                     help="seconds of oracle time for the CPU baseline (about half on all "
                          "cores, a quarter on one thread)")
@@ -500,10 +637,12 @@ def main():
                          "sweep (Fig. 4)")
     ap.add_argument("--sweep-workloads", default="covtype_med,deep,interactions")
     ap.add_argument("--cpu-limit", type=float, default=4.0)
-    ap.add_argument("--streams", type=int, default=NSTREAMS,
+    ap.add_argument("--streams", type=int, default=1,
                     help="compute streams the pipelined steps alternate between")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
+    ap.add_argument("--profile-launches", type=int, default=0,
+                    help="only launch the kernel of --workload this many times (rocprofv3)")
     args = ap.parse_args()
     if args.steps < 1 or args.warmup < 0 or args.streams < 1:
         ap.error("--steps and --streams must be at least 1, --warmup at least 0")
@@ -523,6 +662,10 @@ def main():
 
     if args.copy_probe:
         copy_probe(torch)
+    if args.profile_launches:
+        profile_launches(torch, gts, synth, args.workload,
+                         args.dtype or synth.workload(args.workload).dtype, args.profile_launches)
+        return
 
     if args.experiment == "packers":
         print(json.dumps(experiment_packers(torch, gts, synth, args.suite_reps)), flush=True)
@@ -540,7 +683,6 @@ def main():
     ens = w.ensemble
     rows = w.X.shape[0]
     Xd = torch.from_numpy(w.X).cuda()
-    q = path_features(gts, ens)
 
     wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
                                                       args.warmup, inter, args.streams)
@@ -551,17 +693,14 @@ def main():
     rel = float((out - ref).abs().max() / (ref.abs().max() + 1e-30))
     if not rel < 1e-4:
         raise SystemExit(f"pipelined steps disagree with gts.shap: relative difference {rel:.3g}")
-    # The roofline takes the kernel's mean launch duration from back-to-back
-    # launches (each bracketed by HIP events on its stream), a timed region of
-    # its own right after the steps.  Inside the whole-path steps the GPU
-    # often waits for the host between the start event and the launch, so
-    # there the events also hold host launch latency (a few percent; the
-    # kernel trace shows the kernel itself within about 1 % of back to back).
-    k_only = time_kernel(torch, gts, model, Xd, max(5, args.steps), inter)
-    kern_ms = float(k_only.mean())
-    flops = modelled_flops(q, inter) * rows
+    # roofline: the kernel's launches inside the timed steps (events on its
+    # stream); back-to-back launches in a timed region of their own as well
+    kern_ms = float(kern.mean())
+    k_only = time_kernel(torch, gts, model, Xd, max(5, min(args.steps, 50)), inter)
+    wm = work_model(torch, gts, ens, w.X, dtype, inter)
     peak = PEAK_FP64_TFLOPS if dtype == "f64" else PEAK_FP32_TFLOPS
-    achieved = flops / (kern_ms * 1e-3) / 1e12
+    achieved = wm["flops_live"] / (kern_ms * 1e-3) / 1e12
+    key = (args.workload, dtype, inter)
     line = {
         "metric": METRIC,
         "value": rows * args.steps / wall, "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
@@ -569,8 +708,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
         "data": "synthetic (seeded ensembles and rows shaped like the paper's models)",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "rows": rows,
-                   "trees": int(ens.num_trees), "paths": int(len(q)),
-                   "path_elements": int((q + 1).sum()), "bins": int(model.num_bins),
+                   "trees": int(ens.num_trees), "paths": wm["paths"],
+                   "path_elements": wm["path_elements"], "bins": int(model.num_bins),
                    "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
                               + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": "extract + merge + bias + BFD pack (B=64) + layout (host) + upload "
@@ -579,30 +718,39 @@ def main():
                    "compute_streams": args.streams},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
-                     "traffic": traffic_for((args.workload, dtype, inter)),
+                     "traffic": traffic_for(key),
                      "kernel": "shap_kernel" + (" (interactions)" if inter else ""),
                      "kernel_ms": kern_ms,
-                     "kernel_ms_in_steps": float(kern.mean()),
+                     "kernel_launches": int(len(kern)),
+                     "kernel_ms_back_to_back": float(k_only.mean()),
+                     "modelled_gflop_per_launch": wm["flops_live"] / 1e9,
+                     "live_pair_fraction": wm["live_pairs"] / max(1, wm["pairs"]),
+                     "live_tile_fraction": wm["live_tile_pairs"] / max(1, wm["tile_pairs"]),
+                     "dense_equivalent_tflops": wm["flops_dense"] / (kern_ms * 1e-3) / 1e12,
+                     "executed": executed(key, kern_ms),
                      "host_prepare_ms_in_steps": float(np.median(step_host)),
                      "host_prepare_ms_in_steps_mean": float(step_host.mean()),
                      "host_prepare_ms_in_steps_p90": float(np.percentile(step_host, 90)),
-                     "modelled_gflop_per_launch": flops / 1e9,
-                     "note": "peak is the packed-FP32 vendor figure; non-packed FP32 FMAs "
-                             "measured about 129 TFLOP/s on this chip. kernel_ms: back-to-back "
-                             "launches on one stream; kernel_ms_in_steps: event spans of the "
-                             "pipelined steps' launches, which on two streams overlap the "
-                             "other stream's kernel"},
+                     "note": "achieved: op model over the live (row, path) pairs (a pair "
+                             "whose zero-cover element misses the row contributes exactly "
+                             "0) / mean in-step launch time; peak is the packed-FP32 vendor "
+                             "figure (non-packed FP32 FMAs measured about 129 TFLOP/s); "
+                             "dense_equivalent_tflops counts every pair"},
         "launch": gts.launch_config(model, rows, inter),
         "kernel": {"rows_per_s": rows / (float(np.median(k_only)) * 1e-3),
                    "ms_median": float(np.median(k_only)), "ms_mean": float(k_only.mean()),
                    "ms_std": float(k_only.std()), "runs": len(k_only)},
     }
-    if not args.no_suite:
-        line["configs"] = {name: suite_entry(torch, gts, synth, wl, dt, inter, args.suite_reps)
-                           for name, wl, dt, inter in SUITE}
-    if not args.no_cpu_baseline:
+    orc = None
+    if not args.no_cpu_baseline or args.suite_oracle_s > 0:
         import oracle
-        line["cpu_baseline"] = cpu_baseline(oracle, ens, w.X, args.cpu_budget, inter)
+        orc = oracle
+    if not args.no_suite:
+        line["configs"] = {name: suite_entry(torch, gts, synth, orc, wl, dt, it,
+                                             args.suite_reps, args.suite_oracle_s)
+                           for name, wl, dt, it in SUITE}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(orc, ens, w.X, args.cpu_budget, inter)
     print(json.dumps(line), flush=True)
 
 
