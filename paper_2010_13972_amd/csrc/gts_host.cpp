@@ -225,7 +225,6 @@ struct Walker {
   std::vector<float> upper;     // [M]
   std::vector<double> zf;       // [M]
   std::vector<int32_t> active;  // features with count > 0, ascending
-  std::vector<Split> merged;    // the current leaf's merged elements
   std::vector<unsigned char> seen;
   bool clean = false;
 
@@ -282,10 +281,22 @@ struct Walker {
     }
   }
 
+  // The current leaf's m merged elements, in ascending feature order, into
+  // dst[0..m); returns the product of their zero fractions (a left fold in
+  // that order).
+  double emit(Split* dst) const {
+    double prod = 1.0;
+    for (size_t i = 0; i < active.size(); ++i) {
+      const size_t f = (size_t)active[i];
+      dst[i] = Split{active[i], lower[f], upper[f], zf[f]};
+      prod = prod * zf[f];
+    }
+    return prod;
+  }
+
   // Depth-first walk of tree t, left child (x < t) first, validating every
-  // node it reaches.  Calls leaf(node, m) with m merged elements; with EMIT
-  // they are in merged[0..m), in ascending feature order (without EMIT only
-  // m is computed).  The stack holds nodes still to visit, each with the
+  // node it reaches.  Calls leaf(node, m) with m merged elements (with EMIT,
+  // emit() gives them; without EMIT only m is computed).  The stack holds nodes still to visit, each with the
   // split that leads to it and the undo depth of its parent's path: a visit
   // first unwinds the path to that depth, then enters the split.
   template <bool EMIT, typename LeafFn>
@@ -315,15 +326,7 @@ struct Walker {
       if (a < 0 && b < 0) {
         if (!std::isfinite(e->value[gi]))
           return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
-        const size_t m = active.size();
-        if (EMIT) {
-          merged.resize(m);
-          for (size_t i = 0; i < m; ++i) {
-            const size_t f = (size_t)active[i];
-            merged[i] = Split{active[i], lower[f], upper[f], zf[f]};
-          }
-        }
-        leaf(node, m);
+        leaf(node, active.size());
         continue;
       }
       if (a < 0 || b < 0 || a >= n || b >= n)
@@ -469,13 +472,12 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
       int64_t k = tree_elems[(size_t)t];
       int64_t p = tree_paths[(size_t)t];
       const float inf = std::numeric_limits<float>::infinity();
+      static thread_local std::vector<Split> merged;
+      if (merged.size() < (size_t)ens->num_features) merged.resize((size_t)ens->num_features);
       return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
-        if (bias) {
-          double prod = 1.0;
-          for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
-          term[(size_t)p] = v * prod;
-        }
+        const double prod = w.emit(merged.data());
+        if (bias) term[(size_t)p] = v * prod;
         if (out) {
           gts_path_element* el = out + k;
           el[0].path_idx = p;
@@ -486,7 +488,7 @@ gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
           el[0].zero_fraction = 1.0;
           el[0].v = v;
           for (size_t i = 0; i < m; ++i) {
-            const Split& s = w.merged[i];
+            const Split& s = merged[i];
             el[i + 1].path_idx = p;
             el[i + 1].feature_idx = s.feature;
             el[i + 1].group = group;
@@ -914,13 +916,17 @@ inline void put_element(const gts_model& m, char* blob, int64_t i, int32_t feat,
 // features at a position where an earlier path of the bin already has the
 // same feature.
 //
+// When every launch of the model runs one path per wave (rotate false), the
+// order decides no collisions and the remaining elements keep their feature
+// order.
+//
 // f, z: the path's q feature elements in ascending feature order (z in the
 // blob's precision); used[f] has bit k set when an earlier path of the bin
 // stores feature f at position k.  Writes order[k] = the source index stored
 // at position k and returns the number of zero-fraction elements.
 template <typename Z>
 int32_t device_order(const int32_t* f, const Z* z, int32_t q, int32_t t_in_bin,
-                     const uint64_t* used, int32_t* order) {
+                     const uint64_t* used, bool rotate, int32_t* order) {
   int32_t n0 = 0;
   for (int32_t j = 0; j < q; ++j)
     if (z[j] == Z(0)) order[n0++] = j;
@@ -929,7 +935,7 @@ int32_t device_order(const int32_t* f, const Z* z, int32_t q, int32_t t_in_bin,
   for (int32_t j = 0; j < q; ++j)
     if (z[j] != Z(0)) rest[nr++] = j;
   int32_t best = 0;
-  if (nr > 1) {
+  if (rotate && nr > 1) {
     // cost[rho]: collisions if rest element i goes to position
     // n0 + (i - rho) mod nr
     int32_t cost[kMaxPathLen];
@@ -965,7 +971,7 @@ int32_t device_order(const int32_t* f, const Z* z, int32_t q, int32_t t_in_bin,
 // Applies device_order to the paths of one bin of a blob written in packed
 // order (root first, features ascending), in place.
 template <typename Z>
-void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t a1,
+void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t a1, bool rotate,
                 std::vector<uint64_t>& used, std::vector<int32_t>& touched) {
   Z zbuf[kMaxPathLen];
   float lbuf[kMaxPathLen], hbuf[kMaxPathLen];
@@ -976,7 +982,7 @@ void rotate_bin(int32_t* feat, float* lo, float* hi, Z* zf, int64_t a0, int64_t 
     int64_t e = a + 1;
     while (e < a1 && feat[e] >= 0) ++e;
     const int32_t q = (int32_t)(e - a - 1);
-    const int32_t n0 = device_order(feat + a + 1, zf + a + 1, q, t, used.data(), order);
+    const int32_t n0 = device_order(feat + a + 1, zf + a + 1, q, t, used.data(), rotate, order);
     for (int32_t k = 0; k < q; ++k) {
       const int64_t src = a + 1 + order[k];
       fbuf[k] = feat[src];
@@ -1007,6 +1013,7 @@ void rotate_bins(const gts_model& m, char* blob, const int64_t* bin_offsets) {
   float* lo = reinterpret_cast<float*>(blob + m.off[kLower]);
   float* hi = reinterpret_cast<float*>(blob + m.off[kUpper]);
   const int64_t K = m.num_bins;
+  const bool rotate = !one_path_per_wave(m.num_features, m.dtype);
   std::atomic<int64_t> next{0};
   const int nthreads = host_threads(m.num_elements);
   // about eight chunks a thread, at most 64 bins each
@@ -1021,10 +1028,10 @@ void rotate_bins(const gts_model& m, char* blob, const int64_t* bin_offsets) {
       for (int64_t b = b0; b < b1; ++b) {
         if (m.dtype == GTS_F64)
           rotate_bin(feat, lo, hi, reinterpret_cast<double*>(blob + m.off[kZero]), bin_offsets[b],
-                     bin_offsets[b + 1], used, touched);
+                     bin_offsets[b + 1], rotate, used, touched);
         else
           rotate_bin(feat, lo, hi, reinterpret_cast<float*>(blob + m.off[kZero]), bin_offsets[b],
-                     bin_offsets[b + 1], used, touched);
+                     bin_offsets[b + 1], rotate, used, touched);
       }
     }
   });
@@ -1189,24 +1196,34 @@ struct alignas(128) TreeOut {
   }
 };
 
+// A path as the blob writer reads it: its feature-sorted merged elements (in
+// its tree's buffer), leaf value and feature count, and, once placed, its
+// element offset inside its bin.
+struct PathSrc {
+  const Split* el;
+  double v;
+  int32_t q;
+  int32_t within;
+};
+
 // Working arrays of gts_prepare_model, kept per calling thread between calls
 // so that repeated preparations reuse their memory.
 struct PrepareScratch {
   std::vector<TreeOut> trees;
-  std::vector<int64_t> tree_first, path_tree, chunk_start, key_start, by_bin;
+  std::vector<int64_t> tree_first, chunk_start, key_start;
   std::vector<int32_t> size_at, key, grank, group_of_rank;
+  std::vector<PathSrc> src_at, src_by_bin;   // per placement; per bin slot
   Packing pk;
 };
 
 // Writes the paths of bin b into the blob, in the device order of
 // device_order (the choices rotate_bin makes, taken from the feature-sorted
-// source).  by_bin[bin_first[b] ..]: the placements of bin b in placement
-// order.
+// source).  src[bin_first[b] ..]: the paths of bin b in placement order;
+// src has P entries, of which the writer prefetches a few ahead.
 template <typename Z>
-void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees,
-               const int64_t* path_tree, const int64_t* tree_first, const Packing& pk,
-               const int64_t* by_bin, int64_t b, std::vector<uint64_t>& used,
-               std::vector<int32_t>& touched) {
+void write_bin(const gts_model& m, char* blob, const Packing& pk, const PathSrc* src, int64_t P,
+               int64_t b, std::vector<uint64_t>& used, std::vector<int32_t>& touched) {
+  constexpr int64_t kAhead = 4;
   const float inf = std::numeric_limits<float>::infinity();
   int32_t* const feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]);
   float* const lower = reinterpret_cast<float*>(blob + m.off[kLower]);
@@ -1217,26 +1234,29 @@ void write_bin(const gts_model& m, char* blob, const std::vector<TreeOut>& trees
   Z zs[kMaxPathLen];
   int32_t t_in_bin = 0;
   const int64_t base = pk.bin_offsets[(size_t)b];
+  const bool rotate = !one_path_per_wave(m.num_features, m.dtype);
   for (int64_t i = pk.bin_first[(size_t)b]; i < pk.bin_first[(size_t)b + 1]; ++i, ++t_in_bin) {
-    const int64_t k = by_bin[i];
-    const int64_t p = pk.order[(size_t)k];
-    const int64_t t = path_tree[p];
-    const TreeOut& tr = trees[(size_t)t];
-    const size_t j = (size_t)(p - tree_first[t]);
-    const Split* src = tr.el.data() + tr.first[j];
-    const int32_t q = tr.size[j] - 1;
-    const int64_t d = base + pk.within_at[(size_t)k];
-    for (int32_t jj = 0; jj < q; ++jj) {
-      fs[jj] = src[jj].feature;
-      zs[jj] = (Z)src[jj].zero_fraction;
+    if (i + kAhead < P) {
+      const char* ahead = reinterpret_cast<const char*>(src[i + kAhead].el);
+      __builtin_prefetch(ahead);
+      __builtin_prefetch(ahead + 64);
+      __builtin_prefetch(ahead + 128);
     }
-    const int32_t n0 = device_order(fs, zs, q, t_in_bin, u, order);
+    const PathSrc& ps = src[i];
+    const Split* el = ps.el;
+    const int32_t q = ps.q;
+    const int64_t d = base + ps.within;
+    for (int32_t jj = 0; jj < q; ++jj) {
+      fs[jj] = el[jj].feature;
+      zs[jj] = (Z)el[jj].zero_fraction;
+    }
+    const int32_t n0 = device_order(fs, zs, q, t_in_bin, u, rotate, order);
     feat[d] = -1 - n0;
     lower[d] = -inf;
     upper[d] = inf;
-    zero[d] = (Z)tr.v[j];
+    zero[d] = (Z)ps.v;
     for (int32_t kk = 0; kk < q; ++kk) {
-      const Split& e = src[order[kk]];
+      const Split& e = el[order[kk]];
       const int64_t o = d + 1 + kk;
       feat[o] = e.feature;
       lower[o] = e.lower;
@@ -1291,10 +1311,10 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       const int64_t base = ens->tree_node_offsets[t];
       return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
-        double prod = 1.0;
-        for (size_t i = 0; i < m; ++i) prod = prod * w.merged[i].zero_fraction;
-        out.first.push_back((int64_t)out.el.size());
-        out.el.insert(out.el.end(), w.merged.begin(), w.merged.begin() + (std::ptrdiff_t)m);
+        const size_t at = out.el.size();
+        out.first.push_back((int64_t)at);
+        out.el.resize(at + m);
+        const double prod = w.emit(out.el.data() + at);
         out.size.push_back((int32_t)m + 1);
         out.v.push_back(v);
         out.term_sum = out.term_sum + v * prod;
@@ -1346,11 +1366,9 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     const bool need_size = !size_decreasing(alg);
     std::vector<int32_t>& key = sc.key;
     std::vector<int32_t>& size_at = sc.size_at;
-    std::vector<int64_t>& path_tree = sc.path_tree;
     std::vector<int64_t>& start = sc.chunk_start;
     std::vector<int64_t>& key_start = sc.key_start;
     key.resize((size_t)P);
-    path_tree.resize((size_t)P);
     if (need_size) size_at.resize((size_t)P);
     start.assign((size_t)(chunks * nkeys), 0);
     key_start.resize((size_t)nkeys + 1);
@@ -1371,7 +1389,6 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
             const int32_t r = grank[(size_t)ens->tree_group[t]];
             int64_t p = tree_first[(size_t)t];
             for (size_t k = 0; k < sz.size(); ++k, ++p) {
-              path_tree[(size_t)p] = t;
               const int32_t kk = sort_key(r, sz[k], bin_capacity, alg);
               key[(size_t)p] = kk;
               ++cnt[kk];
@@ -1394,7 +1411,8 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       key_start[(size_t)nkeys] = run;
     }
     Packing& pk = sc.pk;
-    pk.order.resize((size_t)P);
+    std::vector<PathSrc>& src_at = sc.src_at;
+    if (!sizes_only) src_at.resize((size_t)P);
     {
       std::atomic<int64_t> next{0};
       Pool::get().run(sort_threads, [&]() {
@@ -1403,11 +1421,13 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
           chunk_trees(c, t0, t1);
           int64_t* pos = start.data() + c * nkeys;
           for (int64_t t = t0; t < t1; ++t) {
-            const std::vector<int32_t>& sz = trees[(size_t)t].size;
+            const TreeOut& tr = trees[(size_t)t];
+            const std::vector<int32_t>& sz = tr.size;
             int64_t p = tree_first[(size_t)t];
             for (size_t j = 0; j < sz.size(); ++j, ++p) {
               const int64_t k = pos[key[(size_t)p]]++;
-              pk.order[(size_t)k] = p;
+              if (!sizes_only)
+                src_at[(size_t)k] = PathSrc{tr.el.data() + tr.first[j], tr.v[j], sz[j] - 1, 0};
               if (need_size) size_at[(size_t)k] = sz[j];
             }
           }
@@ -1435,18 +1455,21 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     if (blob) {
       zero_padding(bp, blob);
       const int64_t K = pk.K;
-      // each bin's placements in placement order
-      std::vector<int64_t>& by_bin = sc.by_bin;
-      by_bin.resize((size_t)P);
+      // each bin's paths in placement order, with their offsets in the bin
+      std::vector<PathSrc>& src_by_bin = sc.src_by_bin;
+      src_by_bin.resize((size_t)P);
       {
         std::atomic<int64_t> next{0};
         const int64_t step = std::max<int64_t>(4096, P / (4 * nthreads) + 1);
         Pool::get().run(nthreads, [&]() {
           for (int64_t k0; (k0 = next.fetch_add(step)) < P;) {
             const int64_t k1 = std::min(P, k0 + step);
-            for (int64_t k = k0; k < k1; ++k)
-              by_bin[(size_t)(pk.bin_first[(size_t)pk.bin_at[(size_t)k]] + pk.slot_at[(size_t)k])] =
-                  k;
+            for (int64_t k = k0; k < k1; ++k) {
+              PathSrc ps = src_at[(size_t)k];
+              ps.within = pk.within_at[(size_t)k];
+              src_by_bin[(size_t)(pk.bin_first[(size_t)pk.bin_at[(size_t)k]] +
+                                  pk.slot_at[(size_t)k])] = ps;
+            }
           }
         });
       }
@@ -1462,11 +1485,9 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
           const int64_t b1 = std::min(K, b0 + chunk);
           for (int64_t b = b0; b < b1; ++b) {
             if (dtype == GTS_F64)
-              write_bin<double>(bp.m, blob, trees, path_tree.data(), tree_first.data(), pk,
-                                by_bin.data(), b, used, touched);
+              write_bin<double>(bp.m, blob, pk, src_by_bin.data(), P, b, used, touched);
             else
-              write_bin<float>(bp.m, blob, trees, path_tree.data(), tree_first.data(), pk,
-                               by_bin.data(), b, used, touched);
+              write_bin<float>(bp.m, blob, pk, src_by_bin.data(), P, b, used, touched);
           }
         }
       });

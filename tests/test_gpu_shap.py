@@ -296,3 +296,29 @@ def test_largest_feature_count(torch, orc, dtype, inter):
             with pytest.raises(gts.GtsError) as err:
                 fn(model, Xd)
             assert err.value.status == gts.GTS_EINVAL
+
+
+@pytest.mark.parametrize("dtype,largest", [("f32", 13), ("f64", 8)])
+def test_one_path_per_wave_boundary(torch, orc, dtype, largest):
+    """The host keeps a path's elements (after its zero-fraction ones) in
+    feature order, without the collision-avoiding rotation, exactly for the
+    models whose every launch runs one path per wave: M <= 13 in fp32 and
+    M <= 8 in fp64.  gts_launch_config must agree (64-row tiles for SHAP and
+    interaction values up to that M, fewer rows for interaction values one
+    feature above), and the results match the oracle on both sides."""
+    for M in (largest, largest + 1):
+        w = synth.random_workload(50 + M, num_trees=6, max_depth=6, M=M, num_groups=1,
+                                  n_bg=40, rows=40)
+        model = gts.prepare(w.ensemble, dtype)
+        shap_rw = gts.launch_config(model, 40)["rows_per_tile"]
+        inter_rw = gts.launch_config(model, 40, interactions=True)["rows_per_tile"]
+        say("one path per wave", dtype, M, shap_rw, inter_rw)
+        assert shap_rw == 64
+        assert (inter_rw == 64) == (M == largest)
+        got = run_shap(torch, w.ensemble, w.X, dtype)
+        assert_parity(got, orc.treeshap(w.ensemble, w.X), dtype, what=f"M={M}")
+        Xd = torch.from_numpy(w.X).cuda()
+        inter = gts.shap_interactions(model, Xd)
+        torch.cuda.synchronize()
+        assert_parity(inter.cpu().numpy().astype(np.float64), orc.interactions(w.ensemble, w.X),
+                      dtype, 2, f"interactions M={M}")
