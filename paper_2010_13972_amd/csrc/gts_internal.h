@@ -37,10 +37,10 @@ constexpr int64_t kBlobAlign = 256;
 // per wave, i.e. picks 64-row tiles: the launch planner does so while a
 // workgroup's X and phi tiles for 64 rows and the stages of its 8 waves fit
 // in 64 KB of LDS, and the interaction tile ((M+1)^2 entries per row) is the
-// larger, which holds up to M = 13 in fp32 and M = 8 in fp64.  For such
+// larger, which holds up to M = 12 in fp32 and M = 8 in fp64.  For such
 // models the order of a path's elements decides no same-step collisions.
 inline bool one_path_per_wave(int32_t M, int32_t dtype) {
-  return M <= (dtype == GTS_F64 ? 8 : 13);
+  return M <= (dtype == GTS_F64 ? 8 : 12);
 }
 
 // Thread-local error message; returns `status` for convenient tail calls.

@@ -1,7 +1,8 @@
-"""gts_extract_paths_device (Sections 3.1-3.2 on the GPU) against the host
-extraction gts_extract_paths, which is itself bit-exact to the oracle's
-independent extraction: every element field and the bias compare as raw
-bytes."""
+"""gts_extract_paths_device (Sections 3.1-3.2 on the GPU) against the
+oracle's independent extraction (or_extract_paths) and against the host
+extraction gts_extract_paths: every element field and the bias compare as raw
+bytes.  Malformed ensembles, which the oracle does not validate, compare the
+error status with the host call's."""
 import numpy as np
 import pytest
 
@@ -25,31 +26,41 @@ def device_extract(torch, ens):
     return gts.elements_from_device(raw), npaths, bias.cpu().numpy()
 
 
-def assert_same(torch, ens, what):
-    el, npaths, bias = gts.extract_paths(ens)
+FIELDS = ("path_idx", "feature_idx", "group", "lower", "upper", "zero_fraction", "v")
+
+
+def assert_same(torch, orc, ens, what):
     d_el, d_npaths, d_bias = device_extract(torch, ens)
+    oel, onpaths, obias = orc.extract_paths(ens)
+    assert d_npaths == onpaths, what
+    assert len(d_el) == len(oel), what
+    for f in FIELDS:
+        assert np.ascontiguousarray(d_el[f]).tobytes() == np.ascontiguousarray(oel[f]).tobytes(), \
+            (what, f)
+    assert d_bias.tobytes() == np.ascontiguousarray(obias, np.float64).tobytes(), what
+    el, npaths, bias = gts.extract_paths(ens)
     assert d_npaths == npaths, what
     assert d_el.tobytes() == el.tobytes(), what
     assert d_bias.tobytes() == bias.tobytes(), what
 
 
 @pytest.mark.parametrize("name", ["tiny", "covtype_med", "deep", "wide"])
-def test_workload_models_bitwise(torch, name):
+def test_workload_models_bitwise(torch, orc, name):
     w = synth.workload(name, rows=1)
     say("device extraction", name)
-    assert_same(torch, w.ensemble, name)
+    assert_same(torch, orc, w.ensemble, name)
 
 
 @pytest.mark.parametrize("seed", range(10))
-def test_random_edge_case_ensembles_bitwise(torch, seed):
+def test_random_edge_case_ensembles_bitwise(torch, orc, seed):
     """Repeated features, ties, zero-cover nodes, several output groups."""
     w = synth.random_workload(seed, num_trees=20, max_depth=9, M=5, num_groups=3, n_bg=30,
                               rows=1)
     say("device extraction random", seed)
-    assert_same(torch, w.ensemble, f"random{seed}")
+    assert_same(torch, orc, w.ensemble, f"random{seed}")
 
 
-def test_special_trees_bitwise(torch):
+def test_special_trees_bitwise(torch, orc):
     rng = np.random.default_rng(4)
     leaf = [(-1, -1, -1, 0.0, 10.0, 2.5)]
     stump = [(1, 2, 1, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 3.0, -1.0), (-1, -1, -1, 0, 7.0, 4.0)]
@@ -62,7 +73,7 @@ def test_special_trees_bitwise(torch):
     trees = [leaf, stump, dup, chain_tree(63, 63, rng), shuffled, leaf]
     ens = synth.ensemble_from_lists(trees, M=63, num_groups=2)
     say("device extraction special trees")
-    assert_same(torch, ens, "special trees")
+    assert_same(torch, orc, ens, "special trees")
 
 
 def test_errors_match_the_host(torch):

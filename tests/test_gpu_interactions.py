@@ -3,14 +3,15 @@
 
 Small cases compare every element with brute-force enumeration and with the
 oracle's conditioning route (Section 2.2); the full-size workload (the
-covtype-shaped model, 1000 rows) compares sampled rows and checks, on every
-row, symmetry, row sums equal to gts_shap's values and the bias entry.
+covtype-shaped model, 1000 rows) compares every row element by element and
+checks, on every row, symmetry, row sums equal to gts_shap's values and the
+bias entry.
 """
 import numpy as np
 import pytest
 
 from paper_2010_13972_amd import gts, synth
-from parity import assert_parity, sum_tolerance
+from parity import assert_parity, tolerance
 from test_gpu_shap import chain_tree, empty_ensemble, sample_rows, say
 
 pytestmark = pytest.mark.gpu
@@ -68,38 +69,43 @@ def test_long_paths(torch, orc, depth):
 
 
 def test_full_size_workload(torch, orc):
+    """The covtype-shaped model, 1000 rows (the bench's interaction batch):
+    every row element by element against the conditioning route; and on every
+    row symmetry, row sums equal to gts_shap's values and the bias entry."""
     w = synth.workload("interactions")
     M = w.ensemble.num_features
     say("interactions full size", w.X.shape)
     inter, phi = run(torch, w.ensemble, w.X, "f32", both=True)
-    rows = sample_rows(w.X.shape[0], k=8)
-    want = orc.interactions(w.ensemble, w.X[rows])
-    assert_parity(inter[rows], want, "f32", 2, "covtype-shaped model, sampled rows")
-    # every row: symmetric, rows sum to the SHAP values, bias at [M, M]
-    scale = np.abs(inter)
+    want = orc.interactions(w.ensemble, w.X)
+    assert_parity(inter, want, "f32", 2, "covtype-shaped model, every row")
+    # every row: symmetric, rows sum to the SHAP values, bias at [M, M]; the
+    # bounds are the parity tolerance of the oracle's blocks
+    tol = tolerance(want, "f32", 2)
     sym_err = np.abs(inter - np.swapaxes(inter, -1, -2))
-    sym_tol = 1e-3 * scale + 1e-5 * scale.sum(axis=(-2, -1), keepdims=True)
-    assert np.all(sym_err <= 2 * sym_tol)
+    assert np.all(sym_err <= tol + np.swapaxes(tol, -1, -2))
+    want_phi = orc.treeshap(w.ensemble, w.X)
     row_sum = inter[..., :M, :].sum(-1)
-    bound = sum_tolerance(scale[..., :M, :], "f32") + 1e-3 * np.abs(phi[..., :M]) \
-        + 1e-5 * np.abs(phi).sum(-1, keepdims=True)
+    bound = tol[..., :M, :].sum(-1) + tolerance(want_phi, "f32")[..., :M]
     assert np.all(np.abs(row_sum - phi[..., :M]) <= bound)
     assert np.allclose(inter[..., M, M], phi[..., M], rtol=1e-6, atol=1e-7)
     assert np.all(inter[..., M, :M] == 0) and np.all(inter[..., :M, M] == 0)
 
 
 def test_large_row_count_interactions(torch, orc):
-    """2^16 rows (the rows sweep's largest interaction batch): sampled rows
-    against the conditioning oracle, every row's sums against gts_shap."""
+    """2^16 rows (the rows sweep's largest interaction batch): 48 rows spread
+    over the batch against the conditioning oracle; every row's sums against
+    gts_shap, with a bound scaled by the oracle's magnitudes on those rows."""
     w = synth.workload("interactions", rows=1)
     X = synth.sweep_rows("interactions", 1 << 16)
     say("large interaction batch", X.shape)
     inter, phi = run(torch, w.ensemble, X, "f32", both=True)
-    sel = sample_rows(X.shape[0], k=6, seed=5)
-    assert_parity(inter[sel], orc.interactions(w.ensemble, X[sel]), "f32", 2, "2^16 rows")
+    sel = np.unique(np.concatenate([np.arange(0, 1 << 16, 1 << 11), np.arange((1 << 16) - 8, 1 << 16),
+                                    sample_rows(X.shape[0], k=6, seed=5)]))
+    want = orc.interactions(w.ensemble, X[sel])
+    assert_parity(inter[sel], want, "f32", 2, "2^16 rows")
     err = np.abs(inter.sum(-1) - phi)
-    bound = sum_tolerance(np.abs(inter), "f32", 1) + 1e-3 * np.abs(phi) + 1e-5 * np.abs(phi).sum(-1, keepdims=True)
-    assert np.all(err <= bound), float((err / bound).max())
+    scale = 2 * float(tolerance(want, "f32", 2).sum(-1).max())
+    assert np.all(err <= scale), float((err / scale).max())
 
 
 def test_empty_model_and_unfed_groups(torch, orc):
