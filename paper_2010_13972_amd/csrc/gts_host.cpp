@@ -14,8 +14,10 @@
 #include <cstring>
 #include <functional>
 #include <limits>
+#include <memory>
 #include <new>
 #include <thread>
+#include <type_traits>
 #include <vector>
 
 #include "gts_internal.h"
@@ -58,6 +60,14 @@ struct Split {
   int32_t feature;
   float lower, upper;
   double zero_fraction;
+};
+
+// A merged element as an fp32 blob stores it: the zero fraction rounded to
+// float (16 bytes instead of 24).
+struct SplitF {
+  int32_t feature;
+  float lower, upper;
+  float zero_fraction;
 };
 
 inline double cover_ratio(double child, double parent) {
@@ -204,14 +214,15 @@ class Pool {
 // path from the root to the current node are kept up to date on the way down
 // and restored on the way up (Section 3.2): for every feature on the path,
 // the intersection of its ranges and the product of its zero fractions taken
-// in root-to-leaf order, and the features on the path in ascending order.
+// in root-to-leaf order, and the set of features on the path (a bit mask for
+// up to 64 features, else a list kept in ascending order).
 struct Walker {
+  // A node still to visit: its parent (-1 for the root) and the side it hangs
+  // on, and the undo depth of the parent's path.
   struct Frame {
     int32_t node;
-    int32_t depth;    // undo depth of the parent's path
-    int32_t feature;  // the split into this node (-1 at the root)
-    float lo, hi;
-    double ratio;
+    int32_t from;    // parent * 2 + (1 if the right child), -1 at the root
+    int32_t depth;
   };
   struct Undo {
     int32_t feature;
@@ -224,128 +235,188 @@ struct Walker {
   std::vector<float> lower;     // [M]
   std::vector<float> upper;     // [M]
   std::vector<double> zf;       // [M]
-  std::vector<int32_t> active;  // features with count > 0, ascending
+  std::vector<int32_t> active;  // M > 64: features with count > 0, ascending
+  uint64_t mask = 0;            // M <= 64: bit f set when count[f] > 0
   std::vector<unsigned char> seen;
+  bool small = true;
   bool clean = false;
 
-  void reset(int32_t M) {
+  void reset(int32_t M, int32_t n) {
     const float inf = std::numeric_limits<float>::infinity();
+    small = M <= 64;
     if (!clean || (int32_t)count.size() != M) {
       count.assign((size_t)M, 0);
       lower.assign((size_t)M, -inf);
       upper.assign((size_t)M, inf);
       zf.assign((size_t)M, 1.0);
       active.clear();
+      mask = 0;
     }
-    undo.clear();
-    stack.clear();
+    if (stack.size() < (size_t)n + 1) stack.resize((size_t)n + 1);
+    if (undo.size() < (size_t)n + 1) undo.resize((size_t)n + 1);
     clean = false;
   }
 
-  // Enter a split on feature f (range [lo, hi), cover ratio).  Without
-  // VALUES only the set of features on the path is kept.
-  template <bool VALUES>
-  void push(int32_t f, float lo, float hi, double ratio) {
-    const size_t i = (size_t)f;
-    if (VALUES) {
-      undo.push_back(Undo{f, lower[i], upper[i], zf[i]});
-      if (lo > lower[i]) lower[i] = lo;
-      if (hi < upper[i]) upper[i] = hi;
-      zf[i] = zf[i] * ratio;
-    } else {
-      undo.push_back(Undo{f, 0.0f, 0.0f, 0.0});
-    }
-    if (count[i]++ == 0) {
-      active.push_back(f);
-      size_t k = active.size() - 1;
-      for (; k > 0 && active[k - 1] > f; --k) active[k] = active[k - 1];
-      active[k] = f;
-    }
-  }
+  size_t active_count() const { return small ? (size_t)__builtin_popcountll(mask) : active.size(); }
 
-  template <bool VALUES>
-  void pop() {
-    const Undo u = undo.back();
-    undo.pop_back();
-    const size_t i = (size_t)u.feature;
-    if (VALUES) {
-      lower[i] = u.lower;
-      upper[i] = u.upper;
-      zf[i] = u.zero_fraction;
-    }
-    if (--count[i] == 0) {
-      size_t k = 0;
-      while (active[k] != u.feature) ++k;
-      for (; k + 1 < active.size(); ++k) active[k] = active[k + 1];
-      active.pop_back();
-    }
-  }
-
-  // The current leaf's m merged elements, in ascending feature order, into
-  // dst[0..m); returns the product of their zero fractions (a left fold in
-  // that order).
-  double emit(Split* dst) const {
+  // The current leaf's merged elements, in ascending feature order, into
+  // dst[0..active_count()); returns the product of their zero fractions (a
+  // left fold in that order).
+  template <typename S>
+  double emit(S* dst) const {
+    using Z = decltype(S::zero_fraction);
     double prod = 1.0;
-    for (size_t i = 0; i < active.size(); ++i) {
-      const size_t f = (size_t)active[i];
-      dst[i] = Split{active[i], lower[f], upper[f], zf[f]};
-      prod = prod * zf[f];
+    if (small) {
+      size_t i = 0;
+      for (uint64_t m = mask; m; m &= m - 1, ++i) {
+        const int32_t f = __builtin_ctzll(m);
+        dst[i] = S{f, lower[(size_t)f], upper[(size_t)f], (Z)zf[(size_t)f]};
+        prod = prod * zf[(size_t)f];
+      }
+    } else {
+      for (size_t i = 0; i < active.size(); ++i) {
+        const size_t f = (size_t)active[i];
+        dst[i] = S{active[i], lower[f], upper[f], (Z)zf[f]};
+        prod = prod * zf[f];
+      }
     }
     return prod;
   }
 
+  // Enter a split on feature f (range [lo, hi), cover ratio) at undo depth u.
+  // Without VALUES only the set of features on the path is kept.
+  template <bool VALUES>
+  void push(int32_t u, int32_t f, float lo, float hi, double ratio) {
+    const size_t i = (size_t)f;
+    Undo& e = undo[(size_t)u];
+    e.feature = f;
+    if (VALUES) {
+      e.lower = lower[i];
+      e.upper = upper[i];
+      e.zero_fraction = zf[i];
+      if (lo > lower[i]) lower[i] = lo;
+      if (hi < upper[i]) upper[i] = hi;
+      zf[i] = zf[i] * ratio;
+    }
+    if (count[i]++ == 0) {
+      if (small) {
+        mask |= 1ull << f;
+      } else {
+        active.push_back(f);
+        size_t k = active.size() - 1;
+        for (; k > 0 && active[k - 1] > f; --k) active[k] = active[k - 1];
+        active[k] = f;
+      }
+    }
+  }
+
+  template <bool VALUES>
+  void pop(int32_t u) {
+    const Undo& e = undo[(size_t)u];
+    const size_t i = (size_t)e.feature;
+    if (VALUES) {
+      lower[i] = e.lower;
+      upper[i] = e.upper;
+      zf[i] = e.zero_fraction;
+    }
+    if (--count[i] == 0) {
+      if (small) {
+        mask &= ~(1ull << e.feature);
+      } else {
+        size_t k = 0;
+        while (active[k] != e.feature) ++k;
+        for (; k + 1 < active.size(); ++k) active[k] = active[k + 1];
+        active.pop_back();
+      }
+    }
+  }
+
   // Depth-first walk of tree t, left child (x < t) first, validating every
   // node it reaches.  Calls leaf(node, m) with m merged elements (with EMIT,
-  // emit() gives them; without EMIT only m is computed).  The stack holds nodes still to visit, each with the
-  // split that leads to it and the undo depth of its parent's path: a visit
-  // first unwinds the path to that depth, then enters the split.
+  // emit() gives them; without EMIT only m is computed).  The stack holds
+  // nodes still to visit, each with the undo depth of its parent's path: a
+  // visit first unwinds the path to that depth, then enters the split from
+  // the parent (range from the parent's threshold and the side, zero
+  // fraction child cover / parent cover).
   template <bool EMIT, typename LeafFn>
   gts_status walk(const gts_ensemble* e, int64_t t, LeafFn&& leaf) {
     const int64_t base = e->tree_node_offsets[t];
     const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
-    reset(e->num_features);
+    reset(e->num_features, n);
     seen.assign((size_t)n, 0);
+    const int32_t* const left = e->left + base;
+    const int32_t* const right = e->right + base;
+    const int32_t* const feature = e->feature + base;
+    const float* const threshold = e->threshold + base;
+    const double* const cover = e->cover + base;
+    const double* const value = e->value + base;
+    const int32_t M = e->num_features;
     const float inf = std::numeric_limits<float>::infinity();
-    stack.push_back(Frame{0, 0, -1, 0.0f, 0.0f, 0.0});
-    while (!stack.empty()) {
-      const Frame fr = stack.back();
-      stack.pop_back();
-      while ((int32_t)undo.size() > fr.depth) pop<EMIT>();
-      if (fr.feature >= 0) push<EMIT>(fr.feature, fr.lo, fr.hi, fr.ratio);
+    Frame* const st = stack.data();
+    int32_t sp = 0;   // frames on the stack
+    int32_t ud = 0;   // undo depth of the current path
+    st[sp++] = Frame{0, -1, 0};
+    gts_status status = GTS_OK;
+    while (sp > 0) {
+      const Frame fr = st[--sp];
+      while (ud > fr.depth) pop<EMIT>(--ud);
       const int32_t node = fr.node;
-      const int64_t gi = base + node;
-      if (seen[(size_t)node])
-        return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
-                    (long long)t, node);
+      if (fr.from >= 0) {
+        const int32_t parent = fr.from >> 1;
+        const float th = threshold[parent];
+        const bool is_right = fr.from & 1;
+        push<EMIT>(ud++, feature[parent], is_right ? th : -inf, is_right ? inf : th,
+                   EMIT ? cover_ratio(cover[node], cover[parent]) : 0.0);
+      }
+      if (seen[(size_t)node]) {
+        status = fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
+                      (long long)t, node);
+        break;
+      }
       seen[(size_t)node] = 1;
-      const double r = e->cover[gi];
-      if (!(r >= 0.0) || !std::isfinite(r))
-        return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
-                    (long long)t, node);
-      const int32_t a = e->left[gi], b = e->right[gi];
+      const double r = cover[node];
+      if (!(r >= 0.0) || !std::isfinite(r)) {
+        status = fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
+                      (long long)t, node);
+        break;
+      }
+      const int32_t a = left[node], b = right[node];
       if (a < 0 && b < 0) {
-        if (!std::isfinite(e->value[gi]))
-          return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
-        leaf(node, active.size());
+        if (!std::isfinite(value[node])) {
+          status = fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
+          break;
+        }
+        leaf(node, active_count());
         continue;
       }
-      if (a < 0 || b < 0 || a >= n || b >= n)
-        return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
-                    node);
-      const int32_t d = e->feature[gi];
-      if (d < 0 || d >= e->num_features)
-        return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)",
-                    (long long)t, node, d, e->num_features);
-      const float th = e->threshold[gi];
-      if (std::isnan(th))
-        return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
-      const int32_t depth = (int32_t)undo.size();
-      stack.push_back(Frame{b, depth, d, th, inf, EMIT ? cover_ratio(e->cover[base + b], r) : 0.0});
-      stack.push_back(Frame{a, depth, d, -inf, th, EMIT ? cover_ratio(e->cover[base + a], r) : 0.0});
+      if (a < 0 || b < 0 || a >= n || b >= n) {
+        status = fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
+                      node);
+        break;
+      }
+      const int32_t d = feature[node];
+      if (d < 0 || d >= M) {
+        status = fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)", (long long)t,
+                      node, d, M);
+        break;
+      }
+      if (std::isnan(threshold[node])) {
+        status = fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
+        break;
+      }
+      // a node reached twice is refused at its second visit, so every node
+      // is pushed at most twice and the stack holds at most n + 1 frames
+      if (sp + 2 > (int32_t)stack.size()) {
+        status = fail(GTS_EINVAL, "tree %lld node %d: node reached twice (cycle or shared child)",
+                      (long long)t, node);
+        break;
+      }
+      st[sp++] = Frame{b, node * 2 + 1, ud};
+      st[sp++] = Frame{a, node * 2, ud};
     }
-    while (!undo.empty()) pop<EMIT>();
+    while (ud > 0) pop<EMIT>(--ud);
     clean = true;
-    return GTS_OK;
+    return status;
   }
 };
 
@@ -607,13 +678,27 @@ inline int32_t sort_key(int32_t grank, int32_t size, int32_t cap, int32_t alg) {
   return size_decreasing(alg) ? grank * (cap + 1) + (cap - size) : grank;
 }
 
-// The outcome of packing.  Per placement k (the k-th path in processing
-// order, order[k]): its bin, its element offset inside the bin and its rank
-// among the bin's paths.  Per bin: group, elements, paths.  The bins'
-// element ranges, and the bins' path ranges for a list of placements by bin.
+// A run of placements k .. k+n-1 (all of size s) that went into bin b one
+// after another: placement k+i sits at element offset w + i*s of the bin and
+// is the bin's (slot + i)-th path.
+struct Fill {
+  int64_t k;
+  int32_t b;
+  int32_t n;
+  int32_t w;
+  int32_t slot;
+  int32_t s;
+};
+
+// The outcome of packing: the fills in placement order.  Per bin: group,
+// elements, paths.  The bins' element ranges, and the bins' path ranges for a
+// list of placements by bin.  Per placement k (the k-th path in processing
+// order, order[k]), when expanded from the fills: its bin, its element offset
+// inside the bin and its rank among the bin's paths.
 struct Packing {
   std::vector<int64_t> order;        // [P] paths in processing order
-  std::vector<int64_t> bin_at;       // [P] per placement
+  std::vector<Fill> fills;
+  std::vector<int64_t> bin_at;       // [P] per placement (expand())
   std::vector<uint8_t> within_at;    // [P] per placement: element offset inside the bin
   std::vector<uint8_t> slot_at;      // [P] per placement: rank among the bin's paths
   std::vector<int32_t> bin_used;     // [K] elements in the bin
@@ -624,26 +709,34 @@ struct Packing {
   std::vector<int64_t> dest;         // [P] per path: packed element offset (assign_bins)
   int64_t K = 0;
   bool sorted = true;                // every bin's sizes non-increasing in placement order
+
+  // The per-placement arrays from the fills.
+  void expand(int64_t P) {
+    bin_at.resize((size_t)P);
+    within_at.resize((size_t)P);
+    slot_at.resize((size_t)P);
+    for (const Fill& f : fills)
+      for (int32_t i = 0; i < f.n; ++i) {
+        bin_at[(size_t)(f.k + i)] = f.b;
+        within_at[(size_t)(f.k + i)] = (uint8_t)(f.w + i * f.s);
+        slot_at[(size_t)(f.k + i)] = (uint8_t)(f.slot + i);
+      }
+  }
 };
 
 // Runs the heuristic over the placements in processing order.  key_start
 // [ng * nsize + 1]: first placement of every sort key.  The size of a
 // placement is the one its key encodes for BFD and FFD, size_at[k] for the
 // others.  group_of_rank[r]: the group id of rank r.  The loop reads no
-// per-path array for BFD and FFD and writes the per-placement outputs in
-// order.
+// per-path array for BFD and FFD and records one fill per run of placements
+// that goes into one bin.
 void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_rank,
                  const int32_t* size_at, int64_t P, int32_t cap, int32_t alg, Packing& pk) {
-  pk.bin_at.resize((size_t)P);
-  pk.within_at.resize((size_t)P);
-  pk.slot_at.resize((size_t)P);
+  pk.fills.clear();
   pk.bin_used.clear();
   pk.bin_paths.clear();
   pk.bin_group.clear();
   pk.sorted = true;
-  int64_t* const bin_at = pk.bin_at.data();
-  uint8_t* const within_at = pk.within_at.data();
-  uint8_t* const slot_at = pk.slot_at.data();
   int64_t K = 0;
   auto open_bin = [&](int32_t g) {
     pk.bin_used.push_back(0);
@@ -651,12 +744,12 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
     pk.bin_group.push_back(g);
     return K++;
   };
-  // placement k (size s) goes into bin b at element offset w
-  auto put = [&](int64_t k, int64_t b, int32_t w, int32_t s) {
-    bin_at[k] = b;
-    within_at[k] = (uint8_t)w;
-    slot_at[k] = (uint8_t)pk.bin_paths[(size_t)b]++;
-    pk.bin_used[(size_t)b] = w + s;
+  // placements k .. k+n-1 (size s) go into bin b from element offset w on
+  auto put = [&](int64_t k, int64_t b, int32_t n, int32_t w, int32_t s) {
+    int32_t& paths = pk.bin_paths[(size_t)b];
+    pk.fills.push_back(Fill{k, (int32_t)b, n, w, paths, s});
+    paths += n;
+    pk.bin_used[(size_t)b] = w + n * s;
   };
   const int64_t nsize = keys_per_group(cap, alg);
   std::vector<int32_t> resid;
@@ -691,11 +784,10 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
             b = open_bin(g);
             res = cap;
           }
-          const int64_t n = std::min<int64_t>(res / s, k1 - k);
-          for (int64_t t = 0; t < n; ++t, ++k) {
-            put(k, b, cap - res, s);
-            res -= s;
-          }
+          const int32_t n = (int32_t)std::min<int64_t>(res / s, k1 - k);
+          put(k, b, n, cap - res, s);
+          k += n;
+          res -= n * s;
           if (res > 0) {
             heap_push(by_resid[(size_t)res], b);
             open |= 1ull << (res - 1);
@@ -719,11 +811,10 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
             resid[(size_t)local] = cap;
           }
           int32_t res = resid[(size_t)local];
-          const int64_t n = std::min<int64_t>(res / s, k1 - k);
-          for (int64_t t = 0; t < n; ++t, ++k) {
-            put(k, first_bin + local, cap - res, s);
-            res -= s;
-          }
+          const int32_t n = (int32_t)std::min<int64_t>(res / s, k1 - k);
+          put(k, first_bin + local, n, cap - res, s);
+          k += n;
+          res -= n * s;
           resid[(size_t)local] = res;
           tree.set(local, res);
         }
@@ -740,11 +831,11 @@ void place_paths(const int64_t* key_start, int32_t ng, const int32_t* group_of_r
         }
         if (s > last) pk.sorted = false;
         last = s;
-        put(k, K - 1, cap - res, s);
+        put(k, K - 1, 1, cap - res, s);
         res -= s;
       }
     } else {
-      for (int64_t k = i; k < j; ++k) put(k, open_bin(g), 0, size_at[k]);
+      for (int64_t k = i; k < j; ++k) put(k, open_bin(g), 1, 0, size_at[k]);
     }
   }
   pk.K = K;
@@ -789,6 +880,7 @@ void assign_bins(const int32_t* size, const int32_t* group, int64_t P, int32_t c
   }
   place_paths(start.data(), (int32_t)groups.size(), groups.data(), size_at.data(), P, cap, alg,
               pk);
+  pk.expand(P);
   if (!layout) return;
   pk.dest.resize((size_t)P);
   for (int64_t k = 0; k < P; ++k)
@@ -1177,16 +1269,39 @@ namespace {
 // included) and leaf value, and the tree's part of the bias.
 // (aligned to keep the vector headers of trees that different threads fill
 // at the same time on different cache lines)
+// A growable array of trivially copyable elements whose new slots are left
+// uninitialised (std::vector::resize would zero them first: twice the
+// writes).
+template <typename T>
+struct RawBuf {
+  std::unique_ptr<T[]> data;
+  size_t size = 0, cap = 0;
+  T* grow(size_t n) {
+    if (size + n > cap) {
+      const size_t c = std::max(size + n, 2 * cap + 64);
+      std::unique_ptr<T[]> d(new T[c]);
+      if (size) std::memcpy(d.get(), data.get(), size * sizeof(T));
+      data = std::move(d);
+      cap = c;
+    }
+    T* p = data.get() + size;
+    size += n;
+    return p;
+  }
+};
+
 struct alignas(128) TreeOut {
-  std::vector<Split> el;
-  std::vector<int64_t> first;  // per path: its first element in el
+  RawBuf<Split> el;            // fp64 models
+  RawBuf<SplitF> elf;          // fp32 models
+  std::vector<int64_t> first;  // per path: its first element in el / elf
   std::vector<int32_t> size;
   std::vector<double> v;
   double term_sum = 0.0;       // the terms v * prod(z) summed in path order
   int32_t max_size = 0;
   int64_t elements = 0;        // sum of size
   void clear() {
-    el.clear();
+    el.size = 0;
+    elf.size = 0;
     first.clear();
     size.clear();
     v.clear();
@@ -1200,7 +1315,7 @@ struct alignas(128) TreeOut {
 // its tree's buffer), leaf value and feature count, and, once placed, its
 // element offset inside its bin.
 struct PathSrc {
-  const Split* el;
+  const void* el;   // Split for fp64 models, SplitF for fp32
   double v;
   int32_t q;
   int32_t within;
@@ -1243,7 +1358,8 @@ void write_bin(const gts_model& m, char* blob, const Packing& pk, const PathSrc*
       __builtin_prefetch(ahead + 128);
     }
     const PathSrc& ps = src[i];
-    const Split* el = ps.el;
+    using S = std::conditional_t<std::is_same_v<Z, float>, SplitF, Split>;
+    const S* el = static_cast<const S*>(ps.el);
     const int32_t q = ps.q;
     const int64_t d = base + ps.within;
     for (int32_t jj = 0; jj < q; ++jj) {
@@ -1256,7 +1372,7 @@ void write_bin(const gts_model& m, char* blob, const Packing& pk, const PathSrc*
     upper[d] = inf;
     zero[d] = (Z)ps.v;
     for (int32_t kk = 0; kk < q; ++kk) {
-      const Split& e = el[order[kk]];
+      const S& e = el[order[kk]];
       const int64_t o = d + 1 + kk;
       feat[o] = e.feature;
       lower[o] = e.lower;
@@ -1311,10 +1427,14 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       const int64_t base = ens->tree_node_offsets[t];
       return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
-        const size_t at = out.el.size();
-        out.first.push_back((int64_t)at);
-        out.el.resize(at + m);
-        const double prod = w.emit(out.el.data() + at);
+        double prod;
+        if (dtype == GTS_F64) {
+          out.first.push_back((int64_t)out.el.size);
+          prod = w.emit(out.el.grow(m));
+        } else {
+          out.first.push_back((int64_t)out.elf.size);
+          prod = w.emit(out.elf.grow(m));
+        }
         out.size.push_back((int32_t)m + 1);
         out.v.push_back(v);
         out.term_sum = out.term_sum + v * prod;
@@ -1427,7 +1547,10 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
             for (size_t j = 0; j < sz.size(); ++j, ++p) {
               const int64_t k = pos[key[(size_t)p]]++;
               if (!sizes_only)
-                src_at[(size_t)k] = PathSrc{tr.el.data() + tr.first[j], tr.v[j], sz[j] - 1, 0};
+                src_at[(size_t)k] =
+                    PathSrc{dtype == GTS_F64 ? (const void*)(tr.el.data.get() + tr.first[j])
+                                             : (const void*)(tr.elf.data.get() + tr.first[j]),
+                            tr.v[j], sz[j] - 1, 0};
               if (need_size) size_at[(size_t)k] = sz[j];
             }
           }
@@ -1459,16 +1582,21 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       std::vector<PathSrc>& src_by_bin = sc.src_by_bin;
       src_by_bin.resize((size_t)P);
       {
+        const std::vector<Fill>& fills = pk.fills;
+        const int64_t nf = (int64_t)fills.size();
         std::atomic<int64_t> next{0};
-        const int64_t step = std::max<int64_t>(4096, P / (4 * nthreads) + 1);
+        const int64_t step = std::max<int64_t>(1024, nf / (4 * nthreads) + 1);
         Pool::get().run(nthreads, [&]() {
-          for (int64_t k0; (k0 = next.fetch_add(step)) < P;) {
-            const int64_t k1 = std::min(P, k0 + step);
-            for (int64_t k = k0; k < k1; ++k) {
-              PathSrc ps = src_at[(size_t)k];
-              ps.within = pk.within_at[(size_t)k];
-              src_by_bin[(size_t)(pk.bin_first[(size_t)pk.bin_at[(size_t)k]] +
-                                  pk.slot_at[(size_t)k])] = ps;
+          for (int64_t f0; (f0 = next.fetch_add(step)) < nf;) {
+            const int64_t f1 = std::min(nf, f0 + step);
+            for (int64_t f = f0; f < f1; ++f) {
+              const Fill& fl = fills[(size_t)f];
+              PathSrc* dst = src_by_bin.data() + pk.bin_first[(size_t)fl.b] + fl.slot;
+              for (int32_t i = 0; i < fl.n; ++i) {
+                PathSrc ps = src_at[(size_t)(fl.k + i)];
+                ps.within = fl.w + i * fl.s;
+                dst[i] = ps;
+              }
             }
           }
         });
