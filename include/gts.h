@@ -289,7 +289,12 @@ gts_status gts_prepare_model(const gts_ensemble *ens, int32_t bin_capacity, int3
 /*
  * gts_shap -- SHAP values, Eq. (2), by the per-path permutation-weight
  * recurrence of Algorithm 1 (EXTEND over a path's elements, then UNWIND of
- * each element and a sum; Section 3.4, Algorithms 2-3).
+ * each element and a sum), evaluated per (row, path) over the packed bins
+ * of Section 3.4.  A (row, path) with an element of zero fraction whose range
+ * misses the row contributes exactly nothing (Algorithm 1 prunes such
+ * subtrees) and may be skipped.  The kernels for paths longer than 12
+ * features use per-lane private memory that the HIP runtime provides with
+ * the launch; the others use none of their own beyond LDS.
  *
  * model    host descriptor from gts_model_layout.
  * d_model  device copy of the blob.
