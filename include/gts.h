@@ -17,10 +17,11 @@
  * Conventions shared by every call:
  *   - All memory is owned by the caller.  The library calls no device
  *     allocator and never frees caller memory; its only device memory of its
- *     own is the fixed workspace array of gts_extract_paths_device_noalloc.  No result depends on an earlier
- *     call; the host calls reuse a pool of worker threads (up to 16, two
- *     fewer than the process's cores when it has 8 or more, started on first
- *     use) and gts_prepare_model reuses per-thread working memory.
+ *     own is the fixed workspace array of gts_extract_paths_device_noalloc.
+ *     No result depends on an earlier call; the host calls reuse a pool of
+ *     worker threads (up to 16 and the process's cores; two fewer for calls
+ *     under 128 k nodes when it has 8 or more; started on first use) and
+ *     gts_prepare_model reuses per-thread working memory.
  *   - Every call returns a gts_status; on failure gts_last_error() returns a
  *     message for the calling thread (valid until that thread's next call).
  *   - A split sends x to the left child iff x < threshold; a path element
