@@ -309,7 +309,7 @@ gts_status gts_prepare_model(const gts_ensemble *ens, int32_t bin_capacity, int3
  * that is not from gts_model_layout, rows < 0, ld_x < M, or an M whose phi
  * and X rows do not fit in a workgroup's LDS at 4 rows per tile (on a
  * 160 KB-LDS device: M <= 4567 in fp32, M <= 2852 in fp64; for
- * gts_shap_interactions M <= 94 in fp32, M <= 64 in fp64), checked before
+ * gts_shap_interactions M <= 132 in fp32, M <= 90 in fp64), checked before
  * any launch; GTS_EDEVICE if a launch fails.
  */
 gts_status gts_shap(const gts_model *model, const void *d_model,

@@ -35,12 +35,12 @@ constexpr int64_t kBlobAlign = 256;
 
 // Whether every launch of a model (SHAP and interaction values) runs one path
 // per wave, i.e. picks 64-row tiles: the launch planner does so while a
-// workgroup's X and phi tiles for 64 rows and the stages of its 8 waves fit
-// in 64 KB of LDS, and the interaction tile ((M+1)^2 entries per row) is the
-// larger, which holds up to M = 12 in fp32 and M = 8 in fp64.  For such
+// workgroup's X and phi tiles for 64 rows and the stages of its waves fit in
+// 64 KB of LDS, and the interaction tile ((M+1)(M+2)/2 entries per row) is
+// the larger, which holds up to M = 17 in fp32 and M = 11 in fp64.  For such
 // models the order of a path's elements decides no same-step collisions.
 inline bool one_path_per_wave(int32_t M, int32_t dtype) {
-  return M <= (dtype == GTS_F64 ? 8 : 12);
+  return M <= (dtype == GTS_F64 ? 11 : 17);
 }
 
 // Thread-local error message; returns `status` for convenient tail calls.

@@ -62,7 +62,8 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
   if (width64 > (1 << 30)) return fail(GTS_EINVAL, "M = %d is too large", M);
   const int32_t width = (int32_t)width64;
   const int32_t sx = odd_at_least(M);
-  const int32_t sp = odd_at_least(width);
+  // interactions keep the upper triangle of each row's block in LDS
+  const int32_t sp = odd_at_least(INTER ? (int32_t)((int64_t)(M + 1) * (M + 2) / 2) : width);
   // Row tile and accumulation.  If 64 rows with a private phi tile for each
   // of 4 waves fit in half a CU's LDS (two workgroups per CU), use them (no
   // contention, no atomics).  Otherwise 8 waves share one tile: the largest
@@ -90,13 +91,25 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
         break;
       }
     }
+    if (INTER && RW == 0) {
+      // Interaction values: 16 waves (the kernel's registers allow one
+      // workgroup of them per CU) on the largest tile of 16, 8 or 4 rows the
+      // LDS of a workgroup holds.
+      for (int cand : {16, 8, 4}) {
+        if ((int64_t)need(cand, 16, false) <= dev.lds_per_block) {
+          RW = cand;
+          waves = 16;
+          break;
+        }
+      }
+    }
     if (RW == 0 && (int64_t)need(8, 8, false) <= dev.lds_per_block) RW = 8;
     if (RW == 0 && (int64_t)need(4, 8, false) <= dev.lds_per_block) RW = 4;
     // Waves per workgroup for a shared tile of RW <= 16 rows: as many waves
     // per CU as the LDS allows, up to 24 (the VGPR budget of the SHAP
-    // kernels) or 16 (interactions).
-    if (RW != 0 && RW <= 16) {
-      const int cap = INTER ? 16 : 24;
+    // kernels).
+    if (!INTER && RW != 0 && RW <= 16) {
+      const int cap = 24;
       int best = 0;
       for (int w : {8, 12, 16}) {
         const int64_t n = need(RW, w, false);

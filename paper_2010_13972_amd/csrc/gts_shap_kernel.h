@@ -88,6 +88,14 @@ __device__ __forceinline__ bool in_range(int kx, int klo, unsigned span) {
   return (unsigned)kx - (unsigned)klo < span;
 }
 
+// The interaction tile of a row keeps the upper triangle of the symmetric
+// (M+1) x (M+1) block, row by row: entry (a, b), a <= b, at tri_row(a) + b
+// with tri_row(a) = a W - a (a + 1) / 2 (W = M + 1 entries per full row).
+__device__ __forceinline__ int tri_row(int a, int W) { return a * W - ((a * (a + 1)) >> 1); }
+__device__ __forceinline__ int tri_at(int a, int b, int W) {
+  return a <= b ? tri_row(a, W) + b : tri_row(b, W) + a;
+}
+
 template <typename T>
 struct DevModel {
   const int32_t* __restrict__ feat;
@@ -123,7 +131,8 @@ struct Launch {
   int32_t tiles;     // row tiles
   int32_t splits;    // bin slices per group
   int32_t sx;        // LDS row stride of the X tile (floats)
-  int32_t sp;        // LDS row stride of the phi tile (elements)
+  int32_t sp;        // LDS row stride of the phi tile (elements; interactions:
+                     // the upper triangle, W (W + 1) / 2 entries)
   int32_t width;     // phi entries per (row, group): M+1 or (M+1)^2
   int32_t accumulate;  // 1: atomically add the tile to phi (phi pre-zeroed)
   int32_t sorted;      // 1: inside a bin, paths never grow in length
@@ -484,6 +493,9 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
   }
   const T half_v = T(0.5) * v;
   const T k00 = half_v * t_pair;   // (o_i, o_c) = (0, 0)
+  int tr[Q];  // start of feature f_i's row in the triangular tile
+#pragma unroll
+  for (int i = 0; i < Q; ++i) tr[i] = tri_row(f[i], stride);
   T hw[Q];    // v (1 - z_i) / 2
   T zc1[Q];   // 1 - z_c
   T lone[Q];  // -v (1 - z_c) tp[c] / 2: the pair value when only c is present
@@ -553,14 +565,14 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
       diag[c] -= delta;
       diag[i] -= delta;
       pon[i] = on[i] && on[c];
-      p[i] = prow + f[i] * stride + f[c];
+      p[i] = prow + (f[i] < f[c] ? tr[i] + f[c] : tr[c] + f[i]);
       val[i] = delta;
     }
     tile_add<MODE == kExclusive ? kExclusive : kBatched>(p, val, pon);
   }
   T* p[Q];
 #pragma unroll
-  for (int c = 0; c < Q; ++c) p[c] = prow + f[c] * stride + f[c];
+  for (int c = 0; c < Q; ++c) p[c] = prow + tr[c] + f[c];
   tile_add<MODE>(p, diag, on);
 }
 
@@ -635,10 +647,11 @@ __device__ void path_dyn(const Stage<T, GAPPED>* st, int s, int q, const int* __
         else delta = half_v * t_pair;
         diag[c] -= delta;
         diag[i] -= delta;
-        acc_add<MODE == kExclusive>(&prow[f[i] * stride + f[c]], (T)delta);
+        acc_add<MODE == kExclusive>(&prow[tri_at(f[i], f[c], stride)], (T)delta);
       }
     }
-    for (int c = 0; c < q; ++c) acc_add<MODE == kExclusive>(&prow[f[c] * stride + f[c]], (T)diag[c]);
+    for (int c = 0; c < q; ++c)
+      acc_add<MODE == kExclusive>(&prow[tri_row(f[c], stride) + f[c]], (T)diag[c]);
   }
 }
 
@@ -851,26 +864,22 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   __syncthreads();
 
   // write the tile: phi[row][g][.]; the bias goes to the last entry.  An
-  // interaction pair was added to one of its two entries: each of them gets
-  // the sum of both.
+  // interaction entry (a, b) and its mirror (b, a) both get the triangle's
+  // entry, so the output is exactly symmetric.
   const T bias = d.bias[g];
   const int W = L.width;
   for (int i = threadIdx.x; i < RW * W; i += kThreads) {
     const int rr = i / W, c = i - rr * W;
     const int64_t row = r0 + rr;
     if (row >= L.rows) continue;
-    int cm = c;
+    int t = c;
     if constexpr (INTER) {
-      const int a = c / stride, bcol = c - a * stride;
-      cm = bcol * stride + a;
+      const int a = c / stride;
+      t = tri_at(a, c - a * stride, stride);
     }
-    T val = ps[rr * L.sp + c];
-    if (cm != c) val += ps[rr * L.sp + cm];
+    T val = ps[rr * L.sp + t];
 #pragma unroll
-    for (int w = 1; w < NT; ++w) {
-      val += ps[w * tile_elems + rr * L.sp + c];
-      if (cm != c) val += ps[w * tile_elems + rr * L.sp + cm];
-    }
+    for (int w = 1; w < NT; ++w) val += ps[w * tile_elems + rr * L.sp + t];
     if (c == W - 1 && s == 0) val += bias;
     T* out = phi + (row * G + g) * (int64_t)W + c;
     if (L.accumulate) unsafeAtomicAdd(out, val);
@@ -914,8 +923,10 @@ gts_status launch_rw(const KernelArgs& a, const Plan& p) {
   if (grid > 0x7fffffffLL) return fail(GTS_EINVAL, "problem too large for one launch");
   auto kern = shap_kernel<T, RW, INTER, WAVES, PRIV, QMAX>;
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds) != hipSuccess)
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds) != hipSuccess) {
+    (void)hipGetLastError();   // leave no error behind for the caller's next HIP call
     return fail(GTS_EDEVICE, "cannot set the LDS size of the kernel to %zu bytes", p.lds);
+  }
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * WAVES), p.lds, stream, d, a.X,
                      static_cast<T*>(a.phi), L);
   const hipError_t err = hipGetLastError();

@@ -127,16 +127,21 @@ def test_empty_model_and_unfed_groups(torch, orc):
         assert np.all(got[:, 1] == 0.0)
 
 
-@pytest.mark.parametrize("M,rw", [(8, 64), (24, 16), (55, 8)])
-def test_launch_shapes(torch, orc, M, rw):
-    """Tile heights of the interaction launches (gts_launch_config), against
-    the conditioning route."""
+# (M, rows per tile, private tiles) of the interaction launches in fp32
+INTER_SHAPES = [(8, 64, 1), (13, 64, 0), (24, 32, 0), (55, 16, 0)]
+
+
+@pytest.mark.parametrize("M,rw,priv", INTER_SHAPES, ids=[f"M{m}" for m, _, _ in INTER_SHAPES])
+def test_launch_shapes(torch, orc, M, rw, priv):
+    """Tile heights of the interaction launches (gts_launch_config): a private
+    triangular tile per wave, shared tiles of 64, 32 and 16 rows; against the
+    conditioning route."""
     w = synth.random_workload(30 + M, num_trees=8, max_depth=6, M=M, num_groups=2, n_bg=40,
                               rows=37)
     model = gts.prepare(w.ensemble, "f32")
     cfg = gts.launch_config(model, 37, interactions=True)
     say("interactions launch shape", M, cfg)
-    assert cfg["rows_per_tile"] == rw and cfg["private_tiles"] == 0
+    assert cfg["rows_per_tile"] == rw and cfg["private_tiles"] == priv
     assert cfg["workgroups"] == -(-37 // rw) * 2 * cfg["slices"]
     got = run(torch, w.ensemble, w.X, "f32")
     assert_parity(got, orc.interactions(w.ensemble, w.X), "f32", 2, f"M={M}")
