@@ -300,10 +300,13 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                 launch_kernel(k - 1, timed)
         launch_kernel(n - 1, timed)
 
-    # untimed: a few preparations and back-to-back launches bring the host
-    # threads and the GPU clocks up before the warm-up steps
-    for _ in range(2):
+    # untimed: preparations for at least 0.3 s and back-to-back launches
+    # bring the host threads and the GPU clocks up before the warm-up steps
+    t_end = time.perf_counter() + 0.3
+    n_pre = 0
+    while n_pre < 2 or time.perf_counter() < t_end:
         L.gts_prepare_model(*prep_args[0])
+        n_pre += 1
     ref_model = gts.prepare(ens, dtype)
     fn = kernel_fn(gts, interactions)
     for _ in range(5):

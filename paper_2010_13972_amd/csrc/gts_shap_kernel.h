@@ -493,18 +493,8 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
   }
   const T half_v = T(0.5) * v;
   const T k00 = half_v * t_pair;   // (o_i, o_c) = (0, 0)
-  int tr[Q];  // start of feature f_i's row in the triangular tile
-#pragma unroll
-  for (int i = 0; i < Q; ++i) tr[i] = tri_row(f[i], stride);
-  T hw[Q];    // v (1 - z_i) / 2
-  T zc1[Q];   // 1 - z_c
   T lone[Q];  // -v (1 - z_c) tp[c] / 2: the pair value when only c is present
   T diag[Q];  // running phi_cc
-#pragma unroll
-  for (int i = 0; i < Q; ++i) {
-    hw[i] = T(0.5) * w[i];
-    zc1[i] = T(1) - z[i];
-  }
 #pragma unroll
   for (int c = 0; c < Q; ++c) {
     T D[Q];
@@ -518,7 +508,8 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
 #pragma unroll
       for (int k = 0; k < Q - 1; ++k) tpc = fma(T(shapley_weight(Q - 1, k)), D[k], tpc);
     }
-    lone[c] = -hw[c] * tpc;
+    const T cw = T(0.5) * w[c];   // v (1 - z_c) / 2, times (1 - z_i) below
+    lone[c] = -cw * tpc;
     if (c == 0) continue;
     // S_ic for every i < c: the Shapley-weighted sum (q-1 players) of
     // D / (z_i + t).  For many i, as a polynomial in -z_i with coefficients
@@ -533,7 +524,6 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
         for (int k = 1; k + m + 1 < Q; ++k) H[m] = fma(T(shapley_weight(Q - 1, k)), D[k + m + 1], H[m]);
       }
     }
-    const T cw = hw[c];   // v (1 - z_c) / 2, times (1 - z_i) below
     T* p[Q];
     T val[Q];
     bool pon[Q];
@@ -560,19 +550,19 @@ __device__ __forceinline__ void inter_math(const int (&f)[Q], const bool (&o)[Q]
           for (int k = 0; k < Q - 1; ++k) s11 = fma(T(shapley_weight(Q - 1, k)), DD[k], s11);
         }
       }
-      const T both = (cw * zc1[i]) * s11;
+      const T both = (cw * (T(1) - z[i])) * s11;
       const T delta = o[i] ? (o[c] ? both : lone[i]) : (o[c] ? lone[c] : k00);
       diag[c] -= delta;
       diag[i] -= delta;
       pon[i] = on[i] && on[c];
-      p[i] = prow + (f[i] < f[c] ? tr[i] + f[c] : tr[c] + f[i]);
+      p[i] = prow + tri_at(f[i], f[c], stride);
       val[i] = delta;
     }
     tile_add<MODE == kExclusive ? kExclusive : kBatched>(p, val, pon);
   }
   T* p[Q];
 #pragma unroll
-  for (int c = 0; c < Q; ++c) p[c] = prow + tr[c] + f[c];
+  for (int c = 0; c < Q; ++c) p[c] = prow + tri_row(f[c], stride) + f[c];
   tile_add<MODE>(p, diag, on);
 }
 
