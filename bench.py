@@ -85,7 +85,13 @@ SUITE = [
 # the counter's reading of it.  valu_insts / salu_insts / lds_insts:
 # SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
 # summaries and the commands that made them are in profiles/.
-COUNTERS = {}
+COUNTERS = {
+    ('deep', 'f32', False): {"fetch_bytes": 63790077, "write_bytes": 46080000, "valu_insts": 2115768783, "salu_insts": 1464665563, "lds_insts": 270237834, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
+    ('deep', 'f64', False): {"fetch_bytes": 73738864, "write_bytes": 92160000, "valu_insts": 2196190953, "salu_insts": 1442430166, "lds_insts": 290040856, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
+    ('covtype_med', 'f32', False): {"fetch_bytes": 19350772, "write_bytes": 35200000, "valu_insts": 283140291, "salu_insts": 84670654, "lds_insts": 42375069, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
+    ('wide', 'f32', False): {"fetch_bytes": 6193401739, "write_bytes": 316800000, "valu_insts": 5420836828, "salu_insts": 1413132152, "lds_insts": 765195913, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
+    ('interactions', 'f32', True): {"fetch_bytes": 17194684, "write_bytes": 60894374, "valu_insts": 184076128, "salu_insts": 34502649, "lds_insts": 16024014, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
+}
 
 
 def kernel_source_hash() -> str:
