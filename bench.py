@@ -224,106 +224,174 @@ def kernel_fn(gts, interactions):
     return gts.shap_interactions if interactions else gts.shap
 
 
-NBUF = 3      # model buffers in flight in the pipelined steps
-
-
-def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1):
-    """Whole-path steps, pipelined.  Step k prepares its model on the host
-    (gts_prepare_model into pinned buffer k mod 3) and a copy stream uploads
-    it into device buffer k mod 3; its kernel is launched after step k+1's
-    model has been prepared and its upload issued, on compute stream
-    k mod nstreams into output buffer k mod nstreams.  The host orders buffer
-    reuse (it waits for the upload that last read a pinned buffer, and for the
-    kernel that last read a device buffer), so the compute streams hold only
-    kernels and no cross-stream waits.  The loop calls the C ABI with
-    arguments marshalled once (the ensemble struct, descriptors, buffer
-    pointers), so the step measures the library rather than Python wrappers.
-    Timed on the host clock; each kernel is bracketed by HIP events on its
-    stream."""
+def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1,
+                  preps=2):
+    """Whole-path steps, pipelined.  `preps` host threads prepare the models
+    of consecutive steps at the same time: step k runs gts_prepare_model on
+    thread k mod preps, into pinned buffer k mod NB (NB = preps + 2), each
+    thread capped to its share of the cores (gts_set_host_threads).  The main
+    thread uploads step k's model on a copy stream into device buffer k mod NB
+    once it is prepared and launches the kernel of step k as soon as that
+    upload has finished, on compute stream k mod nstreams; the compute
+    streams hold only kernels, with no cross-stream waits.  The host orders buffer reuse: a preparation waits until the kernel
+    that last used its buffers has been launched and its upload has finished,
+    an upload for the kernel that last read its device buffer.  The loop
+    calls the C ABI with arguments marshalled once.  Timed on the host clock; each kernel is
+    bracketed by HIP events on its stream, each preparation by the host clock
+    of its thread."""
     import ctypes
+    import queue
+    import threading
     L = gts.lib()
     launch = L.gts_shap_interactions if interactions else L.gts_shap
+    NB = preps + 2
     computes = [torch.cuda.current_stream()] + [torch.cuda.Stream()
                                                 for _ in range(nstreams - 1)]
     copy = torch.cuda.Stream()
     desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
     nbytes = int(desc0.bytes)
-    pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(NBUF)]
-    dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(NBUF)]
-    copied = [torch.cuda.Event() for _ in range(NBUF)]    # upload from pinned[i] done
-    consumed = [torch.cuda.Event() for _ in range(NBUF)]  # kernel reading dev[i] done
+    pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(NB)]
+    dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(NB)]
+    copied = [torch.cuda.Event() for _ in range(NB)]    # upload from pinned[i] done
+    consumed = [torch.cuda.Event() for _ in range(NB)]  # kernel reading dev[i] done
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     ens_struct, keep = gts._ensemble_struct(ens)
-    descs = [gts.ModelDesc() for _ in range(NBUF)]
-    biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NBUF)]
+    descs = [gts.ModelDesc() for _ in range(NB)]
+    biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NB)]
     rows, M, G = Xd.shape[0], ens.num_features, ens.num_groups
     shape = (rows, G, M + 1, M + 1) if interactions else (rows, G, M + 1)
     outs = [torch.empty(shape, dtype=torch.float64 if dtype == "f64" else torch.float32,
                         device="cuda") for _ in range(nstreams)]
     prep_args = [(ctypes.byref(ens_struct), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
                   ctypes.byref(descs[i]), ctypes.c_void_p(pinned[i].data_ptr()), nbytes,
-                  biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NBUF)]
+                  biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NB)]
     run_args = [[(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
                   ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
                   ctypes.c_void_p(outs[j].data_ptr()), ctypes.c_void_p(computes[j].cuda_stream))
-                 for j in range(nstreams)] for i in range(NBUF)]
-    host_ms = []   # gts_prepare_model inside each timed step, host clock
+                 for j in range(nstreams)] for i in range(NB)]
+    cores = min(16, len(os.sched_getaffinity(0)))
+    share = 0 if preps == 1 else max(1, cores // preps)
 
-    def prepare_and_upload(k, timed):
-        i = k % NBUF
-        copied[i].synchronize()        # the upload of step k-3 has read pinned[i]
-        h0 = time.perf_counter()
-        st = L.gts_prepare_model(*prep_args[i])
-        if timed:
-            host_ms.append(1e3 * (time.perf_counter() - h0))
-        if st != gts.GTS_OK:
-            raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
-        consumed[i].synchronize()      # the kernel of step k-3 is done with dev[i]
-        with torch.cuda.stream(copy):
-            dev[i].copy_(pinned[i], non_blocking=True)
-            copied[i].record(copy)
+    # persistent preparation threads (their per-thread working memory stays
+    # warm between runs), each running the tasks of its queue in order
+    tasks = [queue.Queue() for _ in range(preps)]
 
-    def launch_kernel(k, timed):
-        i, j = k % NBUF, k % nstreams
-        stream = computes[j]
-        copied[i].synchronize()        # step k's model is in dev[i]
-        if timed:
-            ev[k][0].record(stream)
-        st = launch(*run_args[i][j])
-        if st != gts.GTS_OK:
-            raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
-        if timed:
-            ev[k][1].record(stream)
-        consumed[i].record(stream)
+    def worker(h):
+        L.gts_set_host_threads(share)
+        while True:
+            task = tasks[h].get()
+            if task is None:
+                return
+            task()
+
+    threads = [threading.Thread(target=worker, args=(h,), daemon=True) for h in range(preps)]
+    for t in threads:
+        t.start()
+
+    def wait_for(event):
+        # poll and sleep: a wait inside the runtime keeps a core busy, which
+        # the preparations need
+        while not event.query():
+            time.sleep(2e-5)
 
     def run_steps(n, timed):
         if n == 0:
-            return
-        for k in range(n):
-            prepare_and_upload(k, timed)
-            if k > 0:
-                launch_kernel(k - 1, timed)
-        launch_kernel(n - 1, timed)
+            return []
+        prepared = [threading.Event() for _ in range(n)]
+        launched = [threading.Event() for _ in range(n)]
+        host_ms = [0.0] * n
+        errors = []
 
-    # untimed: preparations for at least 0.3 s and back-to-back launches
-    # bring the host threads and the GPU clocks up before the warm-up steps
-    t_end = time.perf_counter() + 0.3
-    n_pre = 0
-    while n_pre < 2 or time.perf_counter() < t_end:
-        L.gts_prepare_model(*prep_args[0])
-        n_pre += 1
-    ref_model = gts.prepare(ens, dtype)
-    fn = kernel_fn(gts, interactions)
-    for _ in range(5):
-        fn(ref_model, Xd, out=outs[0])
-    torch.cuda.synchronize()
-    run_steps(warmup, False)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    run_steps(steps, True)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+        def prepare(k):
+            try:
+                i = k % NB
+                if k >= NB:
+                    launched[k - NB].wait()   # step k-NB's kernel launch has read descs[i]
+                    wait_for(copied[i])       # and its upload has read pinned[i]
+                h0 = time.perf_counter()
+                st = L.gts_prepare_model(*prep_args[i])
+                host_ms[k] = 1e3 * (time.perf_counter() - h0)
+                if st != gts.GTS_OK:
+                    raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
+            except BaseException as e:  # reported by the main thread
+                errors.append(e)
+            prepared[k].set()
+
+        for k in range(n):
+            tasks[k % preps].put(lambda k=k: prepare(k))
+        try:
+            # the main thread issues step k's upload once its model is
+            # prepared and its device buffer free, and launches step k's
+            # kernel once that upload has finished; between the two it polls
+            # and sleeps instead of blocking in the runtime
+            up = kl = 0
+            while kl < n:
+                busy = False
+                if errors:
+                    raise errors[0]
+                if up < n and prepared[up].is_set() and consumed[up % NB].query():
+                    i = up % NB
+                    with torch.cuda.stream(copy):
+                        dev[i].copy_(pinned[i], non_blocking=True)
+                        copied[i].record(copy)
+                    up += 1
+                    busy = True
+                if kl < up and copied[kl % NB].query():
+                    i, j = kl % NB, kl % nstreams
+                    stream = computes[j]
+                    if timed:
+                        ev[kl][0].record(stream)
+                    st = launch(*run_args[i][j])
+                    if st != gts.GTS_OK:
+                        raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
+                    if timed:
+                        ev[kl][1].record(stream)
+                    consumed[i].record(stream)
+                    launched[kl].set()
+                    kl += 1
+                    busy = True
+                if not busy:
+                    time.sleep(2e-5)
+        finally:
+            for e in launched:   # no preparation waits forever after an error
+                e.set()
+            for k in range(n):
+                prepared[k].wait()
+        return host_ms
+
+    def warm(h, t_end):
+        n_pre = 0
+        while n_pre < 2 or time.perf_counter() < t_end:
+            L.gts_prepare_model(*prep_args[h])
+            n_pre += 1
+
+    try:
+        # untimed: every preparation thread prepares for at least 0.3 s, and
+        # back-to-back launches bring the GPU clocks up, before the warm-up
+        # steps
+        done = [threading.Event() for _ in range(preps)]
+        t_end = time.perf_counter() + 0.3
+        for h in range(preps):
+            tasks[h].put(lambda h=h: (warm(h, t_end), done[h].set()))
+        ref_model = gts.prepare(ens, dtype)
+        fn = kernel_fn(gts, interactions)
+        for _ in range(5):
+            fn(ref_model, Xd, out=outs[0])
+        for d in done:
+            d.wait()
+        torch.cuda.synchronize()
+        run_steps(warmup, False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        host_ms = run_steps(steps, True)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    finally:
+        for q in tasks:
+            q.put(None)
+        for t in threads:
+            t.join()
     kern = np.array([a.elapsed_time(b) for a, b in ev])
     return wall, kern, outs[(steps - 1) % nstreams], ref_model, np.array(host_ms)
 
@@ -648,13 +716,15 @@ def main():
     ap.add_argument("--cpu-limit", type=float, default=4.0)
     ap.add_argument("--streams", type=int, default=1,
                     help="compute streams the pipelined steps alternate between")
+    ap.add_argument("--preps", type=int, default=2,
+                    help="model preparations in flight at once in the pipelined steps")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     ap.add_argument("--profile-launches", type=int, default=0,
                     help="only launch the kernel of --workload this many times (rocprofv3)")
     args = ap.parse_args()
-    if args.steps < 1 or args.warmup < 0 or args.streams < 1:
-        ap.error("--steps and --streams must be at least 1, --warmup at least 0")
+    if args.steps < 1 or args.warmup < 0 or args.streams < 1 or args.preps < 1:
+        ap.error("--steps, --streams and --preps must be at least 1, --warmup at least 0")
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; the row-sharded "
@@ -694,7 +764,8 @@ def main():
     Xd = torch.from_numpy(w.X).cuda()
 
     wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                                      args.warmup, inter, args.streams)
+                                                      args.warmup, inter, args.streams,
+                                                      args.preps)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)
@@ -723,8 +794,10 @@ def main():
                               + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": "extract + merge + bias + BFD pack (B=64) + layout (host) + upload "
                            + ("+ interaction kernel" if inter else "+ SHAP kernel")
-                           + "; host work of step k+1 and its upload overlap the kernel of step k",
-                   "compute_streams": args.streams},
+                           + f"; {args.preps} steps' host work in flight at once, each on "
+                           + "its share of the cores; uploads and host work overlap the "
+                           + "kernels of earlier steps",
+                   "compute_streams": args.streams, "preparations_in_flight": args.preps},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": traffic_for(key),

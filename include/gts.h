@@ -21,7 +21,8 @@
  *     No result depends on an earlier call; the host calls reuse a pool of
  *     worker threads (up to 16 and the process's cores; two fewer for calls
  *     under 128 k nodes when it has 8 or more; started on first use) and
- *     gts_prepare_model reuses per-thread working memory.
+ *     gts_prepare_model reuses per-thread working memory.  Calls from several
+ *     threads may run at once (gts_set_host_threads).
  *   - Every call returns a gts_status; on failure gts_last_error() returns a
  *     message for the calling thread (valid until that thread's next call).
  *   - A split sends x to the left child iff x < threshold; a path element
@@ -361,6 +362,21 @@ typedef struct gts_launch {
 
 gts_status gts_launch_config(const gts_model *model, int64_t rows, int32_t interactions,
                              gts_launch *out);
+
+/*
+ * gts_set_host_threads -- caps the host threads (the caller included) that
+ * the host calls made from the calling thread use: the tree walks and blob
+ * writing of gts_extract_paths, gts_pack_paths, gts_model_layout and
+ * gts_prepare_model.  n = 0 restores the default (every core of the
+ * process's affinity mask, up to 16).  The setting belongs to the calling
+ * thread and lasts until its next call.  For running several preparations
+ * at once, each on part of the cores (a pipeline that prepares the models
+ * of its next steps in parallel): calls from different threads run on
+ * different teams of the worker pool (up to four at once; a fifth runs on
+ * its caller alone).  Results never depend on the thread count.
+ * Errors: GTS_EINVAL for n < 0.
+ */
+gts_status gts_set_host_threads(int32_t n);
 
 /* Message describing the calling thread's most recent failure ("" if none). */
 const char *gts_last_error(void);

@@ -101,19 +101,22 @@ gts_status validate_ensemble(const gts_ensemble* e) {
 }
 
 // A small persistent pool of worker threads for the host passes (tree walks,
-// bin rotation).  run(n, body) calls body() on the caller and on up to n-1
+// blob writing).  run(n, body) calls body() on the caller and on up to n-1
 // workers at once; body pulls its work from a shared counter, so it is
-// correct with any number of participants.  One parallel region runs at a
-// time; a caller that finds the pool busy runs body() alone.  The pool is
-// never destroyed (its threads end with the process) and a forked child
-// starts a fresh one.
+// correct with any number of participants.  The workers form a few teams, and
+// one parallel region runs on a team at a time: calls from different threads
+// (several preparations in flight at once) take different teams, each with
+// its own workers.  A caller that finds every team busy runs body() alone.
+// The pool is never destroyed (its threads end with the process) and a forked
+// child starts a fresh one.
 //
 // A region is published as one atomic word (generation << 16 | workers
 // wanted).  Workers that have just finished a region poll that word for a
 // while (first with a pause instruction, then yielding the core) before they
 // block on the condition variable, so back-to-back regions -- a model
-// preparation runs two, a few hundred microseconds apart -- start without a
-// wake-up through the kernel; the caller polls the pending count the same way.
+// preparation runs several, a few hundred microseconds apart -- start without
+// a wake-up through the kernel; the caller polls the pending count the same
+// way.
 class Pool {
  public:
   static Pool& get() {
@@ -126,33 +129,18 @@ class Pool {
 
   template <typename Body>
   void run(int n, Body&& body) {
-    if (n <= 1 || !run_mu_.try_lock()) {
-      body();
-      return;
-    }
-    n = std::min(n, kMaxWorkers + 1);
-    std::function<void()> fn(std::ref(body));
-    bool wake;
-    {
-      std::lock_guard<std::mutex> lock(mu_);
-      while ((int)workers_.size() < n - 1) {
-        const int id = (int)workers_.size();
-        workers_.emplace_back([this, id] { loop(id); });
-        workers_.back().detach();
-      }
-      job_ = &fn;
-      pending_.store(n - 1, std::memory_order_relaxed);
-      gen_ += 1;
-      state_.store(gen_ << 16 | (uint64_t)(n - 1), std::memory_order_release);
-      wake = sleepers_ > 0;
-    }
-    if (wake) cv_.notify_all();
+    if (n > 1)
+      for (Team& t : teams_)
+        if (t.run_mu.try_lock()) {
+          t.run(std::min(n, kMaxWorkers + 1), body);
+          t.run_mu.unlock();
+          return;
+        }
     body();
-    for (int i = 0; pending_.load(std::memory_order_acquire) != 0; ++i) relax(i);
-    run_mu_.unlock();
   }
 
  private:
+  static constexpr int kTeams = 4;
   static constexpr int kMaxWorkers = 63;
   static constexpr int kPauseRounds = 2048;     // ~ tens of microseconds
   static constexpr int kYieldRounds = 4096;     // then yield the core, ~ a millisecond
@@ -176,38 +164,65 @@ class Pool {
     return m;
   }
 
-  void loop(int id) {
-    uint64_t seen = 0;
-    for (;;) {
-      uint64_t s = state_.load(std::memory_order_acquire);
-      for (int i = 0; (s >> 16) == seen && i < kPauseRounds + kYieldRounds; ++i) {
-        relax(i);
-        s = state_.load(std::memory_order_acquire);
-      }
-      if ((s >> 16) == seen) {
-        std::unique_lock<std::mutex> lock(mu_);
-        ++sleepers_;
-        cv_.wait(lock, [&] { return (state_.load(std::memory_order_relaxed) >> 16) != seen; });
-        --sleepers_;
-        s = state_.load(std::memory_order_relaxed);
-      }
-      seen = s >> 16;
-      // the region of generation `seen` cannot end (nor job_ change) before
-      // every worker it wants, this one included, has counted down
-      if (id >= (int)(s & 0xffff)) continue;
-      (*job_)();
-      pending_.fetch_sub(1, std::memory_order_release);
-    }
-  }
+  struct Team {
+    std::mutex run_mu;                  // held by the caller of a region
+    std::mutex mu;
+    std::condition_variable cv;
+    std::vector<std::thread> workers;   // under mu
+    const std::function<void()>* job = nullptr;
+    uint64_t gen = 0;                   // under mu
+    int sleepers = 0;                   // under mu
+    std::atomic<uint64_t> state{0};     // gen << 16 | workers wanted
+    std::atomic<int> pending{0};
 
-  std::mutex run_mu_, mu_;
-  std::condition_variable cv_;
-  std::vector<std::thread> workers_;
-  const std::function<void()>* job_ = nullptr;
-  uint64_t gen_ = 0;                  // under mu_
-  int sleepers_ = 0;                  // under mu_
-  std::atomic<uint64_t> state_{0};    // gen_ << 16 | workers wanted
-  std::atomic<int> pending_{0};
+    template <typename Body>
+    void run(int n, Body& body) {
+      std::function<void()> fn(std::ref(body));
+      bool wake;
+      {
+        std::lock_guard<std::mutex> lock(mu);
+        while ((int)workers.size() < n - 1) {
+          const int id = (int)workers.size();
+          workers.emplace_back([this, id] { loop(id); });
+          workers.back().detach();
+        }
+        job = &fn;
+        pending.store(n - 1, std::memory_order_relaxed);
+        gen += 1;
+        state.store(gen << 16 | (uint64_t)(n - 1), std::memory_order_release);
+        wake = sleepers > 0;
+      }
+      if (wake) cv.notify_all();
+      body();
+      for (int i = 0; pending.load(std::memory_order_acquire) != 0; ++i) relax(i);
+    }
+
+    void loop(int id) {
+      uint64_t seen = 0;
+      for (;;) {
+        uint64_t s = state.load(std::memory_order_acquire);
+        for (int i = 0; (s >> 16) == seen && i < kPauseRounds + kYieldRounds; ++i) {
+          relax(i);
+          s = state.load(std::memory_order_acquire);
+        }
+        if ((s >> 16) == seen) {
+          std::unique_lock<std::mutex> lock(mu);
+          ++sleepers;
+          cv.wait(lock, [&] { return (state.load(std::memory_order_relaxed) >> 16) != seen; });
+          --sleepers;
+          s = state.load(std::memory_order_relaxed);
+        }
+        seen = s >> 16;
+        // the region of generation `seen` cannot end (nor job change) before
+        // every worker it wants, this one included, has counted down
+        if (id >= (int)(s & 0xffff)) continue;
+        (*job)();
+        pending.fetch_sub(1, std::memory_order_release);
+      }
+    }
+  };
+
+  Team teams_[kTeams];
 };
 
 // Per-thread state for walking trees depth first.  The merged elements of the
@@ -456,8 +471,17 @@ int usable_cores() {
 // preparation's slowest tenth measured 40 % above its median.  A large one
 // takes every core: the deep model (646 k nodes) prepares in 4.5 ms on 16
 // threads against 5.0 ms on 14.
+//
+// gts_set_host_threads caps this for the calls of one thread: several
+// preparations in flight at once, each on part of the cores, prepare more
+// models per second than one at a time on all of them (the deep model: two
+// at once on 8 cores each, one every 3.6 ms; one on 16 cores, one every
+// 5.1 ms), because no single preparation uses 16 cores fully.
+thread_local int32_t t_thread_cap = 0;
+
 int host_threads(int64_t work) {
-  const int64_t cores = usable_cores();
+  int64_t cores = usable_cores();
+  if (t_thread_cap > 0) cores = std::min<int64_t>(cores, t_thread_cap);
   const int64_t hw = cores >= 8 && work < (int64_t(1) << 17) ? cores - 2 : cores;
   const int64_t by_work = (work + 1023) / 1024;
   return (int)std::max<int64_t>(1, std::min<int64_t>({hw, 16, by_work}));
@@ -492,6 +516,13 @@ extern "C" {
 const char* gts_last_error(void) { return g_error; }
 
 const char* gts_version(void) { return "gts 0.1 (gfx950)"; }
+
+gts_status gts_set_host_threads(int32_t n) {
+  clear_error();
+  if (n < 0) return fail(GTS_EINVAL, "n must be >= 0");
+  t_thread_cap = n;
+  return GTS_OK;
+}
 
 gts_status gts_extract_paths(const gts_ensemble* ens, gts_path_element* out,
                              int64_t capacity, int64_t* num_elements,
@@ -1331,8 +1362,42 @@ struct PrepareScratch {
   std::vector<int64_t> tree_first, chunk_start, key_start;
   std::vector<int32_t> size_at, key, grank, group_of_rank;
   std::vector<PathSrc> src_at, src_by_bin;   // per placement; per bin slot
+  std::vector<int32_t> kpos, d_at;           // per path: its placement; per placement: its offset
   Packing pk;
 };
+
+// Writes one path, the walker's current leaf, to its place in the blob (root
+// at element offset d, then its elements in device_order without rotation);
+// returns the product of the zero fractions as emit() does.
+template <typename Z>
+double put_path(const gts_model& m, char* blob, const Walker& w, size_t q, double v, int64_t d) {
+  using S = std::conditional_t<std::is_same_v<Z, float>, SplitF, Split>;
+  S el[kMaxPathLen];
+  const double prod = w.emit(el);
+  int32_t fs[kMaxPathLen], order[kMaxPathLen];
+  Z zs[kMaxPathLen];
+  for (size_t j = 0; j < q; ++j) {
+    fs[j] = el[j].feature;
+    zs[j] = (Z)el[j].zero_fraction;
+  }
+  const int32_t n0 = device_order(fs, zs, (int32_t)q, 0, nullptr, false, order);
+  int32_t* const feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]) + d;
+  float* const lower = reinterpret_cast<float*>(blob + m.off[kLower]) + d;
+  float* const upper = reinterpret_cast<float*>(blob + m.off[kUpper]) + d;
+  Z* const zero = reinterpret_cast<Z*>(blob + m.off[kZero]) + d;
+  feat[0] = -1 - n0;
+  lower[0] = -std::numeric_limits<float>::infinity();
+  upper[0] = std::numeric_limits<float>::infinity();
+  zero[0] = (Z)v;
+  for (size_t k = 0; k < q; ++k) {
+    const S& e = el[order[k]];
+    feat[k + 1] = e.feature;
+    lower[k + 1] = e.lower;
+    upper[k + 1] = e.upper;
+    zero[k + 1] = zs[order[k]];
+  }
+  return prod;
+}
 
 // Writes the paths of bin b into the blob, in the device order of
 // device_order (the choices rotate_bin makes, taken from the feature-sorted
@@ -1410,9 +1475,15 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
   try {
     const int64_t T = ens->num_trees;
     const bool sizes_only = host_blob == nullptr && bias == nullptr;
-    // one walk: every path's merged elements (only their count for a size
-    // query), per tree; the pool's workers write into the calling thread's
-    // scratch
+    // When every launch of the model runs one path per wave, a path's order
+    // in the blob does not depend on the other paths of its bin: the first
+    // walk then only counts, and a second walk after the packing writes every
+    // path straight to its place in the blob ("direct").  Otherwise one walk
+    // keeps every path's merged elements (only their count for a size query)
+    // per tree, and the bins are written from them.  The pool's workers write
+    // into the calling thread's scratch.
+    const bool direct = host_blob != nullptr && one_path_per_wave(ens->num_features, dtype);
+    const bool count_only = sizes_only || direct;
     static thread_local PrepareScratch tls;
     PrepareScratch& sc = tls;
     std::vector<TreeOut>& trees = sc.trees;
@@ -1421,7 +1492,7 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     for_each_tree(ens, status, [&](int64_t t, Walker& w) {
       TreeOut& out = trees[(size_t)t];
       out.clear();
-      if (sizes_only)
+      if (count_only)
         return w.walk<false>(ens, t, [&](int32_t, size_t m) {
           out.size.push_back((int32_t)m + 1);
           out.max_size = std::max(out.max_size, (int32_t)m + 1);
@@ -1535,7 +1606,9 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     }
     Packing& pk = sc.pk;
     std::vector<PathSrc>& src_at = sc.src_at;
-    if (!sizes_only) src_at.resize((size_t)P);
+    std::vector<int32_t>& kpos = sc.kpos;
+    if (direct) kpos.resize((size_t)P);
+    else if (!sizes_only) src_at.resize((size_t)P);
     {
       std::atomic<int64_t> next{0};
       Pool::get().run(sort_threads, [&]() {
@@ -1549,7 +1622,9 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
             int64_t p = tree_first[(size_t)t];
             for (size_t j = 0; j < sz.size(); ++j, ++p) {
               const int64_t k = pos[key[(size_t)p]]++;
-              if (!sizes_only)
+              if (direct)
+                kpos[(size_t)p] = (int32_t)k;
+              else if (!sizes_only)
                 src_at[(size_t)k] =
                     PathSrc{dtype == GTS_F64 ? (const void*)(tr.el.data.get() + tr.first[j])
                                              : (const void*)(tr.elf.data.get() + tr.first[j]),
@@ -1569,6 +1644,47 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     if (host_blob != nullptr && blob_capacity < bp.m.bytes)
       return fail(GTS_EBUFSIZE, "blob_capacity %lld < %lld bytes", (long long)blob_capacity,
                   (long long)bp.m.bytes);
+    char* blob = static_cast<char*>(host_blob);
+    if (direct) {
+      // every placement's element offset in the blob, from the fills
+      std::vector<int32_t>& d_at = sc.d_at;
+      d_at.resize((size_t)P);
+      {
+        const std::vector<Fill>& fills = pk.fills;
+        const int64_t nf = (int64_t)fills.size();
+        std::atomic<int64_t> next{0};
+        const int64_t step = std::max<int64_t>(1024, nf / (4 * nthreads) + 1);
+        Pool::get().run(nthreads, [&]() {
+          for (int64_t f0; (f0 = next.fetch_add(step)) < nf;) {
+            const int64_t f1 = std::min(nf, f0 + step);
+            for (int64_t f = f0; f < f1; ++f) {
+              const Fill& fl = fills[(size_t)f];
+              const int64_t b0 = pk.bin_offsets[(size_t)fl.b] + fl.w;
+              for (int32_t i = 0; i < fl.n; ++i)
+                d_at[(size_t)(fl.k + i)] = (int32_t)(b0 + (int64_t)i * fl.s);
+            }
+          }
+        });
+      }
+      zero_padding(bp, blob);
+      // the second walk: each leaf's path to its place, and the tree's
+      // bias terms in path order
+      for_each_tree(ens, status, [&](int64_t t, Walker& w) {
+        TreeOut& out = trees[(size_t)t];
+        out.term_sum = 0.0;
+        const int64_t base = ens->tree_node_offsets[t];
+        int64_t p = tree_first[(size_t)t];
+        return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
+          const double v = ens->value[base + leaf];
+          const int64_t d = d_at[(size_t)kpos[(size_t)p++]];
+          const double prod = dtype == GTS_F64 ? put_path<double>(bp.m, blob, w, m, v, d)
+                                               : put_path<float>(bp.m, blob, w, m, v, d);
+          out.term_sum = out.term_sum + v * prod;
+        });
+      });
+      for (int64_t t = 0; t < T; ++t)
+        if (status[(size_t)t] != GTS_OK) return status[(size_t)t];
+    }
     // bias: per-tree sums of the terms in path order, then per group in tree
     // order
     std::vector<double> bsum((size_t)ens->num_groups, 0.0);
@@ -1577,8 +1693,7 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
                                          trees[(size_t)t].term_sum;
     if (bias)
       for (int32_t g = 0; g < ens->num_groups; ++g) bias[g] = bsum[(size_t)g];
-    char* blob = static_cast<char*>(host_blob);
-    if (blob) {
+    if (blob && !direct) {
       zero_padding(bp, blob);
       const int64_t K = pk.K;
       // each bin's paths in placement order, with their offsets in the bin
@@ -1622,8 +1737,9 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
           }
         }
       });
-      write_bins_and_bias(bp, blob, pk.bin_offsets.data(), pk.bin_group.data(), bsum.data());
     }
+    if (blob)
+      write_bins_and_bias(bp, blob, pk.bin_offsets.data(), pk.bin_group.data(), bsum.data());
     return GTS_OK;
   } catch (const std::bad_alloc&) {
     return fail(GTS_ENOMEM, "host allocation failed");

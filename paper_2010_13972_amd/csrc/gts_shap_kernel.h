@@ -138,6 +138,15 @@ struct Launch {
   int32_t sorted;      // 1: inside a bin, paths never grow in length
 };
 
+// Makes v a value the compiler must hold in registers at this point, so the
+// code that computes it stays on every lane's path: a select between it and
+// another value then costs one v_cndmask instead of a divergent branch around
+// its computation.
+template <typename T>
+__device__ __forceinline__ void keep(T& v) {
+  asm volatile("" : "+v"(v));
+}
+
 // Shapley weight of a coalition of size k among the other n-1 players:
 // k! (n-1-k)! / n!  =  1 / (n * C(n-1, k)).
 __host__ __device__ constexpr double shapley_weight(int n, int k) {
@@ -220,12 +229,14 @@ __device__ __forceinline__ void tile_add(T* const (&p)[N], const T (&val)[N], co
                                    Bits<T>::of(Bits<T>::val(old[i]) + val[i]))
                        : old[i];
     } else {
+      // every lane swaps, so no lane branches around its swap: an entry that
+      // is off adds -0.0, which leaves every value as it is (-0.0 included)
 #pragma unroll
       for (int i = 0; i < N; ++i) {
+        const T add = on[i] ? val[i] : T(-0.0);
         old[i] = *reinterpret_cast<const U*>(p[i]);
-        got[i] = on[i] ? atomicCAS(reinterpret_cast<U*>(p[i]), old[i],
-                                   Bits<T>::of(Bits<T>::val(old[i]) + val[i]))
-                       : old[i];
+        got[i] = atomicCAS(reinterpret_cast<U*>(p[i]), old[i],
+                           Bits<T>::of(Bits<T>::val(old[i]) + add));
       }
     }
     bool retry = false;
@@ -234,7 +245,7 @@ __device__ __forceinline__ void tile_add(T* const (&p)[N], const T (&val)[N], co
     if (retry) {
 #pragma unroll
       for (int i = 0; i < N; ++i)
-        if (got[i] != old[i]) lds_add(p[i], val[i]);
+        if (got[i] != old[i]) lds_add(p[i], on[i] ? val[i] : T(-0.0));
     }
   }
 }
@@ -460,7 +471,12 @@ __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q],
     T s = G[Q - 1];
 #pragma unroll
     for (int m = Q - 2; m >= 0; --m) s = fma(-z[i], s, G[m]);
-    val[i] = o[i] ? w[i] * s : neg_vt;
+    T a = w[i] * s;
+    // several paths per wave: the lanes rarely agree on o_i, so a branch
+    // around the Horner evaluation only adds its cost (one path per wave:
+    // whole waves often have o_i = 0 and skip it)
+    if constexpr (MODE == kPaired) keep(a);
+    val[i] = o[i] ? a : neg_vt;
     p[i] = prow + f[i];
   }
   tile_add<MODE>(p, val, on);

@@ -107,6 +107,8 @@ def lib() -> ctypes.CDLL:
         L.gts_launch_config.argtypes = [ctypes.POINTER(ModelDesc), i64, i32,
                                         ctypes.POINTER(LaunchInfo)]
         L.gts_launch_config.restype = st
+        L.gts_set_host_threads.argtypes = [i32]
+        L.gts_set_host_threads.restype = st
         L.gts_last_error.restype = ctypes.c_char_p
         L.gts_version.restype = ctypes.c_char_p
         _lib = L
@@ -115,6 +117,12 @@ def lib() -> ctypes.CDLL:
 
 def last_error() -> str:
     return lib().gts_last_error().decode()
+
+
+def set_host_threads(n: int):
+    """gts_set_host_threads: cap the host threads of the calling thread's
+    library calls (0: every core, up to 16)."""
+    _check(lib().gts_set_host_threads(int(n)), "gts_set_host_threads")
 
 
 def version() -> str:

@@ -4,9 +4,13 @@
 // current directory and, for every packing heuristic, two bin capacities and
 // both dtypes, prepares the model twice (size query, then the blob) and
 // compares the blob byte for byte with the three-call route
-// extract -> pack -> layout.  Exit status 0 only if every case matches.
+// extract -> pack -> layout.  Then three threads with different thread caps
+// (gts_set_host_threads) prepare the BFD model at the same time, several
+// times each, and every blob must equal the one-at-a-time blob.  Exit status
+// 0 only if every case matches.
 #include <cstdio>
 #include <cstdlib>
+#include <thread>
 #include <vector>
 
 #include "gts.h"
@@ -65,5 +69,33 @@ int main() {
                     same ? "same" : "DIFFERENT");
         if (!same) ++bad;
       }
+  for (int dt : {GTS_F32, GTS_F64}) {
+    gts_model m;
+    if (gts_prepare_model(&e, 64, GTS_PACK_BFD, dt, &m, nullptr, 0, nullptr) != GTS_OK) {
+      ++bad;
+      continue;
+    }
+    std::vector<char> want((size_t)m.bytes);
+    std::vector<double> want_bias((size_t)G);
+    gts_prepare_model(&e, 64, GTS_PACK_BFD, dt, &m, want.data(), m.bytes, want_bias.data());
+    int wrong[3] = {0, 0, 0};
+    std::vector<std::thread> th;
+    for (int k = 0; k < 3; ++k)
+      th.emplace_back([&, k] {
+        gts_set_host_threads(k == 0 ? 4 : k == 1 ? 2 : 0);
+        for (int r = 0; r < 4; ++r) {
+          gts_model mk;
+          std::vector<char> blob((size_t)m.bytes);
+          std::vector<double> bias((size_t)G);
+          const gts_status st = gts_prepare_model(&e, 64, GTS_PACK_BFD, dt, &mk, blob.data(),
+                                                  m.bytes, bias.data());
+          if (st != GTS_OK || blob != want || bias != want_bias) ++wrong[k];
+        }
+      });
+    for (auto& t : th) t.join();
+    const bool same = wrong[0] + wrong[1] + wrong[2] == 0;
+    std::printf("concurrent dtype %d %s\n", dt, same ? "same" : "DIFFERENT");
+    if (!same) ++bad;
+  }
   return bad == 0 ? 0 : 1;
 }

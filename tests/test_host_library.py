@@ -361,9 +361,10 @@ def test_prepare_model_equals_the_three_step_route(name, dtype, alg):
 
 def test_prepare_model_from_concurrent_threads():
     """Preparations from several threads at once (ctypes releases the GIL;
-    the worker pool serves one caller at a time and the others run alone,
-    each in its own scratch) give the blobs of one-at-a-time calls, also when
-    one thread alternates between models of different sizes."""
+    up to four callers run on their own teams of the worker pool, the others
+    alone, each in its own scratch, with per-thread caps on the thread count)
+    give the blobs of one-at-a-time calls, also when one thread alternates
+    between models of different sizes."""
     import threading
     names = ["covtype_med", "wide", "random0", "tiny"]
     ens = {n: _workload(n).ensemble for n in names}
@@ -373,8 +374,11 @@ def test_prepare_model_from_concurrent_threads():
         want[n] = (bytes(d), b.tobytes(), bias.tobytes())
     errors = []
 
+    caps = [0, 1, 2, 3, 8, 16]
+
     def work(k):
         try:
+            gts.set_host_threads(caps[k])
             for r in range(6):
                 n = names[(k + r) % len(names)]
                 d, b, bias = gts.prepare_blob(ens[n], "f32")
@@ -389,6 +393,31 @@ def test_prepare_model_from_concurrent_threads():
     for t in threads:
         t.join()
     assert errors == []
+
+
+def test_host_thread_cap():
+    """gts_set_host_threads: results do not depend on the cap; a negative cap
+    is an error; the cap belongs to the calling thread."""
+    import threading
+    w = _workload("covtype_med")
+    want = gts.prepare_blob(w.ensemble, "f64")
+    try:
+        for cap in (1, 2, 5, 0):
+            gts.set_host_threads(cap)
+            d, b, bias = gts.prepare_blob(w.ensemble, "f64")
+            assert bytes(d) == bytes(want[0]) and b.tobytes() == want[1].tobytes()
+            assert bias.tobytes() == want[2].tobytes()
+        with pytest.raises(gts.GtsError) as e:
+            gts.set_host_threads(-1)
+        assert e.value.status == gts.GTS_EINVAL
+        gts.set_host_threads(1)
+        seen = []
+        t = threading.Thread(target=lambda: seen.append(gts.prepare_blob(w.ensemble, "f64")))
+        t.start()
+        t.join()
+        assert seen[0][1].tobytes() == want[1].tobytes()
+    finally:
+        gts.set_host_threads(0)
 
 
 def test_prepare_model_errors():

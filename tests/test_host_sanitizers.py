@@ -3,9 +3,10 @@
 tests/native/host_check.cpp is compiled with gts_host.cpp by g++ with
 AddressSanitizer + UndefinedBehaviorSanitizer, and separately with
 ThreadSanitizer (the worker pool, the parallel walks, the parallel sort and
-the parallel blob writers).  It prepares models of seeded ensembles for every
-packing heuristic and compares them with the three-call route.  Any
-sanitizer report or mismatch fails the test.
+the parallel blob writers, preparations from three threads at once).  It
+prepares models of seeded ensembles for every packing heuristic and compares
+them with the three-call route, and compares concurrent preparations with
+one-at-a-time ones.  Any sanitizer report or mismatch fails the test.
 """
 import os
 import shutil
@@ -74,3 +75,4 @@ def test_host_library_under_sanitizers(tmp_path, kind, flags):
         assert res.returncode == 0, f"{kind} {name}:\n{report[-3000:]}"
         assert "runtime error" not in report and "WARNING: ThreadSanitizer" not in report, report
         assert report.count("same") >= 8, report
+        assert report.count("concurrent") == 2 and "DIFFERENT" not in report, report
