@@ -86,11 +86,11 @@ SUITE = [
 # SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
 # summaries and the commands that made them are in profiles/.
 COUNTERS = {
-    ('deep', 'f32', False): {"fetch_bytes": 63790077, "write_bytes": 46080000, "valu_insts": 2115768783, "salu_insts": 1464665563, "lds_insts": 270237834, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
-    ('deep', 'f64', False): {"fetch_bytes": 73738864, "write_bytes": 92160000, "valu_insts": 2196190953, "salu_insts": 1442430166, "lds_insts": 290040856, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
-    ('covtype_med', 'f32', False): {"fetch_bytes": 19350772, "write_bytes": 35200000, "valu_insts": 283140291, "salu_insts": 84670654, "lds_insts": 42375069, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
-    ('wide', 'f32', False): {"fetch_bytes": 6193401739, "write_bytes": 316800000, "valu_insts": 5420836828, "salu_insts": 1413132152, "lds_insts": 765195913, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
-    ('interactions', 'f32', True): {"fetch_bytes": 17194684, "write_bytes": 60894374, "valu_insts": 184076128, "salu_insts": 34502649, "lds_insts": 16024014, "source": "c728735ed131a003968bd7a91a43bb28c54b6778c6672132eba5c594c4435ce1"},
+    ('deep', 'f32', False): {"fetch_bytes": 63787351, "write_bytes": 46080000, "valu_insts": 2121882188, "salu_insts": 1454097538, "lds_insts": 269538176, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
+    ('deep', 'f64', False): {"fetch_bytes": 73737331, "write_bytes": 92160000, "valu_insts": 2208411815, "salu_insts": 1429312252, "lds_insts": 290045733, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
+    ('covtype_med', 'f32', False): {"fetch_bytes": 19347737, "write_bytes": 35200000, "valu_insts": 288889013, "salu_insts": 73736997, "lds_insts": 41729165, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
+    ('wide', 'f32', False): {"fetch_bytes": 6043624588, "write_bytes": 316800000, "valu_insts": 5548757236, "salu_insts": 1071712477, "lds_insts": 764326190, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
+    ('interactions', 'f32', True): {"fetch_bytes": 5181096, "write_bytes": 48400000, "valu_insts": 181897185, "salu_insts": 31372059, "lds_insts": 16052090, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
 }
 
 
