@@ -123,7 +123,13 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
     }
   }
   if (RW == 0) return fail(GTS_EINVAL, "M = %d needs more LDS than a workgroup has", M);
-  const size_t lds = need(RW, waves, priv);
+  size_t lds = need(RW, waves, priv);
+  // rank tables for the bin-wide dead-pair test of one-path-per-wave launches
+  size_t rank_off = 0;
+  if (RW == 64 && priv && M <= kRankMaxM) {
+    rank_off = (lds + 7) & ~(size_t)7;
+    lds = rank_off + rank_table_bytes(M);
+  }
   // Bin slices per (row tile, group) when there are too few tiles to fill
   // the GPU.  Every slice adds its tile to phi atomically, so a slice costs
   // rows x width atomic adds.  SHAP values (short phi rows): enough
@@ -159,6 +165,7 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
   plan.sp = sp;
   plan.width = width;
   plan.lds = lds;
+  plan.rank_off = rank_off;
   plan.splits = splits;
   plan.tiles = tiles;
   // the kernel variant: the model's longest path, in features

@@ -22,6 +22,15 @@ constexpr int kQShort = 8;
 constexpr int kQMid = 12;
 constexpr int kQLong = 64;
 
+// Private-tile launches (64-row tiles, one path per wave) of models with at
+// most this many features keep rank tables of the row tile in LDS: per feature, the 64 row
+// keys in ascending order and, for every rank, the mask of the rows below it.
+// They serve the dead-pair test of a whole bin at once.
+constexpr int kRankMaxM = 16;
+inline size_t rank_table_bytes(int M) {
+  return (size_t)M * 65 * sizeof(uint64_t) + (size_t)M * 64 * sizeof(int32_t);
+}
+
 // The launch shape of a model and row count: rows per tile, waves, private
 // tiles, LDS strides and bytes, bin slices, and the kernel variant.
 struct Plan {
@@ -33,6 +42,7 @@ struct Plan {
   int splits = 1;
   int64_t tiles = 0;
   int qmax = kQLong;
+  size_t rank_off = 0;   // LDS offset of the rank tables (0: none)
 };
 
 // Arguments of one gts_shap / gts_shap_interactions call.

@@ -136,6 +136,7 @@ struct Launch {
   int32_t width;     // phi entries per (row, group): M+1 or (M+1)^2
   int32_t accumulate;  // 1: atomically add the tile to phi (phi pre-zeroed)
   int32_t sorted;      // 1: inside a bin, paths never grow in length
+  int32_t rank_off;    // LDS offset of the rank tables; 0: none
 };
 
 // Makes v a value the compiler must hold in registers at this point, so the
@@ -747,6 +748,94 @@ __device__ __forceinline__ bool wave_live(const Bin<T>& b, int rl, int n0,
   return true;
 }
 
+// Rank tables of a 64-row tile, per feature f < M: keys[f][p] = the p-th
+// smallest row key (ties in row order) and below[f][p] = the mask of the rows
+// of ranks < p (p = 0..64).  The rows whose key lies in [klo, khi) are then
+// below[f][c] & ~below[f][a] with a, c the numbers of keys < klo and < khi.
+// Wave w builds the tables of features w, w + WAVES, ...
+struct RankTables {
+  uint64_t* below;   // [M][65]
+  int* keys;         // [M][64]
+  __device__ RankTables(unsigned char* base, int M)
+      : below(reinterpret_cast<uint64_t*>(base)),
+        keys(reinterpret_cast<int*>(base + (size_t)M * 65 * sizeof(uint64_t))) {}
+};
+
+template <int WAVES>
+__device__ void build_ranks(const int* xs, int sx, int M, RankTables rt, int wave, int lane) {
+  for (int f = wave; f < M; f += WAVES) {
+    const int kx = xs[lane * sx + f];
+    int rank = 0;
+#pragma unroll 16
+    for (int j = 0; j < 64; ++j) {
+      const int kj = __builtin_amdgcn_readlane(kx, j);
+      rank += (kj < kx || (kj == kx && j < lane)) ? 1 : 0;
+    }
+    rt.keys[f * 64 + rank] = kx;
+    // lane p takes the row of rank p; the masks are an inclusive OR-scan of
+    // the rows' bits in rank order
+    const int row = __builtin_amdgcn_ds_permute(rank * 4, lane);
+    unsigned lo = row < 32 ? 1u << row : 0u;
+    unsigned hi = row >= 32 ? 1u << (row - 32) : 0u;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const unsigned ulo = __shfl_up(lo, d);
+      const unsigned uhi = __shfl_up(hi, d);
+      if (lane >= d) {
+        lo |= ulo;
+        hi |= uhi;
+      }
+    }
+    rt.below[f * 65 + lane + 1] = (uint64_t)hi << 32 | lo;
+    if (lane == 0) rt.below[f * 65] = 0;
+  }
+}
+
+// Roots of the bin's paths that some row of the tile reaches: every lane
+// holding a zero-fraction element finds the rows inside its range from the
+// rank tables (two binary searches), and each root lane intersects the row
+// sets of its path's zero-fraction elements (stored right after it).  The
+// same test as wave_live, for all paths of the bin at once.
+template <typename T, int QMAX>
+__device__ __forceinline__ uint64_t live_roots(const Bin<T>& b, int lane, uint64_t roots,
+                                               int info, RankTables rt) {
+  uint64_t rows = ~0ull;
+  if (lane < b.len && b.feat >= 0 && b.z == T(0)) {
+    const int* ks = rt.keys + b.feat * 64;
+    const int klo = b.klo;
+    const int khi = (int)((unsigned)b.klo + b.span);
+    int a = 0, c = 0;
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+      a += ks[a + s - 1] < klo ? s : 0;
+      c += ks[c + s - 1] < khi ? s : 0;
+    }
+    a += ks[a] < klo ? 1 : 0;
+    c += ks[c] < khi ? 1 : 0;
+    rows = rt.below[b.feat * 65 + c] & ~rt.below[b.feat * 65 + a];
+  }
+  const bool root = (roots >> lane) & 1ull;
+  const int n0 = root ? info >> 8 : 0;
+  unsigned lo = ~0u, hi = ~0u;
+  const unsigned rlo = (unsigned)rows, rhi = (unsigned)(rows >> 32);
+  auto step = [&](int k) {
+    const unsigned mlo = __shfl_down(rlo, k);
+    const unsigned mhi = __shfl_down(rhi, k);
+    if (k <= n0) {
+      lo &= mlo;
+      hi &= mhi;
+    }
+  };
+  if constexpr (QMAX < kQLong) {
+#pragma unroll 2
+    for (int k = 1; k <= QMAX; ++k) step(k);
+  } else {
+    const int kmax = wave_max_small(n0);
+    for (int k = 1; k <= kmax; ++k) step(k);
+  }
+  return __ballot(root && (info & 0xff) > 0 && (lo | hi) != 0u);
+}
+
 // All paths of one bin.  RW == 64: one path at a time for the whole wave,
 // skipped when no row of the tile reaches its zero-fraction ranges.  RW < 64:
 // rounds of up to P = 64/RW paths, lane (j, r) = (path j, row r).  (Finding
@@ -755,21 +844,23 @@ __device__ __forceinline__ bool wave_live(const Bin<T>& b, int rl, int n0,
 // rounds, and the test of every path costs more than that saves.)
 template <typename T, int RW, bool INTER, bool EXCL, int QMAX>
 __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>& b, int lane,
-                                            const int* xrow, T* prow, int stride, bool sorted) {
+                                            const int* xrow, T* prow, int stride, bool sorted,
+                                            bool ranked, RankTables rt) {
   uint64_t roots;
   int info;
   const int nroots = stage_bin(st, b, lane, roots, info);
   if constexpr (RW == 64) {
     // paths from the roots' ballot, each word from its root lane; in the
-    // ungapped stage, slot = lane
-    uint64_t rest = roots;
+    // ungapped stage, slot = lane.  With rank tables the live paths are
+    // known for the whole bin at once.
+    uint64_t rest = ranked ? live_roots<T, QMAX>(b, lane, roots, info, rt) : roots;
     while (rest != 0) {
       const int rl = __builtin_ctzll(rest);
       rest &= rest - 1ull;
       const int word = __builtin_amdgcn_readlane(info, rl);
       const int q = word & 0xff;
       const int n0 = word >> 8;
-      if (q > 0 && (n0 == 0 || wave_live(b, rl, n0, xrow)))
+      if (ranked || (q > 0 && (n0 == 0 || wave_live(b, rl, n0, xrow))))
         dispatch<T, true, INTER, EXCL ? kExclusive : kBatched, false, QMAX>(q, st, rl, q, xrow,
                                                                              prow, stride);
     }
@@ -843,6 +934,14 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  // rank tables: only the private-tile launches (one path per wave, small
+  // M) have them, so the other variants carry none of their code
+  const bool ranked = PRIV && RW == 64 && L.rank_off > 0;
+  const RankTables rt(smem + L.rank_off, M);
+  if (ranked) {
+    build_ranks<WAVES>(xs, L.sx, M, rt, wave, lane);
+    __syncthreads();
+  }
   const int r = lane % RW;
   init_stage(stages + wave, lane);
   // Slice s takes every splits-th bin of the group.  Bins come longest paths
@@ -863,7 +962,7 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
       const int bn = bi + WAVES * b_step;
       if (bn < gb1) nxt = load_bin(d, bn, lane);
       process_bin<T, RW, INTER, PRIV && RW == 64, QMAX>(stages + wave, cur, lane, xrow, prow,
-                                                        stride, L.sorted != 0);
+                                                        stride, L.sorted != 0, ranked, rt);
       cur = nxt;
     }
   }
@@ -919,6 +1018,7 @@ gts_status launch_rw(const KernelArgs& a, const Plan& p) {
   L.width = p.width;
   L.accumulate = p.splits > 1 ? 1 : 0;
   L.sorted = (m->flags & GTS_MODEL_SORTED_BINS) ? 1 : 0;
+  L.rank_off = (int32_t)p.rank_off;
   const int64_t total = a.rows * (int64_t)m->num_groups * p.width;
   if (L.accumulate) {
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 65536);

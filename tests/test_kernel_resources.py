@@ -60,10 +60,16 @@ def test_fp32_shap_short_variants_use_no_scratch():
             assert x["scratch"] == 0, x
 
 
-def test_headline_variants_fit_eight_waves_per_simd():
+def test_headline_variants_fit_their_occupancy():
     """The fp32 SHAP kernels for paths of at most 8 features with 64-row
-    tiles (the deep, covtype-shaped and tiny workloads) stay within 64
-    registers."""
+    tiles: the shared-tile variant (covtype-shaped workload) stays within 64
+    registers (8 waves per SIMD); the private-tile variant (deep and tiny
+    workloads), whose rank tables hold a workgroup to 24 KB of LDS and so a
+    CU to 6 workgroups of 4 waves, within 80 (6 waves per SIMD)."""
+    seen = 0
     for x in variants():
         if x["dtype"] == "f" and not x["inter"] and x["qmax"] == 8 and x["rw"] == 64:
-            assert x["vgprs"] <= 64 and x["scratch"] == 0, x
+            cap = 80 if x["priv"] else 64
+            assert x["vgprs"] <= cap and x["scratch"] == 0, x
+            seen += 1
+    assert seen == 2
