@@ -239,7 +239,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     calls the C ABI with arguments marshalled once.  Timed on the host clock; each kernel is
     bracketed by HIP events on its stream, each preparation by the host clock
     of its thread."""
+    import collections
     import ctypes
+    import gc
     import queue
     import threading
     L = gts.lib()
@@ -300,6 +302,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
             return []
         prepared = [threading.Event() for _ in range(n)]
         launched = [threading.Event() for _ in range(n)]
+        ready = collections.deque()   # prepared steps, in the order they finish
         host_ms = [0.0] * n
         errors = []
 
@@ -316,40 +319,46 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                     raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
             except BaseException as e:  # reported by the main thread
                 errors.append(e)
+            ready.append(k)
             prepared[k].set()
 
         for k in range(n):
             tasks[k % preps].put(lambda k=k: prepare(k))
         try:
-            # the main thread issues step k's upload once its model is
-            # prepared and its device buffer free, and launches step k's
-            # kernel once that upload has finished; between the two it polls
-            # and sleeps instead of blocking in the runtime
-            up = kl = 0
-            while kl < n:
+            # the main thread uploads every prepared step (in the order the
+            # preparations finish) once its device buffer is free, and
+            # launches each uploaded step once its upload has finished; it
+            # polls and sleeps instead of blocking in the runtime.  (A step's
+            # device buffer is free once the kernel of step k - NB is done:
+            # that kernel was launched before step k's preparation began.)
+            uploaded = collections.deque()
+            done = 0
+            while done < n:
                 busy = False
                 if errors:
                     raise errors[0]
-                if up < n and prepared[up].is_set() and consumed[up % NB].query():
-                    i = up % NB
+                while ready and consumed[ready[0] % NB].query():
+                    k = ready.popleft()
+                    i = k % NB
                     with torch.cuda.stream(copy):
                         dev[i].copy_(pinned[i], non_blocking=True)
                         copied[i].record(copy)
-                    up += 1
+                    uploaded.append(k)
                     busy = True
-                if kl < up and copied[kl % NB].query():
-                    i, j = kl % NB, kl % nstreams
+                while uploaded and copied[uploaded[0] % NB].query():
+                    k = uploaded.popleft()
+                    i, j = k % NB, k % nstreams
                     stream = computes[j]
                     if timed:
-                        ev[kl][0].record(stream)
+                        ev[k][0].record(stream)
                     st = launch(*run_args[i][j])
                     if st != gts.GTS_OK:
                         raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
                     if timed:
-                        ev[kl][1].record(stream)
+                        ev[k][1].record(stream)
                     consumed[i].record(stream)
-                    launched[kl].set()
-                    kl += 1
+                    launched[k].set()
+                    done += 1
                     busy = True
                 if not busy:
                     time.sleep(2e-5)
@@ -360,26 +369,26 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                 prepared[k].wait()
         return host_ms
 
-    def warm(h, t_end):
-        n_pre = 0
-        while n_pre < 2 or time.perf_counter() < t_end:
-            L.gts_prepare_model(*prep_args[h])
-            n_pre += 1
-
+    # no garbage collection while steps run: a collection holds the
+    # interpreter lock for tens of milliseconds, which stalls the threads
+    # that return from the library
+    gc_was_on = gc.isenabled()
+    gc.collect()
+    gc.disable()
     try:
-        # untimed: every preparation thread prepares for at least 0.3 s, and
-        # back-to-back launches bring the GPU clocks up, before the warm-up
-        # steps
-        done = [threading.Event() for _ in range(preps)]
-        t_end = time.perf_counter() + 0.3
-        for h in range(preps):
-            tasks[h].put(lambda h=h: (warm(h, t_end), done[h].set()))
+        # untimed: back-to-back launches, then pipelined steps for at least
+        # 0.5 s (host threads, copies and GPU clocks in the state of the timed
+        # steps), before the warm-up steps
         ref_model = gts.prepare(ens, dtype)
         fn = kernel_fn(gts, interactions)
         for _ in range(5):
             fn(ref_model, Xd, out=outs[0])
-        for d in done:
-            d.wait()
+        torch.cuda.synchronize()
+        t_end = time.perf_counter() + 0.5
+        while True:
+            run_steps(2 * NB, False)
+            if time.perf_counter() >= t_end:
+                break
         torch.cuda.synchronize()
         run_steps(warmup, False)
         torch.cuda.synchronize()
@@ -388,6 +397,8 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
     finally:
+        if gc_was_on:
+            gc.enable()
         for q in tasks:
             q.put(None)
         for t in threads:
