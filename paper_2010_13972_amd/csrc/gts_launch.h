@@ -28,7 +28,7 @@ constexpr int kQLong = 64;
 // They serve the dead-pair test of a whole bin at once.
 constexpr int kRankMaxM = 16;
 inline size_t rank_table_bytes(int M) {
-  return (size_t)M * 65 * sizeof(uint64_t) + (size_t)M * 64 * sizeof(int32_t);
+  return (size_t)M * 65 * (sizeof(uint64_t) + sizeof(int32_t));
 }
 
 // The launch shape of a model and row count: rows per tile, waves, private
