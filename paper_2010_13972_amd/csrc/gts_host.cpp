@@ -347,18 +347,19 @@ struct Walker {
   }
 
   // Depth-first walk of tree t, left child (x < t) first, validating every
-  // node it reaches.  Calls leaf(node, m) with m merged elements (with EMIT,
-  // emit() gives them; without EMIT only m is computed).  The stack holds
-  // nodes still to visit, each with the undo depth of its parent's path: a
-  // visit first unwinds the path to that depth, then enters the split from
-  // the parent (range from the parent's threshold and the side, zero
-  // fraction child cover / parent cover).
-  template <bool EMIT, typename LeafFn>
+  // node it reaches (without CHECK, for a tree an earlier walk has
+  // validated, no node is checked).  Calls leaf(node, m) with m merged
+  // elements (with EMIT, emit() gives them; without EMIT only m is
+  // computed).  The stack holds nodes still to visit, each with the undo
+  // depth of its parent's path: a visit first unwinds the path to that depth,
+  // then enters the split from the parent (range from the parent's threshold
+  // and the side, zero fraction child cover / parent cover).
+  template <bool EMIT, bool CHECK = true, typename LeafFn>
   gts_status walk(const gts_ensemble* e, int64_t t, LeafFn&& leaf) {
     const int64_t base = e->tree_node_offsets[t];
     const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
     reset(e->num_features, n);
-    seen.assign((size_t)n, 0);
+    if (CHECK) seen.assign((size_t)n, 0);
     const int32_t* const left = e->left + base;
     const int32_t* const right = e->right + base;
     const int32_t* const feature = e->feature + base;
@@ -383,25 +384,32 @@ struct Walker {
         push<EMIT>(ud++, feature[parent], is_right ? th : -inf, is_right ? inf : th,
                    EMIT ? cover_ratio(cover[node], cover[parent]) : 0.0);
       }
-      if (seen[(size_t)node]) {
-        status = fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
-                      (long long)t, node);
-        break;
-      }
-      seen[(size_t)node] = 1;
-      const double r = cover[node];
-      if (!(r >= 0.0) || !std::isfinite(r)) {
-        status = fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
-                      (long long)t, node);
-        break;
-      }
       const int32_t a = left[node], b = right[node];
+      if (CHECK) {
+        if (seen[(size_t)node]) {
+          status = fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
+                        (long long)t, node);
+          break;
+        }
+        seen[(size_t)node] = 1;
+        const double r = cover[node];
+        if (!(r >= 0.0) || !std::isfinite(r)) {
+          status = fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
+                        (long long)t, node);
+          break;
+        }
+      }
       if (a < 0 && b < 0) {
-        if (!std::isfinite(value[node])) {
+        if (CHECK && !std::isfinite(value[node])) {
           status = fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
           break;
         }
         leaf(node, active_count());
+        continue;
+      }
+      if (!CHECK) {
+        st[sp++] = Frame{b, node * 2 + 1, ud};
+        st[sp++] = Frame{a, node * 2, ud};
         continue;
       }
       if (a < 0 || b < 0 || a >= n || b >= n) {
@@ -1674,7 +1682,7 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
         out.term_sum = 0.0;
         const int64_t base = ens->tree_node_offsets[t];
         int64_t p = tree_first[(size_t)t];
-        return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
+        return w.walk<true, false>(ens, t, [&](int32_t leaf, size_t m) {
           const double v = ens->value[base + leaf];
           const int64_t d = d_at[(size_t)kpos[(size_t)p++]];
           const double prod = dtype == GTS_F64 ? put_path<double>(bp.m, blob, w, m, v, d)
