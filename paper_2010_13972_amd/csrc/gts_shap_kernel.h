@@ -345,26 +345,42 @@ __device__ __forceinline__ void init_stage(Stage<T, GAPPED>* st, int lane) {
   }
 }
 
-// Stages a bin; returns its number of paths, sets `roots` to the lanes of
-// its root elements and, on a root lane, `info` to the path's features | its
-// zero-fraction elements << 8.
+// Where the paths of a bin start: roots = the lanes of its root elements,
+// rl = this lane's root, len = on a root lane, the path's elements, n0 = on
+// a root lane, its zero-fraction elements (stored first), info = (len - 1) |
+// (n0 << 8).
+struct BinIndex {
+  uint64_t roots;
+  int rl, len, n0, info;
+  bool root;
+};
+
+template <typename T>
+__device__ __forceinline__ BinIndex index_bin(const Bin<T>& b, int lane) {
+  BinIndex ix;
+  ix.root = lane < b.len && b.feat < 0;
+  ix.n0 = ix.root ? -1 - b.feat : 0;
+  ix.roots = __ballot(ix.root);
+  const uint64_t upto = ix.roots & ((2ull << lane) - 1ull);      // roots at or below this lane
+  ix.rl = upto ? 63 - __clzll((long long)upto) : lane;
+  const uint64_t above = ix.roots & ~((2ull << lane) - 1ull);
+  ix.len = (above ? __builtin_ctzll(above) : b.len) - lane;
+  ix.info = (ix.len - 1) | (ix.n0 << 8);
+  return ix;
+}
+
+// Stages a bin (indexed by index_bin); returns its number of paths.  On a
+// root lane, info holds the path's features | its zero-fraction elements << 8.
 template <typename T, bool GAPPED>
 __device__ __forceinline__ int stage_bin(Stage<T, GAPPED>* st, const Bin<T>& b, int lane,
-                                         uint64_t& roots, int& info) {
-  const bool root = lane < b.len && b.feat < 0;
-  const int n0 = root ? -1 - b.feat : 0;   // zero-fraction elements, stored first
-  roots = __ballot(root);
-  const uint64_t upto = roots & ((2ull << lane) - 1ull);      // roots at or below this lane
-  const int rl = upto ? 63 - __clzll((long long)upto) : lane;  // this element's root
-  const uint64_t above = roots & ~((2ull << lane) - 1ull);
-  const int len = (above ? __builtin_ctzll(above) : b.len) - lane;  // path length, on a root
+                                         const BinIndex& ix) {
   int slot = lane;
   if constexpr (GAPPED) {
-    const uint64_t evens = __ballot(root && (len & 1) == 0);
-    slot += __popcll(evens & ((1ull << rl) - 1ull));
+    const uint64_t evens = __ballot(ix.root && (ix.len & 1) == 0);
+    slot += __popcll(evens & ((1ull << ix.rl) - 1ull));
   }
-  const T v = __shfl(b.z, rl);   // a root's zero-fraction slot holds v
-  const T w = root ? v : v * (T(1) - b.z);
+  const T v = __shfl(b.z, ix.rl);   // a root's zero-fraction slot holds v
+  const T w = ix.root ? v : v * (T(1) - b.z);
   st->head[slot] = make_int4(b.feat, b.klo, (int)b.span,
                              sizeof(T) == 4 ? __float_as_int((float)b.z) : 0);
   typename Stage<T, GAPPED>::AuxT ax{};
@@ -375,15 +391,14 @@ __device__ __forceinline__ int stage_bin(Stage<T, GAPPED>* st, const Bin<T>& b, 
     ax.w = w;
   }
   st->aux[slot] = ax;
-  const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(roots >> 32),
-                                             __builtin_amdgcn_mbcnt_lo((unsigned)roots, 0u));
-  info = (len - 1) | (n0 << 8);
-  if (root) st->path[rank] = slot | (info << 8);
+  const int rank = __builtin_amdgcn_mbcnt_hi((unsigned)(ix.roots >> 32),
+                                             __builtin_amdgcn_mbcnt_lo((unsigned)ix.roots, 0u));
+  if (ix.root) st->path[rank] = slot | (ix.info << 8);
   // the stores above are read by other lanes of this wave only
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  return __popcll(roots);
+  return __popcll(ix.roots);
 }
 
 // Fields of a staged path word.
@@ -816,25 +831,24 @@ __device__ __forceinline__ uint64_t live_roots(const Bin<T>& b, int lane, uint64
     c += ks[c] < khi ? 1 : 0;
     rows = rt.below[b.feat * 65 + c] & ~rt.below[b.feat * 65 + a];
   }
-  const bool root = (roots >> lane) & 1ull;
-  const int n0 = root ? info >> 8 : 0;
-  unsigned lo = ~0u, hi = ~0u;
-  const unsigned rlo = (unsigned)rows, rhi = (unsigned)(rows >> 32);
-  auto step = [&](int k) {
-    const unsigned mlo = __shfl_down(rlo, k);
-    const unsigned mhi = __shfl_down(rhi, k);
-    if (k <= n0) {
-      lo &= mlo;
-      hi &= mhi;
+  // AND over each path's lanes (its root and its non-zero-fraction
+  // elements hold all ones): a segmented suffix scan, steps of 1, 2, 4, ...
+  // lanes while no root lies in between; four steps cover paths of up to 16
+  // elements
+  unsigned lo = (unsigned)rows, hi = (unsigned)(rows >> 32);
+  const uint64_t later = lane < 63 ? roots >> (lane + 1) : 0ull;   // roots above this lane
+  constexpr int kSteps = QMAX < kQLong ? 4 : 6;
+#pragma unroll
+  for (int t = 0; t < kSteps; ++t) {
+    const int d = 1 << t;
+    const unsigned nlo = __shfl_down(lo, d);
+    const unsigned nhi = __shfl_down(hi, d);
+    if ((later & ((1ull << d) - 1ull)) == 0) {
+      lo &= nlo;
+      hi &= nhi;
     }
-  };
-  if constexpr (QMAX < kQLong) {
-#pragma unroll 2
-    for (int k = 1; k <= QMAX; ++k) step(k);
-  } else {
-    const int kmax = wave_max_small(n0);
-    for (int k = 1; k <= kmax; ++k) step(k);
   }
+  const bool root = (roots >> lane) & 1ull;
   return __ballot(root && (info & 0xff) > 0 && (lo | hi) != 0u);
 }
 
@@ -848,14 +862,20 @@ template <typename T, int RW, bool INTER, bool EXCL, int QMAX>
 __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>& b, int lane,
                                             const int* xrow, T* prow, int stride, bool sorted,
                                             bool ranked, RankTables rt) {
-  uint64_t roots;
-  int info;
-  const int nroots = stage_bin(st, b, lane, roots, info);
+  const BinIndex ix = index_bin(b, lane);
+  const uint64_t roots = ix.roots;
+  const int info = ix.info;
   if constexpr (RW == 64) {
     // paths from the roots' ballot, each word from its root lane; in the
     // ungapped stage, slot = lane.  With rank tables the live paths are
-    // known for the whole bin at once.
-    uint64_t rest = ranked ? live_roots<T, QMAX>(b, lane, roots, info, rt) : roots;
+    // known for the whole bin at once, before staging: a bin with none is
+    // not staged at all.
+    uint64_t rest = roots;
+    if (ranked) {
+      rest = live_roots<T, QMAX>(b, lane, roots, info, rt);
+      if (rest == 0) return;
+    }
+    stage_bin(st, b, lane, ix);
     while (rest != 0) {
       const int rl = __builtin_ctzll(rest);
       rest &= rest - 1ull;
@@ -869,7 +889,7 @@ __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>&
   } else {
     constexpr int P = 64 / RW;
     const int j = lane / RW;
-    const int npaths = nroots;
+    const int npaths = stage_bin(st, b, lane, ix);
     for (int base = 0; base < npaths; base += P) {
       const int t = base + j;
       const bool valid = t < npaths;
