@@ -441,6 +441,69 @@ struct Walker {
     clean = true;
     return status;
   }
+
+  // walk() without values for up to 64 features: each stack frame carries
+  // the mask of the features on its path, so a leaf's merged element count
+  // is a popcount (no per-feature state, no undo).  The same node checks,
+  // messages and leaf order as walk().
+  struct MaskFrame {
+    int32_t node;
+    uint64_t mask;
+  };
+  std::vector<MaskFrame> mstack;
+
+  template <typename LeafFn>
+  gts_status count_walk(const gts_ensemble* e, int64_t t, LeafFn&& leaf) {
+    const int64_t base = e->tree_node_offsets[t];
+    const int32_t n = (int32_t)(e->tree_node_offsets[t + 1] - base);
+    if (mstack.size() < (size_t)n + 1) mstack.resize((size_t)n + 1);
+    seen.assign((size_t)n, 0);
+    const int32_t* const left = e->left + base;
+    const int32_t* const right = e->right + base;
+    const int32_t* const feature = e->feature + base;
+    const float* const threshold = e->threshold + base;
+    const double* const cover = e->cover + base;
+    const double* const value = e->value + base;
+    const int32_t M = e->num_features;
+    MaskFrame* const st = mstack.data();
+    int32_t sp = 0;
+    st[sp++] = MaskFrame{0, 0};
+    while (sp > 0) {
+      const MaskFrame fr = st[--sp];
+      const int32_t node = fr.node;
+      if (seen[(size_t)node])
+        return fail(GTS_EINVAL, "tree %lld: node %d reached twice (cycle or shared child)",
+                    (long long)t, node);
+      seen[(size_t)node] = 1;
+      const double r = cover[node];
+      if (!(r >= 0.0) || !std::isfinite(r))
+        return fail(GTS_EINVAL, "tree %lld node %d: cover must be finite and >= 0",
+                    (long long)t, node);
+      const int32_t a = left[node], b = right[node];
+      if (a < 0 && b < 0) {
+        if (!std::isfinite(value[node]))
+          return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
+        leaf(node, (size_t)__builtin_popcountll(fr.mask));
+        continue;
+      }
+      if (a < 0 || b < 0 || a >= n || b >= n)
+        return fail(GTS_EINVAL, "tree %lld node %d: child index out of range", (long long)t,
+                    node);
+      const int32_t d = feature[node];
+      if (d < 0 || d >= M)
+        return fail(GTS_EINVAL, "tree %lld node %d: feature %d outside [0, %d)", (long long)t,
+                    node, d, M);
+      if (std::isnan(threshold[node]))
+        return fail(GTS_EINVAL, "tree %lld node %d: threshold is NaN", (long long)t, node);
+      if (sp + 2 > (int32_t)mstack.size())
+        return fail(GTS_EINVAL, "tree %lld node %d: node reached twice (cycle or shared child)",
+                    (long long)t, node);
+      const uint64_t m = fr.mask | 1ull << d;
+      st[sp++] = MaskFrame{b, m};
+      st[sp++] = MaskFrame{a, m};
+    }
+    return GTS_OK;
+  }
 };
 
 // The bias of each output group from the paths' terms v * prod(z): every
@@ -1500,12 +1563,14 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     for_each_tree(ens, status, [&](int64_t t, Walker& w) {
       TreeOut& out = trees[(size_t)t];
       out.clear();
-      if (count_only)
-        return w.walk<false>(ens, t, [&](int32_t, size_t m) {
+      if (count_only) {
+        auto count = [&](int32_t, size_t m) {
           out.size.push_back((int32_t)m + 1);
           out.max_size = std::max(out.max_size, (int32_t)m + 1);
           out.elements += (int64_t)m + 1;
-        });
+        };
+        return ens->num_features <= 64 ? w.count_walk(ens, t, count) : w.walk<false>(ens, t, count);
+      }
       const int64_t base = ens->tree_node_offsets[t];
       return w.walk<true>(ens, t, [&](int32_t leaf, size_t m) {
         const double v = ens->value[base + leaf];
