@@ -86,11 +86,11 @@ SUITE = [
 # SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
 # summaries and the commands that made them are in profiles/.
 COUNTERS = {
-    ('deep', 'f32', False): {"fetch_bytes": 63787351, "write_bytes": 46080000, "valu_insts": 2121882188, "salu_insts": 1454097538, "lds_insts": 269538176, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
-    ('deep', 'f64', False): {"fetch_bytes": 73737331, "write_bytes": 92160000, "valu_insts": 2208411815, "salu_insts": 1429312252, "lds_insts": 290045733, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
-    ('covtype_med', 'f32', False): {"fetch_bytes": 19347737, "write_bytes": 35200000, "valu_insts": 288889013, "salu_insts": 73736997, "lds_insts": 41729165, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
-    ('wide', 'f32', False): {"fetch_bytes": 6043624588, "write_bytes": 316800000, "valu_insts": 5548757236, "salu_insts": 1071712477, "lds_insts": 764326190, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
-    ('interactions', 'f32', True): {"fetch_bytes": 5181096, "write_bytes": 48400000, "valu_insts": 181897185, "salu_insts": 31372059, "lds_insts": 16052090, "source": "1eda4286623449d6195f6f6c75af79c8839a2f7f394255644a93d98d19368f53"},
+    ('deep', 'f32', False): {"fetch_bytes": 63847869, "write_bytes": 46080000, "valu_insts": 1787416579, "salu_insts": 347553710, "lds_insts": 276472423, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
+    ('deep', 'f64', False): {"fetch_bytes": 73797500, "write_bytes": 92160000, "valu_insts": 1878131998, "salu_insts": 322768424, "lds_insts": 292643883, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
+    ('covtype_med', 'f32', False): {"fetch_bytes": 19346723, "write_bytes": 35200000, "valu_insts": 288899270, "salu_insts": 73787612, "lds_insts": 41735930, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
+    ('wide', 'f32', False): {"fetch_bytes": 6115901275, "write_bytes": 316800000, "valu_insts": 5548767961, "salu_insts": 1071719369, "lds_insts": 764330674, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
+    ('interactions', 'f32', True): {"fetch_bytes": 5176066, "write_bytes": 48400000, "valu_insts": 181888728, "salu_insts": 31361013, "lds_insts": 16047992, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
 }
 
 
