@@ -911,10 +911,11 @@ __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>&
 // slice s of that group (every splits-th bin, starting at bin s).  PRIV: every wave accumulates into a phi tile of its
 // own (summed when the tile is written), so waves never contend; with one
 // path per wave (RW == 64) the accumulation then needs no atomics.
-// Workgroups are dealt to the 8 XCDs round-robin; when the (group, slice)
+// Workgroups are dealt to the 8 XCDs round-robin.  When the (group, slice)
 // units divide evenly among the XCDs, consecutive workgroups on an XCD take
-// the same unit for successive row tiles, so each XCD's L2 holds only its own
-// share of the model's bins.
+// the same unit for successive row tiles; otherwise each XCD takes a
+// contiguous run of the (unit, tile) pairs.  Either way each XCD's L2 holds
+// only its own share of the model's bins.
 template <typename T, int RW, bool INTER, int WAVES, bool PRIV, int QMAX>
 __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const float* __restrict__ X,
                                                          T* __restrict__ phi, Launch L) {
@@ -931,8 +932,10 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
     tile = local % L.tiles;
     u = (int)(b & 7) + 8 * (int)(local / L.tiles);
   } else {
-    tile = b / U;
-    u = (int)(b % U);
+    // unit-major: the XCDs work through one unit's row tiles together, so
+    // each L2 holds the bins of about one unit at a time
+    tile = b % L.tiles;
+    u = (int)(b / L.tiles);
   }
   const int g = u / L.splits;
   const int s = u - g * L.splits;
