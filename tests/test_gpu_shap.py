@@ -154,6 +154,46 @@ def test_special_models(torch, orc):
         assert np.all(got[:, 0, 2] == 0.0)  # feature 2 never used
 
 
+@pytest.mark.parametrize("M", [16, 17])
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+def test_rank_table_feature_limit(torch, orc, M, dtype):
+    """One-path-per-wave launches with private tiles test a whole bin for
+    dead (row, path) pairs from rank tables of the row tile when M <= 16, and
+    path by path above: 16 and 17 features, zero-cover splits and rows tied
+    on four values, 150 rows (three 64-row tiles, the last ragged)."""
+    w = synth.random_workload(60 + M, num_trees=14, max_depth=7, M=M, n_bg=30, rows=150)
+    model = gts.prepare(w.ensemble, dtype)
+    cfg = gts.launch_config(model, 150)
+    say("rank tables", M, dtype, cfg)
+    assert cfg["rows_per_tile"] == 64 and cfg["private_tiles"] == 1
+    got = run_shap(torch, w.ensemble, w.X, dtype)
+    assert_parity(got, orc.treeshap(w.ensemble, w.X), dtype, what=f"M={M} {dtype}")
+
+
+def test_bins_without_live_paths(torch, orc):
+    """Trees whose right subtree has zero cover: its paths carry two
+    zero-fraction elements, and rows with x0 < 0.5 reach none of them, so
+    whole bins of these (longer) paths are dead for whole tiles and are not
+    staged; the left paths (cover 10 of 10) stay live.  Rows with x0 >= 0.5 in
+    a later tile make some of them live there."""
+    rng = np.random.default_rng(7)
+    trees = []
+    for t in range(60):
+        f1 = 1 + t % 7
+        trees.append([(1, 2, 0, 0.5, 10.0, 0.0), (-1, -1, -1, 0, 10.0, float(rng.normal())),
+                      (3, 4, f1, 0.25 + 0.5 * rng.random(), 0.0, 0.0),
+                      (-1, -1, -1, 0, 0.0, float(rng.normal())),
+                      (-1, -1, -1, 0, 0.0, float(rng.normal()))])
+    ens = synth.ensemble_from_lists(trees, M=8)
+    X = rng.uniform(0, 0.5, size=(200, 8)).astype(np.float32)
+    X[128:, 0] = rng.uniform(0.5, 1.0, size=72)   # the third and fourth tiles reach the right subtrees
+    for dtype in ("f32", "f64"):
+        got = run_shap(torch, ens, X, dtype)
+        want = orc.treeshap(ens, X)
+        assert_parity(got, want, dtype, what="dead bins")
+        assert np.all(got[:128, 0, 1:8] == 0.0)  # no live path splits on f1..f7 there
+
+
 def empty_ensemble(M, G):
     return synth.Ensemble(
         num_features=M, num_groups=G, tree_node_offsets=np.zeros(1, np.int64),
