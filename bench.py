@@ -86,11 +86,11 @@ SUITE = [
 # SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
 # summaries and the commands that made them are in profiles/.
 COUNTERS = {
-    ('deep', 'f32', False): {"fetch_bytes": 63847869, "write_bytes": 46080000, "valu_insts": 1787416579, "salu_insts": 347553710, "lds_insts": 276472423, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
-    ('deep', 'f64', False): {"fetch_bytes": 73797500, "write_bytes": 92160000, "valu_insts": 1878131998, "salu_insts": 322768424, "lds_insts": 292643883, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
-    ('covtype_med', 'f32', False): {"fetch_bytes": 19346723, "write_bytes": 35200000, "valu_insts": 288899270, "salu_insts": 73787612, "lds_insts": 41735930, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
-    ('wide', 'f32', False): {"fetch_bytes": 6115901275, "write_bytes": 316800000, "valu_insts": 5548767961, "salu_insts": 1071719369, "lds_insts": 764330674, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
-    ('interactions', 'f32', True): {"fetch_bytes": 5176066, "write_bytes": 48400000, "valu_insts": 181888728, "salu_insts": 31361013, "lds_insts": 16047992, "source": "523f02b896e900512458dbc8dca02a5e20bb5f58f2c70a1da0e41aba886ad8a5"},
+    ('deep', 'f32', False): {"fetch_bytes": 63844068, "write_bytes": 46080000, "valu_insts": 1787738115, "salu_insts": 347553710, "lds_insts": 276472423, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
+    ('deep', 'f64', False): {"fetch_bytes": 73798073, "write_bytes": 92160000, "valu_insts": 1878453534, "salu_insts": 322768424, "lds_insts": 292643883, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
+    ('covtype_med', 'f32', False): {"fetch_bytes": 19347765, "write_bytes": 35200000, "valu_insts": 288921726, "salu_insts": 73891934, "lds_insts": 41750631, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
+    ('wide', 'f32', False): {"fetch_bytes": 416313822, "write_bytes": 316800000, "valu_insts": 5548918571, "salu_insts": 1074743240, "lds_insts": 764848748, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
+    ('interactions', 'f32', True): {"fetch_bytes": 11161428, "write_bytes": 48400000, "valu_insts": 181898070, "salu_insts": 31402109, "lds_insts": 16053095, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
 }
 
 
