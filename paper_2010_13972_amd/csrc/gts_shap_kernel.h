@@ -26,9 +26,11 @@
 // z + o t = 0 for every row outside its range, so such a (row, path) has all
 // weights 0 and contributes exactly nothing (the zero-cover pruning of
 // Algorithm 1).  The host stores those elements first in their path and their
-// count in the root; a wave tests them before anything else and skips a path
-// that no row of its tile reaches (RW == 64), or leaves it out of the rounds
-// (RW < 64).
+// count in the root.  With one path per wave (RW == 64) a wave skips every
+// path that no row of its tile reaches: for models of at most 16 features it
+// finds them for a whole bin at once, before staging it, from rank tables of
+// the tile's row keys; otherwise it tests each path's elements in turn.  The
+// multi-path rounds (RW < 64) compute every pair.
 //
 // Arithmetic.  EXTEND keeps permutation weights w_k, which are the
 // coefficients E_k of prod_k (z_k + o_k t) scaled by k!(l-k)!/(l+1)!.  The
@@ -908,14 +910,15 @@ __device__ __forceinline__ void process_bin(Stage<T, RW < 64>* st, const Bin<T>&
 }
 
 // One workgroup: rows [tile*RW, tile*RW + RW) of output group g, bins of
-// slice s of that group (every splits-th bin, starting at bin s).  PRIV: every wave accumulates into a phi tile of its
-// own (summed when the tile is written), so waves never contend; with one
-// path per wave (RW == 64) the accumulation then needs no atomics.
-// Workgroups are dealt to the 8 XCDs round-robin.  When the (group, slice)
-// units divide evenly among the XCDs, consecutive workgroups on an XCD take
-// the same unit for successive row tiles; otherwise each XCD takes a
-// contiguous run of the (unit, tile) pairs.  Either way each XCD's L2 holds
-// only its own share of the model's bins.
+// slice s of that group (every splits-th bin, starting at bin s).  PRIV:
+// every wave accumulates into a phi tile of its own (summed when the tile is
+// written), so waves never contend; with one path per wave (RW == 64) the
+// accumulation then needs no atomics.  Workgroups are dealt to the 8 XCDs
+// round-robin.  When the (group, slice) units divide evenly among the XCDs,
+// consecutive workgroups on an XCD take the same unit for successive row
+// tiles; otherwise the grid is unit-major, all XCDs working through one
+// unit's row tiles together.  Either way each XCD's L2 holds about one
+// unit's bins at a time.
 template <typename T, int RW, bool INTER, int WAVES, bool PRIV, int QMAX>
 __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const float* __restrict__ X,
                                                          T* __restrict__ phi, Launch L) {
