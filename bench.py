@@ -727,15 +727,16 @@ def main():
     ap.add_argument("--cpu-limit", type=float, default=4.0)
     ap.add_argument("--streams", type=int, default=1,
                     help="compute streams the pipelined steps alternate between")
-    ap.add_argument("--preps", type=int, default=2,
-                    help="model preparations in flight at once in the pipelined steps")
+    ap.add_argument("--preps", type=int, default=0,
+                    help="model preparations in flight at once in the pipelined steps "
+                         "(0: two for models of 128 k nodes or more, else one)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     ap.add_argument("--profile-launches", type=int, default=0,
                     help="only launch the kernel of --workload this many times (rocprofv3)")
     args = ap.parse_args()
-    if args.steps < 1 or args.warmup < 0 or args.streams < 1 or args.preps < 1:
-        ap.error("--steps, --streams and --preps must be at least 1, --warmup at least 0")
+    if args.steps < 1 or args.warmup < 0 or args.streams < 1 or args.preps < 0:
+        ap.error("--steps and --streams must be at least 1, --warmup and --preps at least 0")
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; the row-sharded "
@@ -774,9 +775,11 @@ def main():
     rows = w.X.shape[0]
     Xd = torch.from_numpy(w.X).cuda()
 
+    # a large model's preparation does not use 16 cores fully: two in flight
+    # on 8 cores each prepare more models per second; a small one's does
+    preps = args.preps or (2 if ens.num_nodes >= (1 << 17) else 1)
     wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                                      args.warmup, inter, args.streams,
-                                                      args.preps)
+                                                      args.warmup, inter, args.streams, preps)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)
@@ -805,10 +808,10 @@ def main():
                               + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": "extract + merge + bias + BFD pack (B=64) + layout (host) + upload "
                            + ("+ interaction kernel" if inter else "+ SHAP kernel")
-                           + f"; {args.preps} steps' host work in flight at once, each on "
+                           + f"; {preps} steps' host work in flight at once, each on "
                            + "its share of the cores; uploads and host work overlap the "
                            + "kernels of earlier steps",
-                   "compute_streams": args.streams, "preparations_in_flight": args.preps},
+                   "compute_streams": args.streams, "preparations_in_flight": preps},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": traffic_for(key),
