@@ -294,9 +294,10 @@ gts_status gts_prepare_model(const gts_ensemble *ens, int32_t bin_capacity, int3
  * each element and a sum), evaluated per (row, path) over the packed bins
  * of Section 3.4.  A (row, path) with an element of zero fraction whose range
  * misses the row contributes exactly nothing (Algorithm 1 prunes such
- * subtrees) and may be skipped.  The kernels for paths longer than 12
+ * subtrees) and may be skipped.  The kernels for paths longer than 16
  * features use per-lane private memory that the HIP runtime provides with
- * the launch; the others use none of their own beyond LDS.
+ * the launch; the others use none of their own beyond LDS and, at the
+ * tightest register caps, a few words of register spills.
  *
  * model    host descriptor from gts_model_layout.
  * d_model  device copy of the blob.

@@ -172,7 +172,8 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
   const int qmax = std::max(0, m->max_path_len - 1);
   plan.qmax = qmax <= kQShort ? kQShort
               : (!INTER && qmax <= kMaxUnrolledShap) ? kQMid
-                                                     : kQLong;
+              : (!INTER && qmax <= kMaxUnrolledShapF64) ? kQExt
+                                                        : kQLong;
   return GTS_OK;
 }
 

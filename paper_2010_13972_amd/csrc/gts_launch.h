@@ -15,11 +15,16 @@ namespace gts {
 // per-lane private memory; only the long-path kernel variants contain it.
 constexpr int kMaxUnrolledShap = 12;
 constexpr int kMaxUnrolledInter = 8;
+// SHAP paths of 13-16 features run unrolled code in fp64 arithmetic (the
+// fp32 G-form loses accuracy beyond 12), for either model dtype.
+constexpr int kMaxUnrolledShapF64 = 16;
 
 // Kernel variant by the model's longest path: every path has at most 8
-// features, at most 12, or any length up to a full bin (63).
+// features, at most 12, at most 16 (SHAP values only), or any length up to a
+// full bin (63).
 constexpr int kQShort = 8;
 constexpr int kQMid = 12;
+constexpr int kQExt = 16;
 constexpr int kQLong = 64;
 
 // Private-tile launches (64-row tiles, one path per wave) of models with at

@@ -15,12 +15,13 @@
 // RW == 64 all lanes share one path and read its elements from the staging
 // area at the same address (an LDS broadcast); with fewer rows per wave each
 // group of RW lanes reads its own path's elements.  Trip counts are
-// compile-time constants (one variant per path length up to 12 features, 8
+// compile-time constants (one variant per path length up to 16 features, 8
 // for interactions), so a wave never diverges on path length.  This does the
 // q^2 work of a path once per row instead of spreading it over q lanes that
 // then need q shuffles each.  Each kernel is built for the model's longest
-// path: up to 8 features, up to 12, or longer; only the last holds the
-// runtime-loop code for long paths and its per-lane private arrays.
+// path: up to 8 features, up to 12, up to 16 (fp64 arithmetic), or longer;
+// only the last holds the runtime-loop code for long paths and its per-lane
+// private arrays.
 //
 // Dead pairs.  An element whose zero fraction is 0 gives the factor
 // z + o t = 0 for every row outside its range, so such a (row, path) has all
@@ -465,36 +466,40 @@ __device__ __forceinline__ void unwind_one(const T (&E)[Q + 1], T zi, T (&D)[Q])
 // sum_k c_k D^i_k = sum_m (-z_i)^m G_m with G_m = sum_{j>m} c_{j-1-m} E_j.
 // phi[f_i] += v (1 - z_i) * that sum when o_i = 1, and -v sum_k c_k E_k
 // when o_i = 0.
-template <typename T, int Q, AddMode MODE>
+// C: the arithmetic's type (T, or double for paths of 13-16 features).
+template <typename T, int Q, AddMode MODE, typename C = T>
 __device__ __forceinline__ void shap_math(const int (&f)[Q], const bool (&o)[Q], const T (&z)[Q],
                                           const T (&w)[Q], const bool (&on)[Q], T v,
                                           T* __restrict__ prow) {
-  T E[Q + 1];
-  extend_all<T, Q>(o, z, E);
-  T t_all = T(0);
+  C zc[Q];
 #pragma unroll
-  for (int k = 0; k < Q; ++k) t_all = fma(T(shapley_weight(Q, k)), E[k], t_all);
-  T G[Q];
+  for (int k = 0; k < Q; ++k) zc[k] = C(z[k]);
+  C E[Q + 1];
+  extend_all<C, Q>(o, zc, E);
+  C t_all = C(0);
+#pragma unroll
+  for (int k = 0; k < Q; ++k) t_all = fma(C(shapley_weight(Q, k)), E[k], t_all);
+  C G[Q];
 #pragma unroll
   for (int m = 0; m < Q; ++m) {
-    G[m] = T(shapley_weight(Q, Q - 1 - m)) * E[Q];
+    G[m] = C(shapley_weight(Q, Q - 1 - m)) * E[Q];
 #pragma unroll
-    for (int j = Q - 1; j > m; --j) G[m] = fma(T(shapley_weight(Q, j - 1 - m)), E[j], G[m]);
+    for (int j = Q - 1; j > m; --j) G[m] = fma(C(shapley_weight(Q, j - 1 - m)), E[j], G[m]);
   }
-  const T neg_vt = -v * t_all;
+  const C neg_vt = -C(v) * t_all;
   T* p[Q];
   T val[Q];
 #pragma unroll
   for (int i = 0; i < Q; ++i) {
-    T s = G[Q - 1];
+    C s = G[Q - 1];
 #pragma unroll
-    for (int m = Q - 2; m >= 0; --m) s = fma(-z[i], s, G[m]);
-    T a = w[i] * s;
+    for (int m = Q - 2; m >= 0; --m) s = fma(-zc[i], s, G[m]);
+    C a = C(w[i]) * s;
     // several paths per wave: the lanes rarely agree on o_i, so a branch
     // around the Horner evaluation only adds its cost (one path per wave:
     // whole waves often have o_i = 0 and skip it)
     if constexpr (MODE == kPaired) keep(a);
-    val[i] = o[i] ? a : neg_vt;
+    val[i] = T(o[i] ? a : neg_vt);
     p[i] = prow + f[i];
   }
   tile_add<MODE>(p, val, on);
@@ -679,7 +684,7 @@ __device__ void path_dyn(const Stage<T, GAPPED>* st, int s, int q, const int* __
   }
 }
 
-template <typename T, int Q, bool UNIFORM, bool INTER, AddMode MODE, bool GAPPED>
+template <typename T, int Q, bool UNIFORM, bool INTER, AddMode MODE, bool GAPPED, typename C = T>
 __device__ __forceinline__ void path_fixed(const Stage<T, GAPPED>* st, int s, int q,
                                            const int* __restrict__ xrow, T* __restrict__ prow,
                                            int stride) {
@@ -689,7 +694,7 @@ __device__ __forceinline__ void path_fixed(const Stage<T, GAPPED>* st, int s, in
   load_path<T, Q, UNIFORM, GAPPED>(st, s, q, xrow, f, o, z, w, on);
   const T v = st->w(s);
   if constexpr (INTER) inter_math<T, Q, MODE>(f, o, z, w, on, v, prow, stride);
-  else shap_math<T, Q, MODE>(f, o, z, w, on, v, prow);
+  else shap_math<T, Q, MODE, C>(f, o, z, w, on, v, prow);
 }
 
 // Q = features of the longest path in the wave's current set (uniform); q =
@@ -698,10 +703,14 @@ __device__ __forceinline__ void path_fixed(const Stage<T, GAPPED>* st, int s, in
 template <typename T, bool UNIFORM, bool INTER, AddMode MODE, bool GAPPED, int QMAX>
 __device__ __forceinline__ void dispatch(int Q, const Stage<T, GAPPED>* st, int s, int q,
                                          const int* xrow, T* prow, int stride) {
-  static_assert(kMaxUnrolledShap == 12 && kMaxUnrolledInter == 8, "update the case lists");
-  static_assert(QMAX == kQShort || QMAX == kQMid || QMAX == kQLong, "unknown variant");
+  static_assert(kMaxUnrolledShap == 12 && kMaxUnrolledShapF64 == 16 && kMaxUnrolledInter == 8,
+                "update the case lists");
+  static_assert(QMAX == kQShort || QMAX == kQMid || QMAX == kQExt || QMAX == kQLong,
+                "unknown variant");
 #define GTS_CASE(n) \
   case n: path_fixed<T, n, UNIFORM, INTER, MODE, GAPPED>(st, s, q, xrow, prow, stride); break;
+#define GTS_CASE64(n) \
+  case n: path_fixed<T, n, UNIFORM, false, MODE, GAPPED, double>(st, s, q, xrow, prow, stride); break;
   switch (Q) {
     GTS_CASE(1) GTS_CASE(2) GTS_CASE(3) GTS_CASE(4) GTS_CASE(5) GTS_CASE(6)
     GTS_CASE(7) GTS_CASE(8)
@@ -710,7 +719,15 @@ __device__ __forceinline__ void dispatch(int Q, const Stage<T, GAPPED>* st, int 
         switch (Q) {
           GTS_CASE(9) GTS_CASE(10) GTS_CASE(11) GTS_CASE(12)
           default:
-            if constexpr (QMAX == kQLong) path_dyn<T, false, MODE, GAPPED>(st, s, q, xrow, prow, stride);
+            if constexpr (QMAX >= kQExt) {
+              switch (Q) {
+                GTS_CASE64(13) GTS_CASE64(14) GTS_CASE64(15) GTS_CASE64(16)
+                default:
+                  if constexpr (QMAX == kQLong)
+                    path_dyn<T, false, MODE, GAPPED>(st, s, q, xrow, prow, stride);
+                  break;
+              }
+            }
             break;
         }
       } else if constexpr (QMAX == kQLong) {
@@ -719,6 +736,7 @@ __device__ __forceinline__ void dispatch(int Q, const Stage<T, GAPPED>* st, int 
       break;
   }
 #undef GTS_CASE
+#undef GTS_CASE64
 }
 
 // Largest value of v over the wave (v in [0, 64)), from six ballots.
@@ -836,10 +854,10 @@ __device__ __forceinline__ uint64_t live_roots(const Bin<T>& b, int lane, uint64
   // AND over each path's lanes (its root and its non-zero-fraction
   // elements hold all ones): a segmented suffix scan, steps of 1, 2, 4, ...
   // lanes while no root lies in between; four steps cover paths of up to 16
-  // elements
+  // elements, five up to 32
   unsigned lo = (unsigned)rows, hi = (unsigned)(rows >> 32);
   const uint64_t later = lane < 63 ? roots >> (lane + 1) : 0ull;   // roots above this lane
-  constexpr int kSteps = QMAX < kQLong ? 4 : 6;
+  constexpr int kSteps = QMAX <= kQMid ? 4 : QMAX <= kQExt ? 5 : 6;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
     const int d = 1 << t;
@@ -1097,6 +1115,7 @@ gts_status launch_plan(const KernelArgs& a, const Plan& p) {
   if (p.qmax <= kQShort) return launch_shape<T, INTER, kQShort>(a, p);
   if constexpr (!INTER) {
     if (p.qmax <= kQMid) return launch_shape<T, INTER, kQMid>(a, p);
+    if (p.qmax <= kQExt) return launch_shape<T, INTER, kQExt>(a, p);
   }
   return launch_shape<T, INTER, kQLong>(a, p);
 }

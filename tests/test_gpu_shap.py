@@ -170,6 +170,48 @@ def test_rank_table_feature_limit(torch, orc, M, dtype):
     assert_parity(got, orc.treeshap(w.ensemble, w.X), dtype, what=f"M={M} {dtype}")
 
 
+def spine_tree(feats, rng, zero_right):
+    """A spine of splits on the distinct features `feats` (the left child
+    continues the spine) with a leaf on every right; right leaves at the
+    spine positions in `zero_right` have zero cover, so their paths end in a
+    zero-fraction element that rows going left never reach."""
+    res, cover = [], 1000.0
+    for d, f in enumerate(feats):
+        base = len(res)
+        right = 0.0 if d in zero_right else max(1.0, float(int(cover * 0.15)))
+        res.append((base + 2, base + 1, int(f), np.float32(rng.uniform(0.25, 0.75)), cover, 0.0))
+        res.append((-1, -1, -1, 0.0, right, float(rng.normal())))
+        cover -= right
+    res.append((-1, -1, -1, 0.0, cover, float(rng.normal())))
+    return res
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+def test_sixteen_feature_paths(torch, orc, dtype):
+    """Paths of 12 to 16 features on a 16-feature model: the variant
+    unrolled for at most 16 features (fp64 arithmetic), and in fp32 the
+    one-path-per-wave launch whose rank tables cover 16 features and whose
+    scan over a path's zero-fraction elements spans up to 16 lanes; 150 rows
+    (three 64-row tiles, the last ragged)."""
+    rng = np.random.default_rng(16)
+    M = 16
+    trees = []
+    for t in range(24):
+        n = 12 + t % 5
+        zero = set(rng.choice(n, size=1 + t % 4, replace=False).tolist())
+        trees.append(spine_tree(rng.permutation(M)[:n], rng, zero))
+    ens = synth.ensemble_from_lists(trees, M=M)
+    X = rng.uniform(0.0, 1.0, size=(150, M)).astype(np.float32)
+    model = gts.prepare(ens, dtype)
+    cfg = gts.launch_config(model, 150)
+    say("sixteen-feature paths", dtype, cfg)
+    assert model.desc.max_path_len == 17  # 16 features and the root
+    if dtype == "f32":
+        assert cfg["rows_per_tile"] == 64 and cfg["private_tiles"] == 1
+    got = run_shap(torch, ens, X, dtype)
+    assert_parity(got, orc.treeshap(ens, X), dtype, what=f"16-feature paths {dtype}")
+
+
 def test_bins_without_live_paths(torch, orc):
     """Trees whose right subtree has zero cover: its paths carry two
     zero-fraction elements, and rows with x0 < 0.5 reach none of them, so
