@@ -306,22 +306,23 @@ struct Walker {
     Undo& e = undo[(size_t)u];
     e.feature = f;
     if (VALUES) {
-      e.lower = lower[i];
-      e.upper = upper[i];
+      const float l0 = lower[i], u0 = upper[i];
+      e.lower = l0;
+      e.upper = u0;
       e.zero_fraction = zf[i];
-      if (lo > lower[i]) lower[i] = lo;
-      if (hi < upper[i]) upper[i] = hi;
+      lower[i] = lo > l0 ? lo : l0;
+      upper[i] = hi < u0 ? hi : u0;
       zf[i] = zf[i] * ratio;
     }
-    if (count[i]++ == 0) {
-      if (small) {
-        mask |= 1ull << f;
-      } else {
-        active.push_back(f);
-        size_t k = active.size() - 1;
-        for (; k > 0 && active[k - 1] > f; --k) active[k] = active[k - 1];
-        active[k] = f;
-      }
+    if (small) {
+      // no branch on whether the feature is already on the path
+      ++count[i];
+      mask |= 1ull << f;
+    } else if (count[i]++ == 0) {
+      active.push_back(f);
+      size_t k = active.size() - 1;
+      for (; k > 0 && active[k - 1] > f; --k) active[k] = active[k - 1];
+      active[k] = f;
     }
   }
 
@@ -334,15 +335,13 @@ struct Walker {
       upper[i] = e.upper;
       zf[i] = e.zero_fraction;
     }
-    if (--count[i] == 0) {
-      if (small) {
-        mask &= ~(1ull << e.feature);
-      } else {
-        size_t k = 0;
-        while (active[k] != e.feature) ++k;
-        for (; k + 1 < active.size(); ++k) active[k] = active[k + 1];
-        active.pop_back();
-      }
+    if (small) {
+      mask &= ~((uint64_t)(--count[i] == 0) << e.feature);
+    } else if (--count[i] == 0) {
+      size_t k = 0;
+      while (active[k] != e.feature) ++k;
+      for (; k + 1 < active.size(); ++k) active[k] = active[k + 1];
+      active.pop_back();
     }
   }
 
@@ -1439,9 +1438,45 @@ struct PrepareScratch {
 
 // Writes one path, the walker's current leaf, to its place in the blob (root
 // at element offset d, then its elements in device_order without rotation);
-// returns the product of the zero fractions as emit() does.
+// returns the product of the zero fractions as emit() does.  For up to 64
+// features each element goes straight to its slot: its rank among the
+// zero-fraction features of the path, or after them among the others, from
+// masks, with no branch on the values.
 template <typename Z>
 double put_path(const gts_model& m, char* blob, const Walker& w, size_t q, double v, int64_t d) {
+  int32_t* const feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]) + d;
+  float* const lower = reinterpret_cast<float*>(blob + m.off[kLower]) + d;
+  float* const upper = reinterpret_cast<float*>(blob + m.off[kUpper]) + d;
+  Z* const zero = reinterpret_cast<Z*>(blob + m.off[kZero]) + d;
+  if (w.small) {
+    const uint64_t mask = w.mask;
+    uint64_t zmask = 0;   // features whose zero fraction is 0 in the blob's precision
+    for (uint64_t mm = mask; mm; mm &= mm - 1) {
+      const int32_t f = __builtin_ctzll(mm);
+      zmask |= (uint64_t)((Z)w.zf[(size_t)f] == Z(0)) << f;
+    }
+    const int32_t n0 = __builtin_popcountll(zmask);
+    feat[0] = -1 - n0;
+    lower[0] = -std::numeric_limits<float>::infinity();
+    upper[0] = std::numeric_limits<float>::infinity();
+    zero[0] = (Z)v;
+    double prod = 1.0;
+    int32_t iz = 1, ir = 1 + n0;
+    for (uint64_t mm = mask; mm; mm &= mm - 1) {
+      const int32_t f = __builtin_ctzll(mm);
+      const int32_t isz = (int32_t)((zmask >> f) & 1ull);
+      const int32_t k = isz ? iz : ir;
+      iz += isz;
+      ir += 1 - isz;
+      const double z = w.zf[(size_t)f];
+      feat[k] = f;
+      lower[k] = w.lower[(size_t)f];
+      upper[k] = w.upper[(size_t)f];
+      zero[k] = (Z)z;
+      prod = prod * z;
+    }
+    return prod;
+  }
   using S = std::conditional_t<std::is_same_v<Z, float>, SplitF, Split>;
   S el[kMaxPathLen];
   const double prod = w.emit(el);
@@ -1452,10 +1487,6 @@ double put_path(const gts_model& m, char* blob, const Walker& w, size_t q, doubl
     zs[j] = (Z)el[j].zero_fraction;
   }
   const int32_t n0 = device_order(fs, zs, (int32_t)q, 0, nullptr, false, order);
-  int32_t* const feat = reinterpret_cast<int32_t*>(blob + m.off[kFeat]) + d;
-  float* const lower = reinterpret_cast<float*>(blob + m.off[kLower]) + d;
-  float* const upper = reinterpret_cast<float*>(blob + m.off[kUpper]) + d;
-  Z* const zero = reinterpret_cast<Z*>(blob + m.off[kZero]) + d;
   feat[0] = -1 - n0;
   lower[0] = -std::numeric_limits<float>::infinity();
   upper[0] = std::numeric_limits<float>::infinity();
