@@ -86,11 +86,11 @@ SUITE = [
 # SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
 # summaries and the commands that made them are in profiles/.
 COUNTERS = {
-    ('deep', 'f32', False): {"fetch_bytes": 63844068, "write_bytes": 46080000, "valu_insts": 1787738115, "salu_insts": 347553710, "lds_insts": 276472423, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
-    ('deep', 'f64', False): {"fetch_bytes": 73798073, "write_bytes": 92160000, "valu_insts": 1878453534, "salu_insts": 322768424, "lds_insts": 292643883, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
-    ('covtype_med', 'f32', False): {"fetch_bytes": 19347765, "write_bytes": 35200000, "valu_insts": 288921726, "salu_insts": 73891934, "lds_insts": 41750631, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
-    ('wide', 'f32', False): {"fetch_bytes": 416313822, "write_bytes": 316800000, "valu_insts": 5548918571, "salu_insts": 1074743240, "lds_insts": 764848748, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
-    ('interactions', 'f32', True): {"fetch_bytes": 11161428, "write_bytes": 48400000, "valu_insts": 181898070, "salu_insts": 31402109, "lds_insts": 16053095, "source": "a22ca73bc9a4946e9a6d10fa4dd743fec3bd259739524a36e24e5f517957bf7f"},
+    ('deep', 'f32', False): {"fetch_bytes": 63847834, "write_bytes": 46080000, "valu_insts": 1787738115, "salu_insts": 347553710, "lds_insts": 276472423, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
+    ('deep', 'f64', False): {"fetch_bytes": 73798492, "write_bytes": 92160000, "valu_insts": 1878453534, "salu_insts": 322768424, "lds_insts": 292643883, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
+    ('covtype_med', 'f32', False): {"fetch_bytes": 19342692, "write_bytes": 35200000, "valu_insts": 288919510, "salu_insts": 73881230, "lds_insts": 41749159, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
+    ('wide', 'f32', False): {"fetch_bytes": 416389801, "write_bytes": 316800000, "valu_insts": 5548913782, "salu_insts": 1074740394, "lds_insts": 764845531, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
+    ('interactions', 'f32', True): {"fetch_bytes": 11161380, "write_bytes": 48400000, "valu_insts": 181895786, "salu_insts": 31401451, "lds_insts": 16052129, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
 }
 
 
