@@ -4,9 +4,11 @@ One step is one pass of the whole path over one batch of rows of the deep
 regression workload (1000 trees, depth <= 16, split probability 0.7, at most
 1024 leaves per tree, M = 8, 10 000 rows, fp32): path extraction with
 duplicate merging and the bias, Best-Fit-Decreasing packing into 64-element
-bins, device layout and upload of the model (host), then the SHAP kernel over
-the batch (device).  The rows X are resident in HBM before timing starts.
-`value` is rows explained per second over the timed steps.
+bins, device layout and upload of the model (host), then on the device the
+model pruned for the batch (the paths none of its rows reaches dropped,
+gts_prune_model; --no-prune leaves this out) and the SHAP kernel over the
+batch.  The rows X are resident in HBM before timing starts.  `value` is rows
+explained per second over the timed steps.
 
 The same JSON line carries:
   roofline      the SHAP kernel against the MI355X FP32 vector peak.  Its
@@ -25,7 +27,8 @@ The same JSON line carries:
   configs       every workload of the suite (tiny, covtype-shaped, deep fp32
                 and fp64, wide multiclass, interactions): host preparation,
                 kernel time and rows/s, live pairs, modelled rate and
-                fraction, and the CPU oracle's rate on a row prefix;
+                fraction, the pruning pass and the kernel on the pruned model,
+                and the CPU oracle's rate on a row prefix;
   cpu_baseline  the fp64 CPU oracle (Algorithm 1, OpenMP over rows) on a row
                 prefix of the headline batch, on the host's cores, and on one
                 thread.
@@ -57,7 +60,7 @@ METRIC = "rows/sec for SHAP values and SHAP interaction values; % FP32 VALU peak
 CSRC = os.path.join(ROOT, "paper_2010_13972_amd", "csrc")
 KERNEL_SOURCES = [os.path.join(CSRC, f) for f in (
     "gts_shap_kernel.h", "gts_launch.h", "gts_kernels.hip", "gts_shap_f32.hip",
-    "gts_shap_f64.hip", "gts_inter_f32.hip", "gts_inter_f64.hip")]
+    "gts_shap_f64.hip", "gts_inter_f32.hip", "gts_inter_f64.hip", "gts_prune.hip")]
 
 WORKLOAD_TEXT = {
     "tiny": "tiny: 10 full depth-3 trees, M=8, X~U[0,1), 256 rows",
@@ -225,7 +228,7 @@ def kernel_fn(gts, interactions):
 
 
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1,
-                  preps=2):
+                  preps=2, prune=True):
     """Whole-path steps, pipelined.  `preps` host threads prepare the models
     of consecutive steps at the same time: step k runs gts_prepare_model on
     thread k mod preps, into pinned buffer k mod NB (NB = preps + 2), each
@@ -236,9 +239,12 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     streams hold only kernels, with no cross-stream waits.  The host orders buffer reuse: a preparation waits until the kernel
     that last used its buffers has been launched and its upload has finished,
     an upload for the kernel that last read its device buffer.  The loop
-    calls the C ABI with arguments marshalled once.  Timed on the host clock; each kernel is
-    bracketed by HIP events on its stream, each preparation by the host clock
-    of its thread."""
+    calls the C ABI with arguments marshalled once.  With `prune`, each step
+    first prunes its model for the batch (gts_prune_model, on the compute
+    stream, into that stream's workspace) and runs the kernel on the pruned
+    model.  Timed on the host clock; the pruning and the kernel are bracketed
+    by HIP events on their stream, each preparation by the host clock of its
+    thread."""
     import collections
     import ctypes
     import gc
@@ -256,8 +262,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(NB)]
     copied = [torch.cuda.Event() for _ in range(NB)]    # upload from pinned[i] done
     consumed = [torch.cuda.Event() for _ in range(NB)]  # kernel reading dev[i] done
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(steps)]
     ens_struct, keep = gts._ensemble_struct(ens)
     descs = [gts.ModelDesc() for _ in range(NB)]
     biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NB)]
@@ -272,6 +277,24 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                   ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
                   ctypes.c_void_p(outs[j].data_ptr()), ctypes.c_void_p(computes[j].cuda_stream))
                  for j in range(nstreams)] for i in range(NB)]
+    # batch pruning: per compute stream a workspace (the pruned blob stays in
+    # it until that stream's kernel has read it) and the pruned descriptor
+    ws_bytes = ctypes.c_int64(0)
+    if prune:
+        gts._check(L.gts_prune_workspace_bytes(ctypes.byref(desc0), rows, ctypes.byref(ws_bytes)),
+                   "gts_prune_workspace_bytes")
+    wss = [torch.empty(max(1, ws_bytes.value), dtype=torch.uint8, device="cuda")
+           for _ in range(nstreams if prune else 0)]
+    pdescs = [gts.ModelDesc() for _ in range(nstreams)]
+    pptrs = [ctypes.c_void_p() for _ in range(nstreams)]
+    prune_args = [[(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
+                    ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
+                    ctypes.c_void_p(wss[j].data_ptr()), ws_bytes.value, ctypes.byref(pdescs[j]),
+                    ctypes.byref(pptrs[j]), ctypes.c_void_p(computes[j].cuda_stream))
+                   for j in range(nstreams)] for i in range(NB)] if prune else None
+    pruned_args = [(ctypes.byref(pdescs[j]), pptrs[j], ctypes.c_void_p(Xd.data_ptr()), rows,
+                    Xd.stride(0), ctypes.c_void_p(outs[j].data_ptr()),
+                    ctypes.c_void_p(computes[j].cuda_stream)) for j in range(nstreams)]
     cores = min(16, len(os.sched_getaffinity(0)))
     share = 0 if preps == 1 else max(1, cores // preps)
 
@@ -351,11 +374,17 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                     stream = computes[j]
                     if timed:
                         ev[k][0].record(stream)
-                    st = launch(*run_args[i][j])
+                    if prune:
+                        st = L.gts_prune_model(*prune_args[i][j])
+                        if st != gts.GTS_OK:
+                            raise RuntimeError(f"gts_prune_model: {L.gts_last_error().decode()}")
+                    if timed:
+                        ev[k][1].record(stream)
+                    st = launch(*(pruned_args[j] if prune else run_args[i][j]))
                     if st != gts.GTS_OK:
                         raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
                     if timed:
-                        ev[k][1].record(stream)
+                        ev[k][2].record(stream)
                     consumed[i].record(stream)
                     launched[k].set()
                     done += 1
@@ -403,8 +432,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
             q.put(None)
         for t in threads:
             t.join()
-    kern = np.array([a.elapsed_time(b) for a, b in ev])
-    return wall, kern, outs[(steps - 1) % nstreams], ref_model, np.array(host_ms)
+    kern = np.array([b.elapsed_time(c) for a, b, c in ev])
+    prune_ms = np.array([a.elapsed_time(b) for a, b, c in ev])
+    return wall, kern, prune_ms, outs[(steps - 1) % nstreams], ref_model, np.array(host_ms)
 
 
 def time_kernel(torch, gts, model, Xd, reps, interactions):
@@ -423,6 +453,40 @@ def time_kernel(torch, gts, model, Xd, reps, interactions):
         b.record(stream)
     torch.cuda.synchronize()
     return np.array([a.elapsed_time(b) for a, b in ev])
+
+
+def time_prune(torch, gts, model, Xd, reps, interactions):
+    """gts_prune_model for the batch (HIP events around each call), then the
+    kernel on the pruned model as time_kernel times it: (prune ms per call,
+    kernel ms per launch, pruned model)."""
+    ws = torch.empty(gts.prune_workspace_bytes(model, Xd.shape[0]), dtype=torch.uint8,
+                     device="cuda")
+    stream = torch.cuda.current_stream()
+    pm = gts.prune(model, Xd, workspace=ws)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        a.record(stream)
+        pm = gts.prune(model, Xd, workspace=ws)
+        b.record(stream)
+    torch.cuda.synchronize()
+    p = np.array([a.elapsed_time(b) for a, b in ev])
+    k = time_kernel(torch, gts, pm, Xd, reps, interactions)
+    return p, k, pm
+
+
+def pruned_counts(gts, pm):
+    """(bins, paths, elements) of a pruned model, read back from the device."""
+    host = pm.blob.cpu().numpy()
+    G = pm.num_groups
+    o5, o4, o0 = pm.desc.off[5], pm.desc.off[4], pm.desc.off[0]
+    gb = np.frombuffer(host[o5:o5 + 4 * (G + 1)].tobytes(), np.int32)
+    nb = int(gb[G])
+    bs = np.frombuffer(host[o4:o4 + 4 * (nb + 1)].tobytes(), np.int32)
+    ne = int(bs[nb])
+    feat = np.frombuffer(host[o0:o0 + 4 * ne].tobytes(), np.int32)
+    return nb, int(np.count_nonzero(feat < 0)), ne
 
 
 def time_prepare(gts, ens, dtype, reps=5):
@@ -542,6 +606,19 @@ def suite_entry(torch, gts, synth, oracle, workload, dtype, interactions, reps, 
         "traffic_bytes": traffic_for((workload, dtype, interactions)),
         "executed": executed((workload, dtype, interactions), med),
     }
+    p, kp, pm = time_prune(torch, gts, model, Xd, reps, interactions)
+    pmed, kpmed = float(np.median(p)), float(np.median(kp))
+    nb, npaths, nel = pruned_counts(gts, pm)
+    entry["pruned"] = {
+        "prune_ms_median": pmed, "kernel_ms_median": kpmed,
+        "kernel_rows_per_s": rows / (kpmed * 1e-3),
+        "prune_and_kernel_rows_per_s": rows / ((pmed + kpmed) * 1e-3),
+        "paths": npaths, "path_elements": nel, "bins": nb,
+        "modelled_tflops": wm["flops_live"] / (kpmed * 1e-3) / 1e12,
+        "frac": wm["flops_live"] / (kpmed * 1e-3) / 1e12 / peak,
+        "traffic_bytes": traffic_for((workload, dtype, interactions, "pruned")),
+        "executed": executed((workload, dtype, interactions, "pruned"), kpmed),
+    }
     if oracle is not None and oracle_s > 0:
         threads = cpu_threads()
         rate, n, passes, dt = oracle_rate(oracle, ens, w.X, oracle_s, interactions, threads)
@@ -578,19 +655,23 @@ def copy_probe(torch):
     return n * 4
 
 
-def profile_launches(torch, gts, synth, workload, dtype, launches):
+def profile_launches(torch, gts, synth, workload, dtype, launches, pruned=False):
     """Only the kernel of one workload, `launches` times back to back (for
-    rocprofv3 counter and trace runs)."""
+    rocprofv3 counter and trace runs); with `pruned`, on the model pruned for
+    the batch once beforehand."""
     w = synth.workload(workload)
     inter = workload == "interactions"
     model = gts.prepare(w.ensemble, dtype)
     Xd = torch.from_numpy(w.X).cuda()
+    if pruned:
+        model = gts.prune(model, Xd)
     fn = kernel_fn(gts, inter)
     out = fn(model, Xd)
     for _ in range(launches - 1):
         fn(model, Xd, out=out)
     torch.cuda.synchronize()
-    print(json.dumps({"profiled": workload, "dtype": dtype, "launches": launches}), flush=True)
+    print(json.dumps({"profiled": workload, "dtype": dtype, "launches": launches,
+                      "pruned": pruned}), flush=True)
 
 
 # ---------------------------------------------------------------------------
@@ -734,11 +815,16 @@ def main():
                     help="compute streams the pipelined steps alternate between")
     ap.add_argument("--preps", type=int, default=0,
                     help="model preparations in flight at once in the pipelined steps "
-                         "(0: two for models of 128 k nodes or more, else one)")
+                         "(0: three for models of 128 k nodes or more, else one)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     ap.add_argument("--profile-launches", type=int, default=0,
                     help="only launch the kernel of --workload this many times (rocprofv3)")
+    ap.add_argument("--profile-pruned", action="store_true",
+                    help="with --profile-launches: on the model pruned for the batch")
+    ap.add_argument("--no-prune", action="store_true",
+                    help="the steps run the kernel on the whole model, without pruning it "
+                         "for the batch first")
     args = ap.parse_args()
     if args.steps < 1 or args.warmup < 0 or args.streams < 1 or args.preps < 0:
         ap.error("--steps and --streams must be at least 1, --warmup and --preps at least 0")
@@ -760,7 +846,8 @@ def main():
         copy_probe(torch)
     if args.profile_launches:
         profile_launches(torch, gts, synth, args.workload,
-                         args.dtype or synth.workload(args.workload).dtype, args.profile_launches)
+                         args.dtype or synth.workload(args.workload).dtype, args.profile_launches,
+                         args.profile_pruned)
         return
 
     if args.experiment == "packers":
@@ -780,11 +867,13 @@ def main():
     rows = w.X.shape[0]
     Xd = torch.from_numpy(w.X).cuda()
 
-    # a large model's preparation does not use 16 cores fully: two in flight
-    # on 8 cores each prepare more models per second; a small one's does
-    preps = args.preps or (2 if ens.num_nodes >= (1 << 17) else 1)
-    wall, kern, out, model, step_host = time_pipeline(torch, gts, ens, Xd, dtype, args.steps,
-                                                      args.warmup, inter, args.streams, preps)
+    # a large model's preparation does not use 16 cores fully: three in
+    # flight, each on a third of the cores, prepare more models per second; a
+    # small one's does
+    preps = args.preps or (3 if ens.num_nodes >= (1 << 17) else 1)
+    prune = not args.no_prune
+    wall, kern, prune_ms, out, model, step_host = time_pipeline(
+        torch, gts, ens, Xd, dtype, args.steps, args.warmup, inter, args.streams, preps, prune)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)
@@ -795,11 +884,16 @@ def main():
     # roofline: the kernel's launches inside the timed steps (events on its
     # stream); back-to-back launches in a timed region of their own as well
     kern_ms = float(kern.mean())
-    k_only = time_kernel(torch, gts, model, Xd, max(5, min(args.steps, 50)), inter)
+    nrep = max(5, min(args.steps, 50))
+    if prune:
+        _, k_only, kmodel = time_prune(torch, gts, model, Xd, nrep, inter)
+        pbins, ppaths, pelems = pruned_counts(gts, kmodel)
+    else:
+        k_only = time_kernel(torch, gts, model, Xd, nrep, inter)
     wm = work_model(torch, gts, ens, w.X, dtype, inter)
     peak = PEAK_FP64_TFLOPS if dtype == "f64" else PEAK_FP32_TFLOPS
     achieved = wm["flops_live"] / (kern_ms * 1e-3) / 1e12
-    key = (args.workload, dtype, inter)
+    key = (args.workload, dtype, inter) + (("pruned",) if prune else ())
     line = {
         "metric": METRIC,
         "value": rows * args.steps / wall, "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
@@ -812,16 +906,21 @@ def main():
                    "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
                               + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": "extract + merge + bias + BFD pack (B=64) + layout (host) + upload "
+                           + ("+ batch pruning (device) " if prune else "")
                            + ("+ interaction kernel" if inter else "+ SHAP kernel")
                            + f"; {preps} steps' host work in flight at once, each on "
                            + "its share of the cores; uploads and host work overlap the "
                            + "kernels of earlier steps",
-                   "compute_streams": args.streams, "preparations_in_flight": preps},
+                   "compute_streams": args.streams, "preparations_in_flight": preps,
+                   "pruned_for_the_batch": ({"paths": ppaths, "path_elements": pelems,
+                                             "bins": pbins} if prune else None)},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak,
                      "traffic": traffic_for(key),
-                     "kernel": "shap_kernel" + (" (interactions)" if inter else ""),
+                     "kernel": "shap_kernel" + (" (interactions)" if inter else "")
+                               + (" on the model pruned for the batch" if prune else ""),
                      "kernel_ms": kern_ms,
+                     "prune_ms_in_steps": float(prune_ms.mean()) if prune else None,
                      "kernel_launches": int(len(kern)),
                      "kernel_ms_back_to_back": float(k_only.mean()),
                      "modelled_gflop_per_launch": wm["flops_live"] / 1e9,
@@ -834,9 +933,10 @@ def main():
                      "host_prepare_ms_in_steps_p90": float(np.percentile(step_host, 90)),
                      "note": "achieved: op model over the live (row, path) pairs (a pair "
                              "whose zero-cover element misses the row contributes exactly "
-                             "0) / mean in-step launch time; peak is the packed-FP32 vendor "
-                             "figure (non-packed FP32 FMAs measured about 129 TFLOP/s); "
-                             "dense_equivalent_tflops counts every pair"},
+                             "0; pruning drops only paths without live pairs) / mean "
+                             "in-step launch time of the kernel; peak is the packed-FP32 "
+                             "vendor figure (non-packed FP32 FMAs measured about 129 "
+                             "TFLOP/s); dense_equivalent_tflops counts every pair"},
         "launch": gts.launch_config(model, rows, inter),
         "kernel": {"rows_per_s": rows / (float(np.median(k_only)) * 1e-3),
                    "ms_median": float(np.median(k_only)), "ms_mean": float(k_only.mean()),

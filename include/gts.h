@@ -13,6 +13,9 @@
  *   gts_shap            device SHAP values              phi[rows][G][M+1]
  *   gts_shap_interactions device SHAP interaction values phi[rows][G][M+1][M+1]
  *   gts_launch_config   host   the launch shape the two calls above choose
+ *   gts_prune_model     device a copy of a model without the paths that no
+ *                              row of one batch reaches, for the two device
+ *                              calls above on that batch
  *
  * Conventions shared by every call:
  *   - All memory is owned by the caller.  The library calls no device
@@ -107,6 +110,7 @@ typedef struct gts_path_element {
  * byte blob the caller copies to the device; treat them as read-only.
  */
 #define GTS_MODEL_SORTED_BINS 1
+#define GTS_MODEL_PRUNED 2
 
 typedef struct gts_model {
   uint32_t magic;
@@ -115,7 +119,9 @@ typedef struct gts_model {
   int32_t num_groups;      /* G */
   int32_t max_path_len;    /* longest path, root included */
   int32_t flags;           /* GTS_MODEL_SORTED_BINS: inside every bin, paths
-                              are in non-increasing length order (BFD, FFD) */
+                              are in non-increasing length order (BFD, FFD);
+                              GTS_MODEL_PRUNED: from gts_prune_model, whose
+                              counts below are capacities */
   int64_t num_elements;
   int64_t num_paths;
   int64_t num_bins;
@@ -363,6 +369,56 @@ typedef struct gts_launch {
 
 gts_status gts_launch_config(const gts_model *model, int64_t rows, int32_t interactions,
                              gts_launch *out);
+
+/*
+ * gts_prune_workspace_bytes -- device workspace (bytes) that gts_prune_model
+ * needs for this model and row count on the calling thread's current device:
+ * about 16 bytes per path element for fp32 models (20 for fp64) plus 4 bytes
+ * per feature per row.  Errors: GTS_EINVAL as gts_prune_model.
+ */
+gts_status gts_prune_workspace_bytes(const gts_model *model, int64_t rows, int64_t *bytes);
+
+/*
+ * gts_prune_model -- the model without the paths that contribute nothing to
+ * any row of one batch.  A (row, path) pair whose path has an element of zero
+ * fraction with a range that misses the row's value contributes exactly
+ * nothing to that row's SHAP and interaction values (Algorithm 1 prunes such
+ * zero-cover subtrees).  A path is dropped when one of its zero-fraction
+ * elements has a range [lower, upper) that holds the value of no row of d_X
+ * (the same range test as the kernels', on the same keys); every other path
+ * is kept, with its elements unchanged.  gts_shap and gts_shap_interactions
+ * on the pruned model and the same rows give the values they give on the
+ * model itself, up to the rounding of a different summation order: the kept
+ * paths are rebinned by output group and length (longest first), each bin
+ * holding paths of one length (64 / length of them; the last bin of a length
+ * fewer).  The bias is the model's.
+ *
+ * model        host descriptor from gts_model_layout (not from this call).
+ * d_model      device copy of its blob.
+ * d_X, rows, ld_x  the batch, as for gts_shap (rows == 0: nothing is
+ *              launched and the pruned model must not be used).
+ * d_workspace  device memory of gts_prune_workspace_bytes bytes, aligned to
+ *              256 bytes, owned by the caller; it holds the pruned blob, so
+ *              it must stay untouched while the pruned model is in use.
+ * pruned       out: the pruned model's host descriptor, written before the
+ *              call returns.  Its num_elements, num_paths and num_bins are
+ *              capacities (the model's own counts; the device holds the
+ *              pruned counts) and GTS_MODEL_PRUNED and GTS_MODEL_SORTED_BINS
+ *              are set.  Valid only for the rows of d_X: other rows may reach
+ *              dropped paths.
+ * d_pruned     out: device address of the pruned blob, inside d_workspace.
+ * stream       hipStream_t; the work is enqueued (five launches) and the
+ *              pruned blob is complete when the stream reaches its end, so
+ *              later calls on the same stream may use it.
+ * Errors: GTS_EINVAL for NULL pointers, a descriptor not from
+ * gts_model_layout or one from this call, rows < 0, ld_x < M, a misaligned
+ * workspace, or a model with 2^31 elements or more; GTS_EBUFSIZE if
+ * workspace_bytes is too small; GTS_EDEVICE if a launch fails.
+ */
+gts_status gts_prune_model(const gts_model *model, const void *d_model, const float *d_X,
+                           int64_t rows, int64_t ld_x, void *d_workspace,
+                           int64_t workspace_bytes, gts_model *pruned, void **d_pruned,
+                           void *stream);
 
 /*
  * gts_set_host_threads -- caps the host threads (the caller included) that

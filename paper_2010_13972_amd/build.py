@@ -46,7 +46,8 @@ def _run(cmd, verbose):
         print(out)
 
 
-KERNEL_UNITS = ["gts_kernels", "gts_shap_f32", "gts_shap_f64", "gts_inter_f32", "gts_inter_f64"]
+KERNEL_UNITS = ["gts_kernels", "gts_shap_f32", "gts_shap_f64", "gts_inter_f32", "gts_inter_f64",
+                "gts_prune"]
 RESOURCES = os.path.join(BUILD, "kernel_resources.txt")
 
 

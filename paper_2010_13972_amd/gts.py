@@ -107,6 +107,11 @@ def lib() -> ctypes.CDLL:
         L.gts_launch_config.argtypes = [ctypes.POINTER(ModelDesc), i64, i32,
                                         ctypes.POINTER(LaunchInfo)]
         L.gts_launch_config.restype = st
+        L.gts_prune_workspace_bytes.argtypes = [ctypes.POINTER(ModelDesc), i64, vp]
+        L.gts_prune_workspace_bytes.restype = st
+        L.gts_prune_model.argtypes = [ctypes.POINTER(ModelDesc), vp, vp, i64, i64, vp, i64,
+                                      ctypes.POINTER(ModelDesc), ctypes.POINTER(vp), vp]
+        L.gts_prune_model.restype = st
         L.gts_set_host_threads.argtypes = [i32]
         L.gts_set_host_threads.restype = st
         L.gts_last_error.restype = ctypes.c_char_p
@@ -411,6 +416,37 @@ def shap_interactions(model: DeviceModel, X, out=None, stream=None):
                                        ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)),
            "gts_shap_interactions")
     return out
+
+
+def prune_workspace_bytes(model: DeviceModel, rows: int) -> int:
+    """gts_prune_workspace_bytes for this model and row count."""
+    n = ctypes.c_int64(0)
+    _check(lib().gts_prune_workspace_bytes(ctypes.byref(model.desc), int(rows), ctypes.byref(n)),
+           "gts_prune_workspace_bytes")
+    return int(n.value)
+
+
+def prune(model: DeviceModel, X, workspace=None, stream=None) -> DeviceModel:
+    """gts_prune_model: the model without the paths that no row of X reaches,
+    for shap / shap_interactions on the same X.  The pruned blob lives in
+    ``workspace`` (a device uint8 tensor; allocated when None or too small),
+    which must stay alive and unchanged while the returned model is used."""
+    import torch
+    rows, ld = _check_X(model, X)
+    need = prune_workspace_bytes(model, rows)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=X.device)
+    desc = ModelDesc()
+    ptr = ctypes.c_void_p()
+    _check(lib().gts_prune_model(ctypes.byref(model.desc), ctypes.c_void_p(model.blob.data_ptr()),
+                                 ctypes.c_void_p(X.data_ptr()), rows, ld,
+                                 ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                 ctypes.byref(desc), ctypes.byref(ptr), _stream_handle(stream)),
+           "gts_prune_model")
+    off = (ptr.value or workspace.data_ptr()) - workspace.data_ptr()
+    blob = workspace[off:off + desc.bytes]
+    return DeviceModel(desc, blob, model.num_features, model.num_groups, model.dtype,
+                       model.num_paths, model.num_bins, model.bias)
 
 
 def launch_config(model: DeviceModel, rows: int, interactions: bool = False) -> dict:
