@@ -143,10 +143,13 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
   const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(8, dev.lds_per_cu / (int64_t)lds));
   const int64_t bins_per_group = std::max<int64_t>(1, m->num_bins / G);
   int splits = 1;
+  int min_splits = 1;
+  int split_step = 1;
   if constexpr (INTER) {
     const int64_t round = per_cu * dev.cus;
     if (2 * base <= round)
       splits = (int)std::max<int64_t>(1, std::min<int64_t>(round / base, bins_per_group));
+    min_splits = splits;
   } else {
     const int64_t target = 2 * per_cu * dev.cus;
     if (base < target) {
@@ -154,9 +157,12 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
       const int64_t step = 8 / std::gcd(G, 8);
       want = (want + step - 1) / step * step;
       const int64_t fine = std::min<int64_t>(128, bins_per_group / (8 * waves)) / step * step;
+      min_splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
       want = std::max(want, fine);
       splits = (int)std::max<int64_t>(1, std::min<int64_t>(want, bins_per_group));
+      split_step = (int)step;
     }
+    min_splits = std::min(min_splits, splits);
   }
   plan.RW = RW;
   plan.waves = waves;
@@ -167,6 +173,8 @@ gts_status plan_launch(const gts_model* m, int64_t rows, const DeviceInfo& dev, 
   plan.lds = lds;
   plan.rank_off = rank_off;
   plan.splits = splits;
+  plan.min_splits = min_splits;
+  plan.split_step = split_step;
   plan.tiles = tiles;
   // the kernel variant: the model's longest path, in features
   const int qmax = std::max(0, m->max_path_len - 1);

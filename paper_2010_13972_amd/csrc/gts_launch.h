@@ -45,6 +45,8 @@ struct Plan {
   int32_t sx = 0, sp = 0, width = 0;
   size_t lds = 0;
   int splits = 1;
+  int min_splits = 1;    // slices enough for the occupancy target alone
+  int split_step = 1;    // slice counts are multiples of this (XCD balance)
   int64_t tiles = 0;
   int qmax = kQLong;
   size_t rank_off = 0;   // LDS offset of the rank tables (0: none)

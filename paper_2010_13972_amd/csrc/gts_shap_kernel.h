@@ -140,6 +140,12 @@ struct Launch {
   int32_t accumulate;  // 1: atomically add the tile to phi (phi pre-zeroed)
   int32_t sorted;      // 1: inside a bin, paths never grow in length
   int32_t rank_off;    // LDS offset of the rank tables; 0: none
+  // A pruned model's bin count is known only on the device: its workgroups
+  // use min(splits, max(min_splits, bins / (32 waves))) slices, rounded down
+  // to a multiple of split_step, and the others return at once (adaptive).
+  int32_t adaptive;
+  int32_t min_splits;
+  int32_t split_step;
 };
 
 // Makes v a value the compiler must hold in registers at this point, so the
@@ -961,6 +967,15 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   const int g = u / L.splits;
   const int s = u - g * L.splits;
   const int64_t r0 = tile * RW;
+  const int gb0 = d.group_bins[g];
+  const int gb1 = d.group_bins[g + 1];
+  int b_step = L.splits;
+  if (L.adaptive) {
+    // each wave about 32 bins or more; at least the occupancy target
+    const int fine = (gb1 - gb0) / (32 * WAVES) / L.split_step * L.split_step;
+    b_step = min(L.splits, max(L.min_splits, fine));
+    if (s >= b_step) return;   // the whole workgroup, before any barrier
+  }
 
   int* xs = reinterpret_cast<int*>(smem);   // the X tile, as fkey of each value
   T* ps = reinterpret_cast<T*>(smem + (size_t)RW * L.sx * sizeof(float));
@@ -993,9 +1008,7 @@ __global__ __launch_bounds__(64 * WAVES) void shap_kernel(DevModel<T> d, const f
   // Slice s takes every splits-th bin of the group.  Bins come longest paths
   // first, so contiguous runs would give the first slices the most work;
   // strided, every slice gets bins of every size.
-  const int gb1 = d.group_bins[g + 1];
-  const int b_lo = d.group_bins[g] + s;
-  const int b_step = L.splits;
+  const int b_lo = gb0 + s;
   const int* xrow = xs + r * L.sx;
   T* prow = ps + (PRIV ? wave * tile_elems : 0) + r * L.sp;
   const int stride = M + 1;
@@ -1065,6 +1078,9 @@ gts_status launch_rw(const KernelArgs& a, const Plan& p) {
   L.accumulate = p.splits > 1 ? 1 : 0;
   L.sorted = (m->flags & GTS_MODEL_SORTED_BINS) ? 1 : 0;
   L.rank_off = (int32_t)p.rank_off;
+  L.adaptive = (m->flags & GTS_MODEL_PRUNED) ? 1 : 0;
+  L.min_splits = p.min_splits;
+  L.split_step = p.split_step;
   const int64_t total = a.rows * (int64_t)m->num_groups * p.width;
   if (L.accumulate) {
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 65536);
