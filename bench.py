@@ -82,18 +82,24 @@ SUITE = [
 ]
 
 # rocprofv3 counters of the SHAP kernel per launch, keyed by (workload, dtype,
-# interactions); `source` is kernel_source_hash() of the kernel sources the
+# interactions), with a fourth entry "pruned" for the kernel on the model
+# pruned for the batch; `source` is kernel_source_hash() of the kernel sources the
 # counters were taken on.  fetch_bytes / write_bytes: FETCH_SIZE and
 # WRITE_SIZE, each scaled by the ratio of a plain 256 MiB copy's true bytes to
 # the counter's reading of it.  valu_insts / salu_insts / lds_insts:
 # SQ_INSTS_VALU / SQ_INSTS_SALU / SQ_INSTS_LDS (wave instructions).  The
 # summaries and the commands that made them are in profiles/.
 COUNTERS = {
-    ('deep', 'f32', False): {"fetch_bytes": 63847834, "write_bytes": 46080000, "valu_insts": 1787738115, "salu_insts": 347553710, "lds_insts": 276472423, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
-    ('deep', 'f64', False): {"fetch_bytes": 73798492, "write_bytes": 92160000, "valu_insts": 1878453534, "salu_insts": 322768424, "lds_insts": 292643883, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
-    ('covtype_med', 'f32', False): {"fetch_bytes": 19342692, "write_bytes": 35200000, "valu_insts": 288919510, "salu_insts": 73881230, "lds_insts": 41749159, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
-    ('wide', 'f32', False): {"fetch_bytes": 416389801, "write_bytes": 316800000, "valu_insts": 5548913782, "salu_insts": 1074740394, "lds_insts": 764845531, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
-    ('interactions', 'f32', True): {"fetch_bytes": 11161380, "write_bytes": 48400000, "valu_insts": 181895786, "salu_insts": 31401451, "lds_insts": 16052129, "source": "7a81cd38c4bc4b1af4c93a8ce498cfa4576ad8556cd62f4c4db8f4dee4413f3f"},
+    ('deep', 'f32', False): {"fetch_bytes": 63853273, "write_bytes": 46080000, "valu_insts": 1788702723, "salu_insts": 347312558, "lds_insts": 276472423, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('deep', 'f32', False, 'pruned'): {"fetch_bytes": 8800363, "write_bytes": 8640000, "valu_insts": 809664337, "salu_insts": 160894055, "lds_insts": 137874440, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('deep', 'f64', False): {"fetch_bytes": 73801557, "write_bytes": 92160000, "valu_insts": 1879096606, "salu_insts": 322527272, "lds_insts": 292643883, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('deep', 'f64', False, 'pruned'): {"fetch_bytes": 9788162, "write_bytes": 17280000, "valu_insts": 880342252, "salu_insts": 134735606, "lds_insts": 152810820, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('covtype_med', 'f32', False): {"fetch_bytes": 19339592, "write_bytes": 35200000, "valu_insts": 288902461, "salu_insts": 73822658, "lds_insts": 41738121, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('covtype_med', 'f32', False, 'pruned'): {"fetch_bytes": 19017006, "write_bytes": 35200000, "valu_insts": 280929231, "salu_insts": 67801742, "lds_insts": 41065418, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('wide', 'f32', False): {"fetch_bytes": 415594796, "write_bytes": 316800000, "valu_insts": 5550767852, "salu_insts": 1076499619, "lds_insts": 765583007, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('wide', 'f32', False, 'pruned'): {"fetch_bytes": 414847272, "write_bytes": 316800000, "valu_insts": 5506767273, "salu_insts": 1055679113, "lds_insts": 754426459, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('interactions', 'f32', True): {"fetch_bytes": 11157364, "write_bytes": 48400000, "valu_insts": 181893001, "salu_insts": 31405970, "lds_insts": 16051232, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
+    ('interactions', 'f32', True, 'pruned'): {"fetch_bytes": 9414571, "write_bytes": 48400000, "valu_insts": 156394351, "salu_insts": 27377190, "lds_insts": 13662430, "source": "350d1b7705dfaf9f090c31ecde4176169ea0ea396c0774d3335996c7356ca8be"},
 }
 
 
