@@ -181,12 +181,29 @@ def test_deep_model_full_batch(torch, orc, dtype):
     assert_parity(got[rows], orc.treeshap(w.ensemble, w.X[rows]), dtype, what="deep vs oracle")
 
 
+@pytest.mark.parametrize("name", ["wide", "interactions"])
+def test_full_size_wide_and_interaction_batches(torch, orc, name):
+    """The wide model (784 features, 10 groups, 10k rows; the multi-path
+    launch) and the 1000-row interaction batch: every row against the
+    unpruned model (itself checked against the oracle in test_gpu_shap and
+    test_gpu_interactions), and sampled rows against the oracle."""
+    w = synth.workload(name)
+    inter = name == "interactions"
+    say("prune full size", name)
+    got, full = pruned_shap(torch, w.ensemble, w.X, F32, interactions=inter)
+    blocks = 2 if inter else 1
+    assert_parity(got, full, F32, blocks, f"{name} pruned vs unpruned")
+    rows = sample_rows(w.X.shape[0], k=6 if inter else 8, seed=11)
+    want = (orc.interactions if inter else orc.treeshap)(w.ensemble, w.X[rows])
+    assert_parity(got[rows], want, F32, blocks, f"{name} vs oracle")
+
+
 # --------------------------------------------------------------------------
 # the kept paths and the bins
 # --------------------------------------------------------------------------
 
 CASES = [("random", 0, F32), ("random", 1, F64), ("random", 2, F32), ("groups20", 0, F32),
-         ("covtype_med", 0, F32), ("deep", 0, F32)]
+         ("covtype_med", 0, F32), ("deep", 0, F32), ("wide", 0, F32)]
 
 
 @pytest.mark.parametrize("name,seed,dtype", CASES, ids=[f"{n}{s}-{d}" for n, s, d in CASES])
