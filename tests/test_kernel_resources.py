@@ -82,3 +82,20 @@ def test_headline_variants_fit_their_occupancy():
             assert x["vgprs"] <= cap and x["scratch"] == 0, x
             seen += 1
     assert seen == 2
+
+
+def test_prune_kernels_use_no_private_memory():
+    """The batch-pruning kernels (key sort, search, plan, copy) keep their
+    arrays in registers and LDS: no scratch."""
+    if not os.path.exists(REPORT):
+        pytest.skip("library not built (the report comes from the build)")
+    names = ("sort_keys", "mark_paths", "plan_pruned", "copy_paths")
+    seen = set()
+    with open(REPORT) as f:
+        for line in f:
+            d = dict(kv.split("=", 1) for kv in line.rstrip("\n").split("\t"))
+            for n in names:
+                if n in d["name"]:
+                    seen.add(n)
+                    assert d["ScratchSize [bytes/lane]"] == "0", d
+    assert seen == set(names)
