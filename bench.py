@@ -680,6 +680,18 @@ def profile_launches(torch, gts, synth, workload, dtype, launches, pruned=False)
                       "pruned": pruned}), flush=True)
 
 
+def profile_extract(torch, gts, synth, workload, calls):
+    """Only gts_extract_paths_device on one workload's model, `calls` times
+    (for rocprofv3 kernel traces); one workspace for all calls."""
+    w = synth.workload(workload)
+    dens = gts.DeviceEnsemble(w.ensemble)
+    ws = None
+    for _ in range(calls):
+        raw, npaths, _ = gts.extract_paths_device(dens, workspace=ws)
+    torch.cuda.synchronize()
+    print(json.dumps({"profiled_extract": workload, "calls": calls, "paths": npaths}), flush=True)
+
+
 # ---------------------------------------------------------------------------
 # experiments (each prints one JSON line of its own instead of the bench line)
 # ---------------------------------------------------------------------------
@@ -826,6 +838,9 @@ def main():
                     help="run a plain 256 MiB device copy first (counter calibration)")
     ap.add_argument("--profile-launches", type=int, default=0,
                     help="only launch the kernel of --workload this many times (rocprofv3)")
+    ap.add_argument("--profile-extract", type=int, default=0,
+                    help="only run gts_extract_paths_device on --workload's model this many "
+                         "times (rocprofv3)")
     ap.add_argument("--profile-pruned", action="store_true",
                     help="with --profile-launches: on the model pruned for the batch")
     ap.add_argument("--no-prune", action="store_true",
@@ -850,6 +865,9 @@ def main():
 
     if args.copy_probe:
         copy_probe(torch)
+    if args.profile_extract:
+        profile_extract(torch, gts, synth, args.workload, args.profile_extract)
+        return
     if args.profile_launches:
         profile_launches(torch, gts, synth, args.workload,
                          args.dtype or synth.workload(args.workload).dtype, args.profile_launches,
