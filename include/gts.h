@@ -10,6 +10,9 @@
  *   gts_pack_paths      host   paths -> bins of <= 64 path elements
  *   gts_model_layout    host   packed paths -> one device-ready byte blob
  *   gts_prepare_model   host   the three steps above in one pass
+ *   gts_plan_model      host   the same without writing the paths: counts,
+ *                              packing and each path's place, for
+ *   gts_build_model_device  device  which writes the same blob on the GPU
  *   gts_shap            device SHAP values              phi[rows][G][M+1]
  *   gts_shap_interactions device SHAP interaction values phi[rows][G][M+1][M+1]
  *   gts_launch_config   host   the launch shape the two calls above choose
@@ -293,6 +296,80 @@ gts_status gts_model_layout(const gts_path_element *packed, int64_t num_elements
 gts_status gts_prepare_model(const gts_ensemble *ens, int32_t bin_capacity, int32_t alg,
                              int32_t dtype, gts_model *model, void *host_blob,
                              int64_t blob_capacity, double *bias);
+
+/*
+ * gts_plan_model -- gts_prepare_model split between host and device: on the
+ * host, the walk that validates the trees and counts every path's merged
+ * features (Sections 3.1-3.2), the packing (Section 3.3) and each path's
+ * place in the blob; gts_build_model_device then extracts and merges the
+ * paths on the GPU, writes them to those places and sums the bias.  The blob
+ * it writes is byte for byte the one gts_prepare_model writes for the same
+ * ensemble, bin capacity, algorithm and dtype.  Only for models whose every
+ * launch runs one path per wave (M <= 17 in fp32, M <= 11 in fp64), where a
+ * path's element order depends on nothing but the path.
+ *
+ * model      out: the descriptor of the blob gts_build_model_device writes.
+ * plan       out: counts, the plan blob's size and its arrays' byte offsets:
+ *            off[0] uint64 path_dirs[P] path p's turns from its tree's root:
+ *                                       bit k set when its k-th split sends
+ *                                       it right (paths of at most 64 splits)
+ *            off[1] int32 path_dest[P]  element offset of path p's root in
+ *                                       the model blob
+ *            off[2] int32 tree_paths[T+1]  first path of every tree
+ *            off[3] int32 bin_start[K+1]   as in the model blob
+ *            off[4] int32 group_bins[G+1]  as in the model blob
+ * host_plan  host memory of `capacity` bytes for the plan blob, or NULL for
+ *            the descriptors only.
+ * Errors: as gts_prepare_model; GTS_EINVAL for a model with more features
+ * than above, a path of more than 64 splits, or 2^31 nodes or paths or more;
+ * GTS_EBUFSIZE if capacity is smaller than plan->bytes.
+ */
+typedef struct gts_plan {
+  int64_t num_paths;   /* P */
+  int64_t num_trees;   /* T */
+  int64_t num_bins;    /* K */
+  int64_t num_nodes;   /* of the ensemble the plan was made for */
+  int64_t bytes;       /* size of the plan blob */
+  int64_t off[5];
+} gts_plan;
+
+gts_status gts_plan_model(const gts_ensemble *ens, int32_t bin_capacity, int32_t alg,
+                          int32_t dtype, gts_model *model, gts_plan *plan, void *host_plan,
+                          int64_t capacity);
+
+/*
+ * gts_build_workspace_bytes -- device workspace gts_build_model_device needs
+ * for this plan: 8 bytes per path and per tree.
+ */
+gts_status gts_build_workspace_bytes(const gts_plan *plan, int64_t *bytes);
+
+/*
+ * gts_build_model_device -- the model blob of a plan, written on the GPU
+ * (Sections 3.1-3.2 for the elements): one thread per path follows its
+ * turns from its tree's root down to its leaf, merging as it goes (ranges
+ * intersected, zero fractions multiplied in root-to-leaf order, features
+ * ascending), and writes the root and the elements, the zero-fraction ones
+ * first, at the path's place; each tree sums its paths' bias terms
+ * v * prod(z) in path order and each group its trees' sums in tree order,
+ * as on the host.  The result equals gts_prepare_model's blob byte for byte.
+ *
+ * ens        host struct whose array pointers are DEVICE pointers (as for
+ *            gts_extract_paths_device), holding the ensemble the plan was made
+ *            from; it is not validated again.
+ * model, plan  descriptors from gts_plan_model.
+ * d_plan     device copy of the plan blob.
+ * d_model    device memory of model->bytes, overwritten.
+ * d_workspace  device memory of gts_build_workspace_bytes, overwritten; free
+ *            for reuse once the stream has passed the call's work.
+ * stream     hipStream_t; the work is only enqueued (no waits).
+ * Errors: GTS_EINVAL for NULL pointers, a descriptor not from
+ * gts_model_layout or gts_plan_model, or an ensemble whose counts differ
+ * from the plan's; GTS_EBUFSIZE for a workspace too small; GTS_EDEVICE if
+ * a launch fails.
+ */
+gts_status gts_build_model_device(const gts_ensemble *ens, const gts_model *model,
+                                  const gts_plan *plan, const void *d_plan, void *d_model,
+                                  void *d_workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * gts_shap -- SHAP values, Eq. (2), by the per-path permutation-weight

@@ -352,6 +352,175 @@ __global__ void k_bias(DevEnsemble e, Work w, double* __restrict__ bias) {
 }
 
 // ---------------------------------------------------------------------------
+// the model blob of a plan (gts_build_model_device)
+// ---------------------------------------------------------------------------
+
+// Features a plan's merged path may hold: plans are made only for models of
+// at most 17 features.
+constexpr int kPlanMaxM = 17;
+
+// Arrays of the model blob being written.
+template <typename Z>
+struct BlobOut {
+  int32_t* __restrict__ feat;
+  float* __restrict__ lower;
+  float* __restrict__ upper;
+  Z* __restrict__ zero;
+  int32_t* __restrict__ bin_start;
+  int32_t* __restrict__ group_bins;
+  Z* __restrict__ bias;
+};
+
+// Tree of path p: the last t with tree_paths[t] <= p.
+__device__ __forceinline__ int64_t tree_of_path(const int32_t* __restrict__ tree_paths,
+                                                int64_t T, int64_t p) {
+  int64_t lo = 0, hi = T - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (tree_paths[mid] <= p) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Per path: follow its turns from the root, merging the splits (ranges
+// intersected, zero fractions multiplied in root-to-leaf order), then write
+// the root (-1 - zero-fraction count, (-inf, +inf), v) and the features,
+// those whose zero fraction is 0 in the blob's precision first, each group in
+// ascending feature order, at the path's place; keep its bias term
+// v * prod(z) (the product over the features in ascending order).
+template <typename Z>
+__global__ void k_build_paths(DevEnsemble e, const uint64_t* __restrict__ dirs,
+                              const int32_t* __restrict__ dest,
+                              const int32_t* __restrict__ tree_paths, int64_t P, int64_t E,
+                              BlobOut<Z> out, double* __restrict__ term) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= P) return;
+  const int64_t t = tree_of_path(tree_paths, e.T, p);
+  const int64_t base = e.off[t];
+  const int64_t size = e.off[t + 1] - base;
+  float lo[kPlanMaxM], hi[kPlanMaxM];
+  double z[kPlanMaxM];
+  uint32_t on = 0;
+  const uint64_t turns = dirs[p];
+  int32_t node = 0;
+  for (int d = 0; d < 64; ++d) {
+    const int32_t a = e.left[base + node], b = e.right[base + node];
+    if (a < 0 || b < 0) break;   // the leaf
+    const bool right = (turns >> d) & 1ull;
+    const int32_t child = right ? b : a;
+    if (child >= size) break;    // never for an ensemble the plan walked
+    const int32_t f = e.feature[base + node];
+    if (f < 0 || f >= kPlanMaxM) break;
+    if (!((on >> f) & 1u)) {
+      on |= 1u << f;
+      lo[f] = -INFINITY;
+      hi[f] = INFINITY;
+      z[f] = 1.0;
+    }
+    const float th = e.threshold[base + node];
+    if (right) {
+      if (th > lo[f]) lo[f] = th;
+    } else {
+      if (th < hi[f]) hi[f] = th;
+    }
+    z[f] = z[f] * cover_ratio(e.cover[base + child], e.cover[base + node]);
+    node = child;
+  }
+  const double v = e.value[base + node];
+  uint32_t zmask = 0;
+  double prod = 1.0;
+  for (uint32_t m = on; m; m &= m - 1) {
+    const int f = __builtin_ctz(m);
+    zmask |= (uint32_t)((Z)z[f] == Z(0)) << f;
+    prod = prod * z[f];
+  }
+  term[p] = v * prod;
+  const int64_t d0 = dest[p];
+  const int n0 = __builtin_popcount(zmask);
+  // an ensemble other than the planned one could make the path longer than
+  // its place: no write leaves the element arrays
+  if (d0 < 0 || d0 + 1 + __builtin_popcount(on) > E) return;
+  out.feat[d0] = -1 - n0;
+  out.lower[d0] = -INFINITY;
+  out.upper[d0] = INFINITY;
+  out.zero[d0] = (Z)v;
+  int64_t iz = d0 + 1, ir = d0 + 1 + n0;
+  for (uint32_t m = on; m; m &= m - 1) {
+    const int f = __builtin_ctz(m);
+    const bool zf = (zmask >> f) & 1u;
+    const int64_t k = zf ? iz++ : ir++;
+    out.feat[k] = f;
+    out.lower[k] = lo[f];
+    out.upper[k] = hi[f];
+    out.zero[k] = (Z)z[f];
+  }
+}
+
+// Sum of x[i] for i in [a, b) in index order, by one wave: the lanes load 64
+// values at a time, then every lane adds them in order (all lanes hold the
+// same sum).  `keep[i]` selects the values that take part (NULL: all).
+__device__ __forceinline__ double wave_ordered_sum(const double* __restrict__ x, int64_t a,
+                                                   int64_t b, const int32_t* __restrict__ sel,
+                                                   int32_t want) {
+  const int lane = threadIdx.x & 63;
+  double s = 0.0;
+  for (int64_t c = a; c < b; c += 64) {
+    const int64_t i = c + lane;
+    const bool in = i < b && (sel == nullptr || sel[i] == want);
+    const double xi = in ? x[i] : 0.0;
+    const uint64_t take = __ballot(in);
+    const int n = (int)min<int64_t>(64, b - c);
+    for (int l = 0; l < n; ++l) {
+      const double y = __shfl(xi, l);
+      if ((take >> l) & 1ull) s = s + y;
+    }
+  }
+  return s;
+}
+
+// Per tree (one wave): its paths' bias terms in path order.
+__global__ void k_plan_tree_sums(const int32_t* __restrict__ tree_paths, int64_t T,
+                                 const double* __restrict__ term, double* __restrict__ tree_sum) {
+  const int64_t t = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const double s = wave_ordered_sum(term, tree_paths[t], tree_paths[t + 1], nullptr, 0);
+  if ((threadIdx.x & 63) == 0) tree_sum[t] = s;
+}
+
+// Per group (one wave): its trees' sums in tree order, in the blob's dtype.
+template <typename Z>
+__global__ void k_plan_bias(DevEnsemble e, const double* __restrict__ tree_sum, Z* __restrict__ bias) {
+  const int64_t g = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (g >= e.G) return;
+  const double s = wave_ordered_sum(tree_sum, 0, e.T, e.group, (int32_t)g);
+  if ((threadIdx.x & 63) == 0) bias[g] = (Z)s;
+}
+
+// The plan's bin starts and group ranges into the blob.
+__global__ void k_plan_bins(const int32_t* __restrict__ bin_start, int64_t K,
+                            const int32_t* __restrict__ group_bins, int64_t G,
+                            int32_t* __restrict__ out_bins, int32_t* __restrict__ out_groups) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i <= K) out_bins[i] = bin_start[i];
+  if (i <= G) out_groups[i] = group_bins[i];
+}
+
+// Zero bytes [a, b) of the blob, for up to kBlobArrays gaps (the padding that
+// aligns every array); spans[2 j], spans[2 j + 1] is gap j.
+struct Gaps {
+  int64_t span[2 * kBlobArrays];
+};
+
+__global__ void k_zero_gaps(unsigned char* __restrict__ blob, Gaps gaps) {
+  const int j = blockIdx.y;
+  const int64_t a = gaps.span[2 * j], b = gaps.span[2 * j + 1];
+  for (int64_t i = a + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < b;
+       i += (int64_t)gridDim.x * blockDim.x)
+    blob[i] = 0;
+}
+
+// ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
 
@@ -545,6 +714,116 @@ extern "C" gts_status gts_extract_paths_device(const gts_ensemble* ens, gts_path
   clear_error();
   return extract_device(ens, d_out, capacity, num_elements, num_paths, d_bias, d_workspace,
                         workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// gts_build_model_device
+// ---------------------------------------------------------------------------
+
+namespace gts {
+namespace {
+
+// Workspace of gts_build_model_device: path terms [P], tree sums [T].
+int64_t build_workspace(const gts_plan* plan, int64_t* tree_off) {
+  const int64_t a = up(8 * std::max<int64_t>(1, plan->num_paths));
+  *tree_off = a;
+  return a + up(8 * std::max<int64_t>(1, plan->num_trees));
+}
+
+template <typename Z>
+gts_status build_device(const gts_ensemble* ens, const gts_model* m, const gts_plan* plan,
+                        const char* d_plan, char* d_model, char* ws, hipStream_t s) {
+  DevEnsemble e{ens->tree_node_offsets, ens->tree_group, ens->left, ens->right, ens->feature,
+                ens->threshold, ens->cover, ens->value, ens->num_trees, ens->num_nodes,
+                ens->num_features, ens->num_groups};
+  const int64_t P = plan->num_paths, T = plan->num_trees, K = plan->num_bins;
+  const int64_t G = ens->num_groups;
+  BlobOut<Z> out{reinterpret_cast<int32_t*>(d_model + m->off[kFeat]),
+                 reinterpret_cast<float*>(d_model + m->off[kLower]),
+                 reinterpret_cast<float*>(d_model + m->off[kUpper]),
+                 reinterpret_cast<Z*>(d_model + m->off[kZero]),
+                 reinterpret_cast<int32_t*>(d_model + m->off[kBinStart]),
+                 reinterpret_cast<int32_t*>(d_model + m->off[kGroupBins]),
+                 reinterpret_cast<Z*>(d_model + m->off[kBias])};
+  const uint64_t* dirs = reinterpret_cast<const uint64_t*>(d_plan + plan->off[0]);
+  const int32_t* dest = reinterpret_cast<const int32_t*>(d_plan + plan->off[1]);
+  const int32_t* tree_paths = reinterpret_cast<const int32_t*>(d_plan + plan->off[2]);
+  const int32_t* bins = reinterpret_cast<const int32_t*>(d_plan + plan->off[3]);
+  const int32_t* groups = reinterpret_cast<const int32_t*>(d_plan + plan->off[4]);
+  int64_t tree_off = 0;
+  build_workspace(plan, &tree_off);
+  double* term = reinterpret_cast<double*>(ws);
+  double* tree_sum = reinterpret_cast<double*>(ws + tree_off);
+  // the alignment padding after every array
+  const size_t zb = sizeof(Z);
+  const int64_t sizes[kBlobArrays] = {4 * m->num_elements, 4 * m->num_elements,
+                                      4 * m->num_elements, (int64_t)zb * m->num_elements,
+                                      4 * (K + 1),         4 * (G + 1),
+                                      (int64_t)zb * G};
+  Gaps gaps;
+  for (int k = 0; k < kBlobArrays; ++k) {
+    gaps.span[2 * k] = m->off[k] + sizes[k];
+    gaps.span[2 * k + 1] = k + 1 < kBlobArrays ? m->off[k + 1] : m->bytes;
+  }
+  hipLaunchKernelGGL(k_zero_gaps, dim3(1, kBlobArrays), dim3(kThreads), 0, s,
+                     reinterpret_cast<unsigned char*>(d_model), gaps);
+  if (P > 0)
+    hipLaunchKernelGGL(k_build_paths<Z>, dim3(blocks(P)), dim3(kThreads), 0, s, e, dirs, dest,
+                       tree_paths, P, m->num_elements, out, term);
+  hipLaunchKernelGGL(k_plan_bins, dim3(blocks(std::max(K, G) + 1)), dim3(kThreads), 0, s, bins,
+                     K, groups, G, out.bin_start, out.group_bins);
+  constexpr int kWaves = kThreads / 64;
+  if (T > 0)
+    hipLaunchKernelGGL(k_plan_tree_sums, dim3((unsigned)((T + kWaves - 1) / kWaves)),
+                       dim3(kThreads), 0, s, tree_paths, T, term, tree_sum);
+  hipLaunchKernelGGL(k_plan_bias<Z>, dim3((unsigned)((G + kWaves - 1) / kWaves)),
+                     dim3(kThreads), 0, s, e, tree_sum, out.bias);
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(GTS_EDEVICE, "kernel launch failed: %s", hipGetErrorString(err));
+  return GTS_OK;
+}
+
+}  // namespace
+}  // namespace gts
+
+extern "C" gts_status gts_build_workspace_bytes(const gts_plan* plan, int64_t* bytes) {
+  clear_error();
+  if (plan == nullptr || bytes == nullptr) return fail(GTS_EINVAL, "plan and bytes must not be NULL");
+  int64_t t = 0;
+  *bytes = build_workspace(plan, &t);
+  return GTS_OK;
+}
+
+extern "C" gts_status gts_build_model_device(const gts_ensemble* ens, const gts_model* model,
+                                             const gts_plan* plan, const void* d_plan,
+                                             void* d_model, void* d_workspace,
+                                             int64_t workspace_bytes, void* stream) {
+  clear_error();
+  if (ens == nullptr || model == nullptr || plan == nullptr || d_plan == nullptr ||
+      d_model == nullptr || d_workspace == nullptr)
+    return fail(GTS_EINVAL, "NULL argument");
+  gts_status st = check_model(model);
+  if (st != GTS_OK) return st;
+  if (model->flags & GTS_MODEL_PRUNED) return fail(GTS_EINVAL, "a pruned model has no plan");
+  if (ens->num_trees != plan->num_trees || ens->num_nodes != plan->num_nodes ||
+      model->num_paths != plan->num_paths || model->num_bins != plan->num_bins ||
+      ens->num_features != model->num_features || ens->num_groups != model->num_groups)
+    return fail(GTS_EINVAL, "the ensemble, model and plan do not belong together");
+  if (ens->num_features > kPlanMaxM) return fail(GTS_EINVAL, "a plan needs M <= %d", kPlanMaxM);
+  if (plan->num_trees > 0 &&
+      (!ens->tree_node_offsets || !ens->tree_group || !ens->left || !ens->right ||
+       !ens->feature || !ens->threshold || !ens->cover || !ens->value))
+    return fail(GTS_EINVAL, "an ensemble array pointer is NULL");
+  int64_t t = 0;
+  const int64_t need = build_workspace(plan, &t);
+  if (workspace_bytes < need)
+    return fail(GTS_EBUFSIZE, "workspace of %lld bytes needed", (long long)need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const char* dp = static_cast<const char*>(d_plan);
+  char* dm = static_cast<char*>(d_model);
+  char* ws = static_cast<char*>(d_workspace);
+  return model->dtype == GTS_F64 ? build_device<double>(ens, model, plan, dp, dm, ws, s)
+                                 : build_device<float>(ens, model, plan, dp, dm, ws, s);
 }
 
 // ---------------------------------------------------------------------------

@@ -447,7 +447,9 @@ struct Walker {
   // messages and leaf order as walk().
   struct MaskFrame {
     int32_t node;
+    int32_t depth;   // splits from the root
     uint64_t mask;
+    uint64_t dirs;   // bit k set when the k-th split sends the path right
   };
   std::vector<MaskFrame> mstack;
 
@@ -466,7 +468,7 @@ struct Walker {
     const int32_t M = e->num_features;
     MaskFrame* const st = mstack.data();
     int32_t sp = 0;
-    st[sp++] = MaskFrame{0, 0};
+    st[sp++] = MaskFrame{0, 0, 0, 0};
     while (sp > 0) {
       const MaskFrame fr = st[--sp];
       const int32_t node = fr.node;
@@ -482,7 +484,7 @@ struct Walker {
       if (a < 0 && b < 0) {
         if (!std::isfinite(value[node]))
           return fail(GTS_EINVAL, "tree %lld leaf %d: value is not finite", (long long)t, node);
-        leaf(node, (size_t)__builtin_popcountll(fr.mask));
+        leaf(node, (size_t)__builtin_popcountll(fr.mask), fr.dirs, fr.depth);
         continue;
       }
       if (a < 0 || b < 0 || a >= n || b >= n)
@@ -498,8 +500,9 @@ struct Walker {
         return fail(GTS_EINVAL, "tree %lld node %d: node reached twice (cycle or shared child)",
                     (long long)t, node);
       const uint64_t m = fr.mask | 1ull << d;
-      st[sp++] = MaskFrame{b, m};
-      st[sp++] = MaskFrame{a, m};
+      const uint64_t right = fr.depth < 64 ? 1ull << fr.depth : 0;
+      st[sp++] = MaskFrame{b, fr.depth + 1, m, fr.dirs | right};
+      st[sp++] = MaskFrame{a, fr.depth + 1, m, fr.dirs};
     }
     return GTS_OK;
   }
@@ -1400,6 +1403,9 @@ struct alignas(128) TreeOut {
   std::vector<int64_t> first;  // per path: its first element in el / elf
   std::vector<int32_t> size;
   std::vector<double> v;
+  std::vector<uint64_t> dirs;  // per path, for a plan: bit k set when its k-th
+                               // split from the root sends it right
+  bool too_deep = false;       // a path of more than 64 splits (no plan)
   double term_sum = 0.0;       // the terms v * prod(z) summed in path order
   int32_t max_size = 0;
   int64_t elements = 0;        // sum of size
@@ -1409,6 +1415,8 @@ struct alignas(128) TreeOut {
     first.clear();
     size.clear();
     v.clear();
+    dirs.clear();
+    too_deep = false;
     term_sum = 0.0;
     max_size = 0;
     elements = 0;
@@ -1560,9 +1568,19 @@ void write_bin(const gts_model& m, char* blob, const Packing& pk, const PathSrc*
 }  // namespace
 }  // namespace gts
 
-extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_capacity,
-                                        int32_t alg, int32_t dtype, gts_model* model,
-                                        void* host_blob, int64_t blob_capacity, double* bias) {
+namespace gts {
+namespace {
+
+// Where gts_plan_model's outputs go (absent for gts_prepare_model).
+struct PlanOut {
+  gts_plan* plan;
+  char* host_plan;      // NULL: sizes only
+  int64_t capacity;
+};
+
+gts_status prepare_model(const gts_ensemble* ens, int32_t bin_capacity, int32_t alg,
+                         int32_t dtype, gts_model* model, void* host_blob,
+                         int64_t blob_capacity, double* bias, const PlanOut* po) {
   clear_error();
   if (model == nullptr) return fail(GTS_EINVAL, "model must not be NULL");
   if (bin_capacity < 1 || bin_capacity > kMaxPathLen)
@@ -1584,7 +1602,12 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     // keeps every path's merged elements (only their count for a size query)
     // per tree, and the bins are written from them.  The pool's workers write
     // into the calling thread's scratch.
-    const bool direct = host_blob != nullptr && one_path_per_wave(ens->num_features, dtype);
+    if (po != nullptr && !one_path_per_wave(ens->num_features, dtype))
+      return fail(GTS_EINVAL,
+                  "a plan needs a model whose every launch runs one path per wave "
+                  "(M <= 17 in fp32, M <= 11 in fp64); M = %d", ens->num_features);
+    const bool direct =
+        (host_blob != nullptr && one_path_per_wave(ens->num_features, dtype)) || po != nullptr;
     const bool count_only = sizes_only || direct;
     static thread_local PrepareScratch tls;
     PrepareScratch& sc = tls;
@@ -1595,10 +1618,14 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
       TreeOut& out = trees[(size_t)t];
       out.clear();
       if (count_only) {
-        auto count = [&](int32_t, size_t m) {
+        auto count = [&](int32_t, size_t m, uint64_t dirs = 0, int32_t depth = 0) {
           out.size.push_back((int32_t)m + 1);
           out.max_size = std::max(out.max_size, (int32_t)m + 1);
           out.elements += (int64_t)m + 1;
+          if (po != nullptr) {
+            out.dirs.push_back(dirs);
+            out.too_deep |= depth > 64;
+          }
         };
         return ens->num_features <= 64 ? w.count_walk(ens, t, count) : w.walk<false>(ens, t, count);
       }
@@ -1744,6 +1771,81 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
     BlobPlan bp = plan_blob(n, P, pk.K, ens->num_features, ens->num_groups, dtype, maxlen);
     bp.m.flags = pk.sorted ? GTS_MODEL_SORTED_BINS : 0;
     *model = bp.m;
+    if (po != nullptr) {
+      // the plan: per path its turns and its root's element offset, per tree
+      // its first path, the bins' element ranges and the groups' bin ranges
+      if (ens->num_nodes >= INT32_MAX || P >= INT32_MAX)
+        return fail(GTS_EINVAL, "too many nodes or paths for a plan's 32-bit indices");
+      gts_plan& pl = *po->plan;
+      std::memset(&pl, 0, sizeof(pl));
+      pl.num_paths = P;
+      pl.num_trees = T;
+      pl.num_bins = pk.K;
+      pl.num_nodes = ens->num_nodes;
+      for (int64_t t = 0; t < T; ++t)
+        if (trees[(size_t)t].too_deep)
+          return fail(GTS_EINVAL, "tree %lld: a path of more than 64 splits (a plan records "
+                      "each path's turns in 64 bits)", (long long)t);
+      const int64_t sizes[5] = {8 * P, 4 * P, 4 * (T + 1), 4 * (pk.K + 1),
+                                4 * ((int64_t)ens->num_groups + 1)};
+      int64_t cur = 0;
+      for (int k = 0; k < 5; ++k) {
+        pl.off[k] = cur;
+        cur += (sizes[k] + kBlobAlign - 1) / kBlobAlign * kBlobAlign;
+      }
+      pl.bytes = cur;
+      if (po->host_plan == nullptr) return GTS_OK;
+      if (po->capacity < pl.bytes)
+        return fail(GTS_EBUFSIZE, "plan capacity %lld < %lld bytes", (long long)po->capacity,
+                    (long long)pl.bytes);
+      char* hp = po->host_plan;
+      std::memset(hp, 0, (size_t)pl.bytes);
+      uint64_t* path_dirs = reinterpret_cast<uint64_t*>(hp + pl.off[0]);
+      int32_t* path_dest = reinterpret_cast<int32_t*>(hp + pl.off[1]);
+      int32_t* tree_paths = reinterpret_cast<int32_t*>(hp + pl.off[2]);
+      const std::vector<Fill>& fills = pk.fills;
+      const int64_t nf = (int64_t)fills.size();
+      {
+        // every placement's element offset, then every path's
+        std::vector<int32_t>& d_at = sc.d_at;
+        d_at.resize((size_t)P);
+        std::atomic<int64_t> next{0};
+        const int64_t step = std::max<int64_t>(1024, nf / (4 * nthreads) + 1);
+        Pool::get().run(nthreads, [&]() {
+          for (int64_t f0; (f0 = next.fetch_add(step)) < nf;) {
+            const int64_t f1 = std::min(nf, f0 + step);
+            for (int64_t f = f0; f < f1; ++f) {
+              const Fill& fl = fills[(size_t)f];
+              const int64_t b0 = pk.bin_offsets[(size_t)fl.b] + fl.w;
+              for (int32_t i = 0; i < fl.n; ++i)
+                d_at[(size_t)(fl.k + i)] = (int32_t)(b0 + (int64_t)i * fl.s);
+            }
+          }
+        });
+        std::atomic<int64_t> nt{0};
+        Pool::get().run(nthreads, [&]() {
+          for (int64_t t; (t = nt.fetch_add(8)) < T;) {
+            for (int64_t u = t; u < std::min(T, t + 8); ++u) {
+              const TreeOut& tr = trees[(size_t)u];
+              int64_t p = tree_first[(size_t)u];
+              tree_paths[u] = (int32_t)p;
+              for (size_t j = 0; j < tr.dirs.size(); ++j, ++p) {
+                path_dirs[p] = tr.dirs[j];
+                path_dest[p] = d_at[(size_t)kpos[(size_t)p]];
+              }
+            }
+          }
+        });
+      }
+      tree_paths[T] = (int32_t)P;
+      int32_t* bstart = reinterpret_cast<int32_t*>(hp + pl.off[3]);
+      int32_t* gbins = reinterpret_cast<int32_t*>(hp + pl.off[4]);
+      for (int64_t b = 0; b <= pk.K; ++b) bstart[b] = (int32_t)pk.bin_offsets[(size_t)b];
+      for (int64_t g = 0; g <= ens->num_groups; ++g) gbins[g] = 0;
+      for (int64_t b = 0; b < pk.K; ++b) gbins[pk.bin_group[(size_t)b] + 1] += 1;
+      for (int64_t g = 0; g < ens->num_groups; ++g) gbins[g + 1] += gbins[g];
+      return GTS_OK;
+    }
     if (sizes_only) return GTS_OK;
     if (host_blob != nullptr && blob_capacity < bp.m.bytes)
       return fail(GTS_EBUFSIZE, "blob_capacity %lld < %lld bytes", (long long)blob_capacity,
@@ -1848,4 +1950,26 @@ extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_cap
   } catch (const std::bad_alloc&) {
     return fail(GTS_ENOMEM, "host allocation failed");
   }
+}
+
+}  // namespace
+}  // namespace gts
+
+extern "C" gts_status gts_prepare_model(const gts_ensemble* ens, int32_t bin_capacity,
+                                        int32_t alg, int32_t dtype, gts_model* model,
+                                        void* host_blob, int64_t blob_capacity, double* bias) {
+  return gts::prepare_model(ens, bin_capacity, alg, dtype, model, host_blob, blob_capacity, bias,
+                            nullptr);
+}
+
+extern "C" gts_status gts_plan_model(const gts_ensemble* ens, int32_t bin_capacity, int32_t alg,
+                                     int32_t dtype, gts_model* model, gts_plan* plan,
+                                     void* host_plan, int64_t capacity) {
+  using namespace gts;
+  clear_error();
+  if (plan == nullptr) return fail(GTS_EINVAL, "plan must not be NULL");
+  if (capacity < 0 || (capacity > 0 && host_plan == nullptr))
+    return fail(GTS_EINVAL, "bad host_plan / capacity");
+  const PlanOut po{plan, static_cast<char*>(host_plan), capacity};
+  return prepare_model(ens, bin_capacity, alg, dtype, model, nullptr, 0, nullptr, &po);
 }

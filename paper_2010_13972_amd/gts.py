@@ -58,6 +58,13 @@ class ModelDesc(ctypes.Structure):
 _lib = None
 
 
+class PlanDesc(ctypes.Structure):
+    """gts_plan"""
+    _fields_ = [("num_paths", ctypes.c_int64), ("num_trees", ctypes.c_int64),
+                ("num_bins", ctypes.c_int64), ("num_nodes", ctypes.c_int64),
+                ("bytes", ctypes.c_int64), ("off", ctypes.c_int64 * 5)]
+
+
 class LaunchInfo(ctypes.Structure):
     """gts_launch (include/gts.h)."""
     _fields_ = [("rows_per_tile", ctypes.c_int32), ("waves", ctypes.c_int32),
@@ -107,6 +114,15 @@ def lib() -> ctypes.CDLL:
         L.gts_launch_config.argtypes = [ctypes.POINTER(ModelDesc), i64, i32,
                                         ctypes.POINTER(LaunchInfo)]
         L.gts_launch_config.restype = st
+        L.gts_plan_model.argtypes = [ctypes.POINTER(_Ensemble), i32, i32, i32,
+                                     ctypes.POINTER(ModelDesc), ctypes.POINTER(PlanDesc), vp,
+                                     i64]
+        L.gts_plan_model.restype = st
+        L.gts_build_workspace_bytes.argtypes = [ctypes.POINTER(PlanDesc), vp]
+        L.gts_build_workspace_bytes.restype = st
+        L.gts_build_model_device.argtypes = [ctypes.POINTER(_Ensemble), ctypes.POINTER(ModelDesc),
+                                             ctypes.POINTER(PlanDesc), vp, vp, vp, i64, vp]
+        L.gts_build_model_device.restype = st
         L.gts_prune_workspace_bytes.argtypes = [ctypes.POINTER(ModelDesc), i64, vp]
         L.gts_prune_workspace_bytes.restype = st
         L.gts_prune_model.argtypes = [ctypes.POINTER(ModelDesc), vp, vp, i64, i64, vp, i64,
@@ -348,6 +364,49 @@ def prepare_blob(ens, dtype: str = "f32", bin_capacity: int = 64, alg: str = "bf
            "gts_prepare_model")
     _cache[key] = int(desc.bytes)
     return desc, blob[:desc.bytes], bias
+
+
+def plan_model(ens, dtype: str = "f32", bin_capacity: int = 64, alg: str = "bfd",
+               out: Optional[np.ndarray] = None):
+    """gts_plan_model: (ModelDesc of the blob to build, PlanDesc, host plan blob
+    as a uint8 array; written into ``out`` when it is large enough)."""
+    s, keep = _ensemble_struct(ens)
+    desc, plan = ModelDesc(), PlanDesc()
+    _check(lib().gts_plan_model(ctypes.byref(s), bin_capacity, PACK_ALGS[alg], DTYPES[dtype],
+                                ctypes.byref(desc), ctypes.byref(plan), None, 0),
+           "gts_plan_model")
+    buf = out if out is not None and out.nbytes >= plan.bytes else np.empty(plan.bytes, np.uint8)
+    _check(lib().gts_plan_model(ctypes.byref(s), bin_capacity, PACK_ALGS[alg], DTYPES[dtype],
+                                ctypes.byref(desc), ctypes.byref(plan), _ptr(buf), buf.nbytes),
+           "gts_plan_model")
+    return desc, plan, buf[:plan.bytes]
+
+
+def build_workspace_bytes(plan: PlanDesc) -> int:
+    n = ctypes.c_int64(0)
+    _check(lib().gts_build_workspace_bytes(ctypes.byref(plan), ctypes.byref(n)),
+           "gts_build_workspace_bytes")
+    return int(n.value)
+
+
+def build_model_device(dens: "DeviceEnsemble", desc: ModelDesc, plan: PlanDesc, d_plan,
+                       dtype: str, out=None, workspace=None, stream=None) -> DeviceModel:
+    """gts_build_model_device: the model blob of a plan, written on the GPU
+    into ``out`` (a device uint8 tensor of desc.bytes; allocated when None)."""
+    import torch
+    dev = dens.tensors["left"].device
+    if out is None or out.numel() < desc.bytes:
+        out = torch.empty(desc.bytes, dtype=torch.uint8, device=dev)
+    need = build_workspace_bytes(plan)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _check(lib().gts_build_model_device(ctypes.byref(dens.struct), ctypes.byref(desc),
+                                        ctypes.byref(plan), ctypes.c_void_p(d_plan.data_ptr()),
+                                        ctypes.c_void_p(out.data_ptr()),
+                                        ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                        _stream_handle(stream)), "gts_build_model_device")
+    return DeviceModel(desc, out[:desc.bytes], desc.num_features, desc.num_groups, dtype,
+                       desc.num_paths, desc.num_bins, None)
 
 
 def prepare(ens, dtype: str = "f32", device="cuda", bin_capacity: int = 64,

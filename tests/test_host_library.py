@@ -493,3 +493,92 @@ def test_sorted_bins_flag(alg):
         if alg in ("bfd", "ffd", "none"):
             assert sorted_
         assert gts.prepare_blob(w.ensemble, "f32", alg=alg)[0].flags == desc.flags
+
+
+# --------------------------------------------------------------------------
+# gts_plan_model: the host half of a model built on the device
+# --------------------------------------------------------------------------
+
+def _plan_arrays(plan, hp):
+    P, T, K = plan.num_paths, plan.num_trees, plan.num_bins
+
+    def arr(k, t, n):
+        o = plan.off[k]
+        return np.frombuffer(hp[o:o + n * np.dtype(t).itemsize].tobytes(), t)
+
+    return (arr(0, np.uint64, P), arr(1, np.int32, P), arr(2, np.int32, T + 1),
+            arr(3, np.int32, K + 1))
+
+
+@pytest.mark.parametrize("name,dtype", [("tiny", "f64"), ("random0", "f32"), ("random2", "f64"),
+                                        ("random3", "f32")])
+def test_plan_walks_to_the_blob_paths(name, dtype):
+    """Every path's turns, followed from its tree's root, end at a leaf whose
+    value is the root slot of the blob at the path's place, and pass exactly
+    the features the blob holds for the path; the plan's bins are the blob's."""
+    ens = _workload(name).ensemble
+    desc, plan, hp = gts.plan_model(ens, dtype)
+    pdesc, blob, _ = gts.prepare_blob(ens, dtype)
+    assert bytes(desc) == bytes(pdesc)
+    dirs, dest, tree_paths, bins = _plan_arrays(plan, hp)
+    zt = np.float64 if dtype == "f64" else np.float32
+
+    def barr(k, t, n):
+        o = desc.off[k]
+        return np.frombuffer(blob[o:o + n * np.dtype(t).itemsize].tobytes(), t)
+
+    feat = barr(0, np.int32, desc.num_elements)
+    zero = barr(3, zt, desc.num_elements)
+    assert np.array_equal(bins, barr(4, np.int32, desc.num_bins + 1))
+    off = ens.tree_node_offsets
+    assert tree_paths[0] == 0 and tree_paths[-1] == desc.num_paths
+    for t in range(ens.num_trees):
+        base = off[t]
+        for p in range(tree_paths[t], tree_paths[t + 1]):
+            node, feats = 0, set()
+            for d in range(64):
+                a, b = ens.left[base + node], ens.right[base + node]
+                if a < 0 and b < 0:
+                    break
+                feats.add(int(ens.feature[base + node]))
+                node = b if (int(dirs[p]) >> d) & 1 else a
+            e = dest[p]
+            n0 = -1 - feat[e]
+            assert n0 >= 0 and zero[e] == zt(ens.value[base + node])
+            q = len(feats)
+            assert set(feat[e + 1:e + 1 + q].tolist()) == feats
+            assert e + 1 + q == len(feat) or feat[e + 1 + q] < 0
+
+
+def test_plan_refusals():
+    """Plans only for models whose launches run one path per wave, with
+    paths of at most 64 splits; the two-call idiom's capacity check."""
+    w = synth.random_workload(5, num_trees=3, max_depth=4, M=18, rows=4)
+    with pytest.raises(gts.GtsError) as e:
+        gts.plan_model(w.ensemble, "f32")
+    assert e.value.status == gts.GTS_EINVAL
+    w = synth.random_workload(5, num_trees=3, max_depth=4, M=12, rows=4)
+    with pytest.raises(gts.GtsError):
+        gts.plan_model(w.ensemble, "f64")      # M <= 11 in fp64
+    desc, plan, hp = gts.plan_model(w.ensemble, "f32")
+    s, keep = gts._ensemble_struct(w.ensemble)
+    small = np.empty(plan.bytes - 1, np.uint8)
+    st = gts.lib().gts_plan_model(ctypes.byref(s), 64, 0, 0, ctypes.byref(gts.ModelDesc()),
+                                  ctypes.byref(gts.PlanDesc()),
+                                  small.ctypes.data_as(ctypes.c_void_p), small.nbytes)
+    assert st == gts.GTS_EBUFSIZE
+
+    def chain(depth):
+        nodes, cover = [], 1000.0
+        for d in range(depth):
+            b = len(nodes)
+            nodes.append((b + 2, b + 1, d % 5, 0.5 + 0.001 * d, cover, 0.0))
+            nodes.append((-1, -1, -1, 0.0, 1.0, 0.5))
+            cover -= 1.0
+        nodes.append((-1, -1, -1, 0.0, cover, 1.0))
+        return nodes
+
+    gts.plan_model(synth.ensemble_from_lists([chain(64)], M=5), "f32")
+    with pytest.raises(gts.GtsError) as e:
+        gts.plan_model(synth.ensemble_from_lists([chain(65)], M=5), "f32")
+    assert "64 splits" in str(e.value)
