@@ -4,11 +4,16 @@ One step is one pass of the whole path over one batch of rows of the deep
 regression workload (1000 trees, depth <= 16, split probability 0.7, at most
 1024 leaves per tree, M = 8, 10 000 rows, fp32): path extraction with
 duplicate merging and the bias, Best-Fit-Decreasing packing into 64-element
-bins, device layout and upload of the model (host), then on the device the
-model pruned for the batch (the paths none of its rows reaches dropped,
-gts_prune_model; --no-prune leaves this out) and the SHAP kernel over the
-batch.  The rows X are resident in HBM before timing starts.  `value` is rows
-explained per second over the timed steps.
+bins and the device layout of the model, then on the device the model pruned
+for the batch (the paths none of its rows reaches dropped, gts_prune_model;
+--no-prune leaves this out) and the SHAP kernel over the batch.  By default
+(--build auto) the host runs the validating walk that counts the paths, the
+packing and each path's place (gts_plan_model), the plan and the ensemble
+are uploaded, and the GPU extracts, merges and lays out the paths and sums
+the bias (gts_build_model_device); --build host prepares the whole blob on
+the host (gts_prepare_model) and uploads it.  The rows X are resident in HBM
+before timing starts.  `value` is rows explained per second over the timed
+steps.
 
 The same JSON line carries:
   roofline      the SHAP kernel against the MI355X FP32 vector peak.  Its
@@ -234,7 +239,7 @@ def kernel_fn(gts, interactions):
 
 
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1,
-                  preps=2, prune=True):
+                  preps=2, prune=True, device_build=False):
     """Whole-path steps, pipelined.  `preps` host threads prepare the models
     of consecutive steps at the same time: step k runs gts_prepare_model on
     thread k mod preps, into pinned buffer k mod NB (NB = preps + 2), each
@@ -248,9 +253,14 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     calls the C ABI with arguments marshalled once.  With `prune`, each step
     first prunes its model for the batch (gts_prune_model, on the compute
     stream, into that stream's workspace) and runs the kernel on the pruned
-    model.  Timed on the host clock; the pruning and the kernel are bracketed
-    by HIP events on their stream, each preparation by the host clock of its
-    thread."""
+    model.  With `device_build`, a preparation is gts_plan_model (the host
+    half: the counting walk, the packing, each path's place) into a pinned
+    plan buffer; the upload moves the plan and the ensemble's node arrays
+    (from pinned copies) to the device, and the compute stream runs
+    gts_build_model_device (extraction and merging into the blob on the GPU)
+    before the pruning and the kernel.  Timed on the host clock; the build,
+    the pruning and the kernel are bracketed by HIP events on their stream,
+    each preparation by the host clock of its thread."""
     import collections
     import ctypes
     import gc
@@ -264,11 +274,37 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     copy = torch.cuda.Stream()
     desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
     nbytes = int(desc0.bytes)
-    pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(NB)]
     dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(NB)]
+    if device_build:
+        # the ensemble as the host walks it (pinned, so its upload is a DMA),
+        # one device copy per buffer, the plan buffers and the build workspace
+        _, plan0, hp0 = gts.plan_model(ens, dtype)
+        _, arrs = gts._ensemble_struct(ens)
+        ens_pin = {k: torch.from_numpy(v).pin_memory() for k, v in arrs.items()}
+        ens_dev = [{k: torch.empty_like(v, device="cuda") for k, v in ens_pin.items()}
+                   for _ in range(NB)]
+
+        def ens_struct(t):
+            return gts._Ensemble(ens.num_features, ens.num_groups, len(arrs["group"]),
+                                 len(arrs["left"]), *(t[k].data_ptr() for k in
+                                                      ("off", "group", "left", "right", "feat",
+                                                       "thr", "cover", "value")))
+
+        host_ens = ens_struct(ens_pin)
+        dev_ens = [ens_struct(d) for d in ens_dev]
+        pinned = [torch.empty(int(plan0.bytes), dtype=torch.uint8).pin_memory()
+                  for _ in range(NB)]
+        dev_plan = [torch.empty(int(plan0.bytes), dtype=torch.uint8, device="cuda")
+                    for _ in range(NB)]
+        plans = [gts.PlanDesc() for _ in range(NB)]
+        build_ws_bytes = gts.build_workspace_bytes(plan0)
+        build_ws = [torch.empty(build_ws_bytes, dtype=torch.uint8, device="cuda")
+                    for _ in range(nstreams)]
+    else:
+        pinned = [torch.empty(nbytes, dtype=torch.uint8).pin_memory() for _ in range(NB)]
     copied = [torch.cuda.Event() for _ in range(NB)]    # upload from pinned[i] done
     consumed = [torch.cuda.Event() for _ in range(NB)]  # kernel reading dev[i] done
-    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(steps)]
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(steps)]
     ens_struct, keep = gts._ensemble_struct(ens)
     descs = [gts.ModelDesc() for _ in range(NB)]
     biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NB)]
@@ -276,9 +312,23 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     shape = (rows, G, M + 1, M + 1) if interactions else (rows, G, M + 1)
     outs = [torch.empty(shape, dtype=torch.float64 if dtype == "f64" else torch.float32,
                         device="cuda") for _ in range(nstreams)]
-    prep_args = [(ctypes.byref(ens_struct), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
-                  ctypes.byref(descs[i]), ctypes.c_void_p(pinned[i].data_ptr()), nbytes,
-                  biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NB)]
+    if device_build:
+        prep = L.gts_plan_model
+        prep_args = [(ctypes.byref(host_ens), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
+                      ctypes.byref(descs[i]), ctypes.byref(plans[i]),
+                      ctypes.c_void_p(pinned[i].data_ptr()), pinned[i].numel())
+                     for i in range(NB)]
+        build_args = [[(ctypes.byref(dev_ens[i]), ctypes.byref(descs[i]), ctypes.byref(plans[i]),
+                        ctypes.c_void_p(dev_plan[i].data_ptr()),
+                        ctypes.c_void_p(dev[i].data_ptr()),
+                        ctypes.c_void_p(build_ws[j].data_ptr()), build_ws_bytes,
+                        ctypes.c_void_p(computes[j].cuda_stream))
+                       for j in range(nstreams)] for i in range(NB)]
+    else:
+        prep = L.gts_prepare_model
+        prep_args = [(ctypes.byref(ens_struct), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
+                      ctypes.byref(descs[i]), ctypes.c_void_p(pinned[i].data_ptr()), nbytes,
+                      biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NB)]
     run_args = [[(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
                   ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
                   ctypes.c_void_p(outs[j].data_ptr()), ctypes.c_void_p(computes[j].cuda_stream))
@@ -342,10 +392,10 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                     launched[k - NB].wait()   # step k-NB's kernel launch has read descs[i]
                     wait_for(copied[i])       # and its upload has read pinned[i]
                 h0 = time.perf_counter()
-                st = L.gts_prepare_model(*prep_args[i])
+                st = prep(*prep_args[i])
                 host_ms[k] = 1e3 * (time.perf_counter() - h0)
                 if st != gts.GTS_OK:
-                    raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
+                    raise RuntimeError(f"model preparation: {L.gts_last_error().decode()}")
             except BaseException as e:  # reported by the main thread
                 errors.append(e)
             ready.append(k)
@@ -370,7 +420,12 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                     k = ready.popleft()
                     i = k % NB
                     with torch.cuda.stream(copy):
-                        dev[i].copy_(pinned[i], non_blocking=True)
+                        if device_build:
+                            dev_plan[i].copy_(pinned[i], non_blocking=True)
+                            for key, t in ens_pin.items():
+                                ens_dev[i][key].copy_(t, non_blocking=True)
+                        else:
+                            dev[i].copy_(pinned[i], non_blocking=True)
                         copied[i].record(copy)
                     uploaded.append(k)
                     busy = True
@@ -380,17 +435,24 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                     stream = computes[j]
                     if timed:
                         ev[k][0].record(stream)
+                    if device_build:
+                        st = L.gts_build_model_device(*build_args[i][j])
+                        if st != gts.GTS_OK:
+                            raise RuntimeError(f"gts_build_model_device: "
+                                               f"{L.gts_last_error().decode()}")
+                    if timed:
+                        ev[k][1].record(stream)
                     if prune:
                         st = L.gts_prune_model(*prune_args[i][j])
                         if st != gts.GTS_OK:
                             raise RuntimeError(f"gts_prune_model: {L.gts_last_error().decode()}")
                     if timed:
-                        ev[k][1].record(stream)
+                        ev[k][2].record(stream)
                     st = launch(*(pruned_args[j] if prune else run_args[i][j]))
                     if st != gts.GTS_OK:
                         raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
                     if timed:
-                        ev[k][2].record(stream)
+                        ev[k][3].record(stream)
                     consumed[i].record(stream)
                     launched[k].set()
                     done += 1
@@ -438,9 +500,11 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
             q.put(None)
         for t in threads:
             t.join()
-    kern = np.array([b.elapsed_time(c) for a, b, c in ev])
-    prune_ms = np.array([a.elapsed_time(b) for a, b, c in ev])
-    return wall, kern, prune_ms, outs[(steps - 1) % nstreams], ref_model, np.array(host_ms)
+    build_ms = np.array([a.elapsed_time(b) for a, b, c, d in ev])
+    prune_ms = np.array([b.elapsed_time(c) for a, b, c, d in ev])
+    kern = np.array([c.elapsed_time(d) for a, b, c, d in ev])
+    return (wall, kern, prune_ms, build_ms, outs[(steps - 1) % nstreams], ref_model,
+            np.array(host_ms))
 
 
 def time_kernel(torch, gts, model, Xd, reps, interactions):
@@ -843,6 +907,12 @@ def main():
                          "times (rocprofv3)")
     ap.add_argument("--profile-pruned", action="store_true",
                     help="with --profile-launches: on the model pruned for the batch")
+    ap.add_argument("--build", default="auto", choices=["auto", "host", "device"],
+                    help="host: each step prepares the whole blob on the host "
+                         "(gts_prepare_model); device: the host plans it (gts_plan_model) "
+                         "and the GPU writes it (gts_build_model_device); auto: device "
+                         "where a plan can be made (one path per wave, paths of at most 64 "
+                         "splits), else host")
     ap.add_argument("--no-prune", action="store_true",
                     help="the steps run the kernel on the whole model, without pruning it "
                          "for the batch first")
@@ -896,8 +966,16 @@ def main():
     # small one's does
     preps = args.preps or (3 if ens.num_nodes >= (1 << 17) else 1)
     prune = not args.no_prune
-    wall, kern, prune_ms, out, model, step_host = time_pipeline(
-        torch, gts, ens, Xd, dtype, args.steps, args.warmup, inter, args.streams, preps, prune)
+    device_build = args.build == "device"
+    if args.build == "auto":
+        try:
+            gts.plan_model(ens, dtype)
+            device_build = True
+        except gts.GtsError:
+            device_build = False
+    wall, kern, prune_ms, build_ms, out, model, step_host = time_pipeline(
+        torch, gts, ens, Xd, dtype, args.steps, args.warmup, inter, args.streams, preps, prune,
+        device_build)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)
@@ -929,13 +1007,18 @@ def main():
                    "path_elements": wm["path_elements"], "bins": int(model.num_bins),
                    "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
                               + (f", {ens.num_features + 1}]" if inter else "]")),
-                   "step": "extract + merge + bias + BFD pack (B=64) + layout (host) + upload "
+                   "step": ("validating walk with path counts + BFD pack (B=64) + each "
+                            "path's place (host) + upload of the plan and the ensemble + "
+                            "extract + merge + bias + layout (device) "
+                            if device_build else
+                            "extract + merge + bias + BFD pack (B=64) + layout (host) + upload ")
                            + ("+ batch pruning (device) " if prune else "")
                            + ("+ interaction kernel" if inter else "+ SHAP kernel")
                            + f"; {preps} steps' host work in flight at once, each on "
                            + "its share of the cores; uploads and host work overlap the "
                            + "kernels of earlier steps",
                    "compute_streams": args.streams, "preparations_in_flight": preps,
+                   "model_build": "device" if device_build else "host",
                    "pruned_for_the_batch": ({"paths": ppaths, "path_elements": pelems,
                                              "bins": pbins} if prune else None)},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
@@ -945,6 +1028,7 @@ def main():
                                + (" on the model pruned for the batch" if prune else ""),
                      "kernel_ms": kern_ms,
                      "prune_ms_in_steps": float(prune_ms.mean()) if prune else None,
+                     "device_build_ms_in_steps": float(build_ms.mean()) if device_build else None,
                      "kernel_launches": int(len(kern)),
                      "kernel_ms_back_to_back": float(k_only.mean()),
                      "modelled_gflop_per_launch": wm["flops_live"] / 1e9,
