@@ -404,6 +404,7 @@ __global__ void k_build_paths(DevEnsemble e, const uint64_t* __restrict__ dirs,
   uint32_t on = 0;
   const uint64_t turns = dirs[p];
   int32_t node = 0;
+  double cover = e.cover[base];   // the current node's
   for (int d = 0; d < 64; ++d) {
     const int32_t a = e.left[base + node], b = e.right[base + node];
     if (a < 0 || b < 0) break;   // the leaf
@@ -424,7 +425,9 @@ __global__ void k_build_paths(DevEnsemble e, const uint64_t* __restrict__ dirs,
     } else {
       if (th < hi[f]) hi[f] = th;
     }
-    z[f] = z[f] * cover_ratio(e.cover[base + child], e.cover[base + node]);
+    const double child_cover = e.cover[base + child];
+    z[f] = z[f] * cover_ratio(child_cover, cover);
+    cover = child_cover;
     node = child;
   }
   const double v = e.value[base + node];
@@ -457,23 +460,43 @@ __global__ void k_build_paths(DevEnsemble e, const uint64_t* __restrict__ dirs,
   }
 }
 
+// Lane l's value of x (l wave-uniform), through two scalar reads.
+__device__ __forceinline__ double read_lane(double x, int l) {
+  const long long bits = __double_as_longlong(x);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)bits, l);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(bits >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 // Sum of x[i] for i in [a, b) in index order, by one wave: the lanes load 64
-// values at a time, then every lane adds them in order (all lanes hold the
-// same sum).  `keep[i]` selects the values that take part (NULL: all).
+// values at a time, then every lane adds them in order, reading each from
+// its lane (all lanes hold the same sum).  sel[i] == want selects the values
+// that take part (sel NULL: all).
 __device__ __forceinline__ double wave_ordered_sum(const double* __restrict__ x, int64_t a,
                                                    int64_t b, const int32_t* __restrict__ sel,
                                                    int32_t want) {
   const int lane = threadIdx.x & 63;
   double s = 0.0;
+  // the next chunk is loaded before the current one is added up, so the
+  // loads wait behind the adds instead of the other way round
+  int64_t i = a + lane;
+  bool in = i < b && (sel == nullptr || sel[i] == want);
+  double xi = in ? x[i] : 0.0;
   for (int64_t c = a; c < b; c += 64) {
-    const int64_t i = c + lane;
-    const bool in = i < b && (sel == nullptr || sel[i] == want);
-    const double xi = in ? x[i] : 0.0;
-    const uint64_t take = __ballot(in);
-    const int n = (int)min<int64_t>(64, b - c);
-    for (int l = 0; l < n; ++l) {
-      const double y = __shfl(xi, l);
-      if ((take >> l) & 1ull) s = s + y;
+    const uint64_t take0 = __ballot(in);
+    const double cur = xi;
+    i = c + 64 + lane;
+    in = i < b && (sel == nullptr || sel[i] == want);
+    xi = in ? x[i] : 0.0;
+    if (take0 == ~0ull) {
+#pragma unroll
+      for (int l = 0; l < 64; ++l) s = s + read_lane(cur, l);
+    } else {
+#pragma unroll
+      for (int l = 0; l < 64; ++l) {
+        const double y = read_lane(cur, l);
+        s = ((take0 >> l) & 1ull) ? s + y : s;
+      }
     }
   }
   return s;
