@@ -80,13 +80,14 @@ def build(verbose: bool = False, save_temps: bool = False) -> str:
         dev_cmds.append(cmd)
     ext_obj = os.path.join(BUILD, "gts_extract.o")
     ext_cmd = ["hipcc", *EXTRACT_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c",
-               os.path.join(CSRC, "gts_extract.hip"), "-o", ext_obj]
+               os.path.join(CSRC, "gts_extract.hip"), "-o", ext_obj,
+               "-Rpass-analysis=kernel-resource-usage"]
     cmds = [host_cmd, ext_cmd] + dev_cmds
     with ThreadPoolExecutor(min(len(cmds), os.cpu_count() or 4)) as ex:
         outs = list(ex.map(lambda c: _run_capture(c, verbose), cmds))
-    # kernel-resource remarks of the kernel units, one line per kernel
+    # kernel-resource remarks of the device units, one line per kernel
     report = []
-    for lines in outs[2:]:
+    for lines in outs[1:]:
         cur = {}
         for l in lines:
             if "remark:" not in l:

@@ -371,16 +371,42 @@ struct BlobOut {
   Z* __restrict__ bias;
 };
 
-// Tree of path p: the last t with tree_paths[t] <= p.
-__device__ __forceinline__ int64_t tree_of_path(const int32_t* __restrict__ tree_paths,
-                                                int64_t T, int64_t p) {
-  int64_t lo = 0, hi = T - 1;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if (tree_paths[mid] <= p) lo = mid;
-    else hi = mid - 1;
+// Tree of every lane's path p, the last t with tree_paths[t] <= p (tree_paths
+// is non-decreasing, tree_paths[0] = 0, tree_paths[T] = P).  The wave holds 64
+// consecutive paths from p0 on.  It first narrows [0, T) to the tree of p0,
+// probing 64 evenly spaced starts a round (two rounds for 4096 trees); then
+// every lane counts, by bisection over the lanes, how many of the next 64 tree
+// starts lie at or before its own path.  Only empty trees can put more than 63
+// starts inside one wave; those lanes finish with a bisection of their own.
+// Every lane of the wave must take part.
+__device__ __forceinline__ int64_t wave_tree_of_path(const int32_t* __restrict__ tp, int64_t T,
+                                                     int64_t p0, int64_t p) {
+  const int lane = threadIdx.x & 63;
+  int64_t lo = 0, n = T;   // the tree of p0 is in [lo, lo + n)
+  while (n > 1) {
+    const int64_t step = (n + 63) >> 6;
+    const int64_t i = lo + lane * step;
+    const uint64_t m = __ballot(i < lo + n && tp[i] <= p0);   // a prefix of the lanes, lane 0 in it
+    const int64_t next = lo + (int64_t)(63 - __builtin_clzll(m)) * step;
+    n = min(step, lo + n - next);
+    lo = next;
   }
-  return lo;
+  const int64_t j = lo + 1 + lane;
+  const int32_t v = j <= T ? tp[j] : INT32_MAX;   // non-decreasing over the lanes
+  int c = 0;
+  for (int b = 32; b >= 1; b >>= 1)
+    if (__shfl(v, c + b - 1) <= p) c += b;
+  if (c == 63 && __shfl(v, 63) <= p) c = 64;
+  int64_t t = lo + c;
+  if (c == 64) {
+    int64_t hi = T - 1;
+    while (t < hi) {
+      const int64_t mid = (t + hi + 1) >> 1;
+      if (tp[mid] <= p) t = mid;
+      else hi = mid - 1;
+    }
+  }
+  return min(t, T - 1);
 }
 
 // Per path: follow its turns from the root, merging the splits (ranges
@@ -388,55 +414,72 @@ __device__ __forceinline__ int64_t tree_of_path(const int32_t* __restrict__ tree
 // the root (-1 - zero-fraction count, (-inf, +inf), v) and the features,
 // those whose zero fraction is 0 in the blob's precision first, each group in
 // ascending feature order, at the path's place; keep its bias term
-// v * prod(z) (the product over the features in ascending order).
-template <typename Z>
+// v * prod(z) (the product over the features in ascending order).  The merged
+// ranges and fractions of the MF possible features stay in registers: every
+// update goes through all MF slots with a select, since an array indexed by
+// the split's feature would live in private memory.  A level issues one batch
+// of loads, the node's own fields with its cover, whose ratio to the parent's
+// cover is the fraction of the split above.
+template <typename Z, int MF>
 __global__ void k_build_paths(DevEnsemble e, const uint64_t* __restrict__ dirs,
                               const int32_t* __restrict__ dest,
                               const int32_t* __restrict__ tree_paths, int64_t P, int64_t E,
                               BlobOut<Z> out, double* __restrict__ term) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= P) return;
-  const int64_t t = tree_of_path(tree_paths, e.T, p);
+  const int64_t wave0 = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~63);
+  if (wave0 >= P) return;   // the whole wave
+  const int64_t own = wave0 + (threadIdx.x & 63);
+  const int64_t p = min(own, P - 1);
+  const int64_t t = wave_tree_of_path(tree_paths, e.T, wave0, p);
+  if (own >= P) return;
   const int64_t base = e.off[t];
   const int64_t size = e.off[t + 1] - base;
-  float lo[kPlanMaxM], hi[kPlanMaxM];
-  double z[kPlanMaxM];
+  if (size <= 0) return;   // never for an ensemble the plan walked
+  float lo[MF], hi[MF];
+  double z[MF];
+#pragma unroll
+  for (int k = 0; k < MF; ++k) {
+    lo[k] = -INFINITY;
+    hi[k] = INFINITY;
+    z[k] = 1.0;
+  }
   uint32_t on = 0;
   const uint64_t turns = dirs[p];
   int32_t node = 0;
-  double cover = e.cover[base];   // the current node's
-  for (int d = 0; d < 64; ++d) {
-    const int32_t a = e.left[base + node], b = e.right[base + node];
-    if (a < 0 || b < 0) break;   // the leaf
+  int32_t pf = -1;    // the feature of the split above node
+  double pc = 0.0;    // the cover of node's parent
+  for (int d = 0;; ++d) {
+    const int64_t gi = base + node;
+    const int32_t a = e.left[gi], b = e.right[gi], f = e.feature[gi];
+    const float th = e.threshold[gi];
+    const double c = e.cover[gi];
+    if (pf >= 0) {
+      const double r = cover_ratio(c, pc);
+#pragma unroll
+      for (int k = 0; k < MF; ++k) z[k] = k == pf ? z[k] * r : z[k];
+    }
+    if (a < 0 || b < 0 || d == 64) break;   // the leaf (or 64 turns taken)
     const bool right = (turns >> d) & 1ull;
     const int32_t child = right ? b : a;
-    if (child >= size) break;    // never for an ensemble the plan walked
-    const int32_t f = e.feature[base + node];
-    if (f < 0 || f >= kPlanMaxM) break;
-    if (!((on >> f) & 1u)) {
-      on |= 1u << f;
-      lo[f] = -INFINITY;
-      hi[f] = INFINITY;
-      z[f] = 1.0;
+    // never for an ensemble the plan walked
+    if (child >= size || f < 0 || f >= MF) break;
+    on |= 1u << f;
+#pragma unroll
+    for (int k = 0; k < MF; ++k) {
+      lo[k] = k == f && right && th > lo[k] ? th : lo[k];
+      hi[k] = k == f && !right && th < hi[k] ? th : hi[k];
     }
-    const float th = e.threshold[base + node];
-    if (right) {
-      if (th > lo[f]) lo[f] = th;
-    } else {
-      if (th < hi[f]) hi[f] = th;
-    }
-    const double child_cover = e.cover[base + child];
-    z[f] = z[f] * cover_ratio(child_cover, cover);
-    cover = child_cover;
+    pf = f;
+    pc = c;
     node = child;
   }
   const double v = e.value[base + node];
   uint32_t zmask = 0;
   double prod = 1.0;
-  for (uint32_t m = on; m; m &= m - 1) {
-    const int f = __builtin_ctz(m);
-    zmask |= (uint32_t)((Z)z[f] == Z(0)) << f;
-    prod = prod * z[f];
+#pragma unroll
+  for (int k = 0; k < MF; ++k) {
+    const bool in = (on >> k) & 1u;
+    zmask |= (uint32_t)(in && (Z)z[k] == Z(0)) << k;
+    prod = in ? prod * z[k] : prod;
   }
   term[p] = v * prod;
   const int64_t d0 = dest[p];
@@ -449,14 +492,18 @@ __global__ void k_build_paths(DevEnsemble e, const uint64_t* __restrict__ dirs,
   out.upper[d0] = INFINITY;
   out.zero[d0] = (Z)v;
   int64_t iz = d0 + 1, ir = d0 + 1 + n0;
-  for (uint32_t m = on; m; m &= m - 1) {
-    const int f = __builtin_ctz(m);
-    const bool zf = (zmask >> f) & 1u;
-    const int64_t k = zf ? iz++ : ir++;
-    out.feat[k] = f;
-    out.lower[k] = lo[f];
-    out.upper[k] = hi[f];
-    out.zero[k] = (Z)z[f];
+#pragma unroll
+  for (int k = 0; k < MF; ++k) {
+    if ((on >> k) & 1u) {
+      const bool zf = (zmask >> k) & 1u;
+      const int64_t q = zf ? iz : ir;
+      iz += zf ? 1 : 0;
+      ir += zf ? 0 : 1;
+      out.feat[q] = k;
+      out.lower[q] = lo[k];
+      out.upper[q] = hi[k];
+      out.zero[q] = (Z)z[k];
+    }
   }
 }
 
@@ -790,9 +837,13 @@ gts_status build_device(const gts_ensemble* ens, const gts_model* m, const gts_p
   }
   hipLaunchKernelGGL(k_zero_gaps, dim3(1, kBlobArrays), dim3(kThreads), 0, s,
                      reinterpret_cast<unsigned char*>(d_model), gaps);
-  if (P > 0)
-    hipLaunchKernelGGL(k_build_paths<Z>, dim3(blocks(P)), dim3(kThreads), 0, s, e, dirs, dest,
-                       tree_paths, P, m->num_elements, out, term);
+  // a model of at most 8 features carries 8 slots per path, any other 17
+  if (P > 0 && e.M <= 8)
+    hipLaunchKernelGGL((k_build_paths<Z, 8>), dim3(blocks(P)), dim3(kThreads), 0, s, e, dirs,
+                       dest, tree_paths, P, m->num_elements, out, term);
+  else if (P > 0)
+    hipLaunchKernelGGL((k_build_paths<Z, kPlanMaxM>), dim3(blocks(P)), dim3(kThreads), 0, s, e,
+                       dirs, dest, tree_paths, P, m->num_elements, out, term);
   hipLaunchKernelGGL(k_plan_bins, dim3(blocks(std::max(K, G) + 1)), dim3(kThreads), 0, s, bins,
                      K, groups, G, out.bin_start, out.group_bins);
   constexpr int kWaves = kThreads / 64;

@@ -41,10 +41,32 @@ def chain(depth, M):
     return nodes
 
 
+def stumps(n):
+    """n small trees: single leaves, one-split stumps and two-split trees, so a
+    wave of 64 paths spans up to 64 trees and the tree search takes two rounds
+    of probes."""
+    trees = []
+    for k in range(n):
+        c = 100.0 + k
+        if k % 3 == 0:
+            trees.append([(-1, -1, -1, 0.0, c, 0.01 * k)])
+        elif k % 3 == 1:
+            trees.append([(1, 2, k % 5, np.float32(0.1 * (k % 7)), c, 0.0),
+                          (-1, -1, -1, 0.0, c - 1.0 - (k % 4), -0.5),
+                          (-1, -1, -1, 0.0, 1.0 + (k % 4), 0.5 + 0.001 * k)])
+        else:
+            trees.append([(1, 2, k % 5, np.float32(0.2), c, 0.0),
+                          (3, 4, (k + 1) % 5, np.float32(-0.3), c - 10.0, 0.0),
+                          (-1, -1, -1, 0.0, 10.0, 1.0),
+                          (-1, -1, -1, 0.0, 0.0, 2.0 - 0.01 * k),
+                          (-1, -1, -1, 0.0, c - 10.0, -1.0)])
+    return synth.ensemble_from_lists(trees, M=5, num_groups=2)
+
+
 # random<s>: M = 5 + 3 s (fp64 plans need M <= 11)
 CASES = [("tiny", "f64"), ("deep", "f32"), ("deep", "f64"), ("random0", "f32"), ("random1", "f64"),
          ("random2", "f64"), ("random3", "f32"), ("chain64", "f32"), ("chain64", "f64"),
-         ("empty", "f32")]
+         ("stumps", "f32"), ("stumps", "f64"), ("empty", "f32")]
 
 
 def case(name):
@@ -55,6 +77,8 @@ def case(name):
     if name == "chain64":
         return synth.ensemble_from_lists([chain(64, 7), chain(30, 7)], M=7, num_groups=2,
                                          tree_group=[1, 0])
+    if name == "stumps":
+        return stumps(300)
     if name == "empty":
         return empty_ensemble(4, 2)
     return synth.workload(name).ensemble

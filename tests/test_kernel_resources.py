@@ -99,3 +99,20 @@ def test_prune_kernels_use_no_private_memory():
                     seen.add(n)
                     assert d["ScratchSize [bytes/lane]"] == "0", d
     assert seen == set(names)
+
+
+def test_device_build_kernels_use_no_private_memory():
+    """The kernels that write a model blob from a host plan keep every path's
+    merged feature ranges and fractions in registers: no scratch."""
+    if not os.path.exists(REPORT):
+        pytest.skip("library not built (the report comes from the build)")
+    names = ("k_build_paths", "k_plan_tree_sums", "k_plan_bias", "k_plan_bins", "k_zero_gaps")
+    seen = set()
+    with open(REPORT) as f:
+        for line in f:
+            d = dict(kv.split("=", 1) for kv in line.rstrip("\n").split("\t"))
+            for n in names:
+                if n in d["name"]:
+                    seen.add(n)
+                    assert d["ScratchSize [bytes/lane]"] == "0", d
+    assert seen == set(names)
