@@ -255,8 +255,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     stream, into that stream's workspace) and runs the kernel on the pruned
     model.  With `device_build`, a preparation is gts_plan_model (the host
     half: the counting walk, the packing, each path's place) into a pinned
-    plan buffer; the upload moves the plan and the ensemble's node arrays
-    (from pinned copies) to the device, and the compute stream runs
+    plan buffer; the ensemble's node arrays (from pinned copies) go up as soon
+    as the step's device buffers are free, the plan once it is made, and the
+    compute stream runs
     gts_build_model_device (extraction and merging into the blob on the GPU)
     before the pruning and the kernel.  Timed on the host clock; the build,
     the pruning and the kernel are bracketed by HIP events on their stream,
@@ -412,18 +413,38 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
             # that kernel was launched before step k's preparation began.)
             uploaded = collections.deque()
             done = 0
+            ens_sent = [False] * n
+            ens_next = 0
+
+            def send_ensemble(k):
+                with torch.cuda.stream(copy):
+                    for key, t in ens_pin.items():
+                        ens_dev[k % NB][key].copy_(t, non_blocking=True)
+                ens_sent[k] = True
+
             while done < n:
                 busy = False
                 if errors:
                     raise errors[0]
+                # a device build's ensemble upload needs no plan: it goes out
+                # as soon as the step's device buffers are free (the kernel of
+                # step k - NB launched and done), ahead of the plan's upload
+                # on the same copy stream
+                while (device_build and ens_next < n and
+                       (ens_next < NB or launched[ens_next - NB].is_set()) and
+                       consumed[ens_next % NB].query()):
+                    if not ens_sent[ens_next]:
+                        send_ensemble(ens_next)
+                    ens_next += 1
+                    busy = True
                 while ready and consumed[ready[0] % NB].query():
                     k = ready.popleft()
                     i = k % NB
                     with torch.cuda.stream(copy):
                         if device_build:
+                            if not ens_sent[k]:
+                                send_ensemble(k)
                             dev_plan[i].copy_(pinned[i], non_blocking=True)
-                            for key, t in ens_pin.items():
-                                ens_dev[i][key].copy_(t, non_blocking=True)
                         else:
                             dev[i].copy_(pinned[i], non_blocking=True)
                         copied[i].record(copy)
@@ -897,7 +918,8 @@ def main():
                     help="compute streams the pipelined steps alternate between")
     ap.add_argument("--preps", type=int, default=0,
                     help="model preparations in flight at once in the pipelined steps "
-                         "(0: three for models of 128 k nodes or more, else one)")
+                         "(0: for models of 128 k nodes or more five plans of device "
+                         "builds or three host preparations, else one)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     ap.add_argument("--profile-launches", type=int, default=0,
@@ -961,10 +983,6 @@ def main():
     rows = w.X.shape[0]
     Xd = torch.from_numpy(w.X).cuda()
 
-    # a large model's preparation does not use 16 cores fully: three in
-    # flight, each on a third of the cores, prepare more models per second; a
-    # small one's does
-    preps = args.preps or (3 if ens.num_nodes >= (1 << 17) else 1)
     prune = not args.no_prune
     device_build = args.build == "device"
     if args.build == "auto":
@@ -973,6 +991,10 @@ def main():
             device_build = True
         except gts.GtsError:
             device_build = False
+    # a large model's host work does not use 16 cores fully: several steps'
+    # in flight, each on its share of the cores, finish more of them per
+    # second (five plans, or three whole preparations); a small one's does
+    preps = args.preps or ((5 if device_build else 3) if ens.num_nodes >= (1 << 17) else 1)
     wall, kern, prune_ms, build_ms, out, model, step_host = time_pipeline(
         torch, gts, ens, Xd, dtype, args.steps, args.warmup, inter, args.streams, preps, prune,
         device_build)
