@@ -239,11 +239,13 @@ def kernel_fn(gts, interactions):
 
 
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1,
-                  preps=2, prune=True, device_build=False):
+                  preps=2, prune=True, device_build=False, prep_threads=None):
     """Whole-path steps, pipelined.  `preps` host threads prepare the models
     of consecutive steps at the same time: step k runs gts_prepare_model on
-    thread k mod preps, into pinned buffer k mod NB (NB = preps + 2), each
-    thread capped to its share of the cores (gts_set_host_threads).  The main
+    thread k mod preps, into pinned buffer k mod NB (NB = preps + 2).  The
+    preparations share the library's worker pool, which serves the one that
+    started first (each may use every core unless `prep_threads` caps it
+    through gts_set_host_threads).  The main
     thread uploads step k's model on a copy stream into device buffer k mod NB
     once it is prepared and launches the kernel of step k as soon as that
     upload has finished, on compute stream k mod nstreams; the compute
@@ -353,7 +355,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                     Xd.stride(0), ctypes.c_void_p(outs[j].data_ptr()),
                     ctypes.c_void_p(computes[j].cuda_stream)) for j in range(nstreams)]
     cores = min(16, len(os.sched_getaffinity(0)))
-    share = 0 if preps == 1 else max(1, cores // preps)
+    share = 0 if prep_threads is None else prep_threads
 
     # persistent preparation threads (their per-thread working memory stays
     # warm between runs), each running the tasks of its queue in order
@@ -916,10 +918,11 @@ def main():
     ap.add_argument("--cpu-limit", type=float, default=4.0)
     ap.add_argument("--streams", type=int, default=1,
                     help="compute streams the pipelined steps alternate between")
+    ap.add_argument("--prep-threads", type=int, default=0,
+                    help="host threads each preparation in flight may use (0: every core)")
     ap.add_argument("--preps", type=int, default=0,
                     help="model preparations in flight at once in the pipelined steps "
-                         "(0: for models of 128 k nodes or more five plans of device "
-                         "builds or three host preparations, else one)")
+                         "(0: three for models of 128 k nodes or more, else one)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run a plain 256 MiB device copy first (counter calibration)")
     ap.add_argument("--profile-launches", type=int, default=0,
@@ -939,8 +942,10 @@ def main():
                     help="the steps run the kernel on the whole model, without pruning it "
                          "for the batch first")
     args = ap.parse_args()
-    if args.steps < 1 or args.warmup < 0 or args.streams < 1 or args.preps < 0:
-        ap.error("--steps and --streams must be at least 1, --warmup and --preps at least 0")
+    if (args.steps < 1 or args.warmup < 0 or args.streams < 1 or args.preps < 0 or
+            args.prep_threads < 0):
+        ap.error("--steps and --streams must be at least 1, --warmup, --preps and "
+                 "--prep-threads at least 0")
 
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; the row-sharded "
@@ -991,13 +996,13 @@ def main():
             device_build = True
         except gts.GtsError:
             device_build = False
-    # a large model's host work does not use 16 cores fully: several steps'
-    # in flight, each on its share of the cores, finish more of them per
-    # second (five plans, or three whole preparations); a small one's does
-    preps = args.preps or ((5 if device_build else 3) if ens.num_nodes >= (1 << 17) else 1)
+    # a large model's host work does not use 16 cores fully: three steps' in
+    # flight at once finish more of them per second (the worker pool gives
+    # every free core to the one that started first); a small one's does
+    preps = args.preps or (3 if ens.num_nodes >= (1 << 17) else 1)
     wall, kern, prune_ms, build_ms, out, model, step_host = time_pipeline(
         torch, gts, ens, Xd, dtype, args.steps, args.warmup, inter, args.streams, preps, prune,
-        device_build)
+        device_build, args.prep_threads)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)
@@ -1036,9 +1041,9 @@ def main():
                             "extract + merge + bias + BFD pack (B=64) + layout (host) + upload ")
                            + ("+ batch pruning (device) " if prune else "")
                            + ("+ interaction kernel" if inter else "+ SHAP kernel")
-                           + f"; {preps} steps' host work in flight at once, each on "
-                           + "its share of the cores; uploads and host work overlap the "
-                           + "kernels of earlier steps",
+                           + f"; {preps} steps' host work in flight at once on a shared "
+                           + "worker pool that serves the oldest first; uploads and host "
+                           + "work overlap the kernels of earlier steps",
                    "compute_streams": args.streams, "preparations_in_flight": preps,
                    "model_build": "device" if device_build else "host",
                    "pruned_for_the_batch": ({"paths": ppaths, "path_elements": pelems,

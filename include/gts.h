@@ -505,9 +505,10 @@ gts_status gts_prune_model(const gts_model *model, const void *d_model, const fl
  * process's affinity mask, up to 16).  The setting belongs to the calling
  * thread and lasts until its next call.  For running several preparations
  * at once, each on part of the cores (a pipeline that prepares the models
- * of its next steps in parallel): calls from different threads run on
- * different teams of the worker pool (up to four at once; a fifth runs on
- * its caller alone).  Results never depend on the thread count.
+ * of its next steps in parallel): calls from different threads share one
+ * pool of workers, and a free worker serves the preparation that started
+ * first, so the oldest call in flight finishes soonest.  Results never
+ * depend on the thread count.
  * Errors: GTS_EINVAL for n < 0.
  */
 gts_status gts_set_host_threads(int32_t n);

@@ -100,23 +100,38 @@ gts_status validate_ensemble(const gts_ensemble* e) {
   return GTS_OK;
 }
 
+// Priority of a parallel region: the ticket of the host call it belongs to.
+// A preparation takes a ticket when it starts (TicketScope); a region of a
+// thread without one takes its own when it opens.  Both come from one
+// counter, so a smaller ticket is an earlier start.
+std::atomic<uint64_t> g_tickets{0};
+thread_local uint64_t t_ticket = 0;
+
+struct TicketScope {
+  uint64_t saved;
+  TicketScope() : saved(t_ticket) { t_ticket = g_tickets.fetch_add(1) + 1; }
+  ~TicketScope() { t_ticket = saved; }
+};
+
 // A small persistent pool of worker threads for the host passes (tree walks,
 // blob writing).  run(n, body) calls body() on the caller and on up to n-1
 // workers at once; body pulls its work from a shared counter, so it is
-// correct with any number of participants.  The workers form a few teams, and
-// one parallel region runs on a team at a time: calls from different threads
-// (several preparations in flight at once) take different teams, each with
-// its own workers.  A caller that finds every team busy runs body() alone.
-// The pool is never destroyed (its threads end with the process) and a forked
+// correct with any number of participants.  Regions opened by different
+// threads (several preparations in flight at once) share one crew: a free
+// worker joins the open region with the smallest ticket that still wants
+// workers, so the preparation that started first gets every free worker and
+// is done soonest, and the others take what it leaves (its serial parts, the
+// end of its regions).  A region's caller closes it to further workers when
+// its own body() returns and then waits for the workers that joined.  The
+// pool is never destroyed (its threads end with the process) and a forked
 // child starts a fresh one.
 //
-// A region is published as one atomic word (generation << 16 | workers
-// wanted).  Workers that have just finished a region poll that word for a
-// while (first with a pause instruction, then yielding the core) before they
-// block on the condition variable, so back-to-back regions -- a model
-// preparation runs several, a few hundred microseconds apart -- start without
-// a wake-up through the kernel; the caller polls the pending count the same
-// way.
+// Workers that find nothing to join poll a version word, bumped whenever a
+// region opens, for a while (first with a pause instruction, then yielding
+// the core) before they block on the condition variable, so back-to-back
+// regions -- a model preparation runs several, a few hundred microseconds
+// apart -- start without a wake-up through the kernel; the caller polls the
+// count of joined workers the same way.
 class Pool {
  public:
   static Pool& get() {
@@ -129,21 +144,47 @@ class Pool {
 
   template <typename Body>
   void run(int n, Body&& body) {
-    if (n > 1)
-      for (Team& t : teams_)
-        if (t.run_mu.try_lock()) {
-          t.run(std::min(n, kMaxWorkers + 1), body);
-          t.run_mu.unlock();
-          return;
-        }
+    if (n <= 1) {
+      body();
+      return;
+    }
+    std::function<void()> fn(std::ref(body));
+    Region r;
+    r.job = &fn;
+    r.want = std::min(n - 1, kMaxWorkers);
+    {
+      std::lock_guard<std::mutex> lock(mu_);
+      r.ticket = t_ticket != 0 ? t_ticket : g_tickets.fetch_add(1) + 1;
+      while ((int)workers_ < r.want) {
+        std::thread([this] { loop(); }).detach();
+        ++workers_;
+      }
+      auto at = open_.begin();
+      while (at != open_.end() && (*at)->ticket <= r.ticket) ++at;
+      open_.insert(at, &r);
+      version_.fetch_add(1, std::memory_order_release);
+      if (sleepers_ > 0) cv_.notify_all();
+    }
     body();
+    {
+      std::lock_guard<std::mutex> lock(mu_);
+      open_.erase(std::find(open_.begin(), open_.end(), &r));
+    }
+    // no worker joins a closed region; wait for those inside it
+    for (int i = 0; r.active.load(std::memory_order_acquire) != 0; ++i) relax(i);
   }
 
  private:
-  static constexpr int kTeams = 4;
   static constexpr int kMaxWorkers = 63;
   static constexpr int kPauseRounds = 2048;     // ~ tens of microseconds
   static constexpr int kYieldRounds = 4096;     // then yield the core, ~ a millisecond
+
+  struct Region {
+    const std::function<void()>* job = nullptr;
+    uint64_t ticket = 0;
+    int want = 0;                   // workers that may still join (under mu_)
+    std::atomic<int> active{0};     // workers that joined and have not left
+  };
 
   static void relax(int i) {
 #if defined(__x86_64__) || defined(__i386__)
@@ -164,65 +205,47 @@ class Pool {
     return m;
   }
 
-  struct Team {
-    std::mutex run_mu;                  // held by the caller of a region
-    std::mutex mu;
-    std::condition_variable cv;
-    std::vector<std::thread> workers;   // under mu
-    const std::function<void()>* job = nullptr;
-    uint64_t gen = 0;                   // under mu
-    int sleepers = 0;                   // under mu
-    std::atomic<uint64_t> state{0};     // gen << 16 | workers wanted
-    std::atomic<int> pending{0};
-
-    template <typename Body>
-    void run(int n, Body& body) {
-      std::function<void()> fn(std::ref(body));
-      bool wake;
+  void loop() {
+    for (;;) {
+      Region* r = nullptr;
+      uint64_t seen;
       {
-        std::lock_guard<std::mutex> lock(mu);
-        while ((int)workers.size() < n - 1) {
-          const int id = (int)workers.size();
-          workers.emplace_back([this, id] { loop(id); });
-          workers.back().detach();
+        std::lock_guard<std::mutex> lock(mu_);
+        for (Region* x : open_)
+          if (x->want > 0) {
+            r = x;
+            break;
+          }
+        if (r != nullptr) {
+          r->want -= 1;
+          r->active.fetch_add(1, std::memory_order_relaxed);
         }
-        job = &fn;
-        pending.store(n - 1, std::memory_order_relaxed);
-        gen += 1;
-        state.store(gen << 16 | (uint64_t)(n - 1), std::memory_order_release);
-        wake = sleepers > 0;
+        seen = version_.load(std::memory_order_relaxed);
       }
-      if (wake) cv.notify_all();
-      body();
-      for (int i = 0; pending.load(std::memory_order_acquire) != 0; ++i) relax(i);
-    }
-
-    void loop(int id) {
-      uint64_t seen = 0;
-      for (;;) {
-        uint64_t s = state.load(std::memory_order_acquire);
-        for (int i = 0; (s >> 16) == seen && i < kPauseRounds + kYieldRounds; ++i) {
-          relax(i);
-          s = state.load(std::memory_order_acquire);
-        }
-        if ((s >> 16) == seen) {
-          std::unique_lock<std::mutex> lock(mu);
-          ++sleepers;
-          cv.wait(lock, [&] { return (state.load(std::memory_order_relaxed) >> 16) != seen; });
-          --sleepers;
-          s = state.load(std::memory_order_relaxed);
-        }
-        seen = s >> 16;
-        // the region of generation `seen` cannot end (nor job change) before
-        // every worker it wants, this one included, has counted down
-        if (id >= (int)(s & 0xffff)) continue;
-        (*job)();
-        pending.fetch_sub(1, std::memory_order_release);
+      if (r != nullptr) {
+        // the region stays alive until its caller has seen active drop to 0
+        (*r->job)();
+        r->active.fetch_sub(1, std::memory_order_release);
+        continue;
+      }
+      int i = 0;
+      while (version_.load(std::memory_order_acquire) == seen && i < kPauseRounds + kYieldRounds)
+        relax(i++);
+      if (version_.load(std::memory_order_acquire) == seen) {
+        std::unique_lock<std::mutex> lock(mu_);
+        ++sleepers_;
+        cv_.wait(lock, [&] { return version_.load(std::memory_order_relaxed) != seen; });
+        --sleepers_;
       }
     }
-  };
+  }
 
-  Team teams_[kTeams];
+  std::mutex mu_;
+  std::condition_variable cv_;
+  std::vector<Region*> open_;        // under mu_, ascending ticket
+  int workers_ = 0;                  // under mu_
+  int sleepers_ = 0;                 // under mu_
+  std::atomic<uint64_t> version_{0}; // bumped (under mu_) when a region opens
 };
 
 // Per-thread state for walking trees depth first.  The merged elements of the
@@ -545,11 +568,11 @@ int usable_cores() {
 // takes every core: the deep model (646 k nodes) prepares in 4.5 ms on 16
 // threads against 5.0 ms on 14.
 //
-// gts_set_host_threads caps this for the calls of one thread: several
-// preparations in flight at once, each on part of the cores, prepare more
-// models per second than one at a time on all of them (the deep model: two
-// at once on 8 cores each, one every 3.6 ms; one on 16 cores, one every
-// 5.1 ms), because no single preparation uses 16 cores fully.
+// gts_set_host_threads caps this for the calls of one thread.  Several
+// preparations in flight at once prepare more models per second than one at
+// a time, because no single preparation uses 16 cores fully (its packing is
+// serial); they share the pool, which gives every free worker to the one
+// that started first.
 thread_local int32_t t_thread_cap = 0;
 
 int host_threads(int64_t work) {
@@ -1582,6 +1605,7 @@ gts_status prepare_model(const gts_ensemble* ens, int32_t bin_capacity, int32_t 
                          int32_t dtype, gts_model* model, void* host_blob,
                          int64_t blob_capacity, double* bias, const PlanOut* po) {
   clear_error();
+  const TicketScope ticket;   // this preparation's regions, before later ones
   if (model == nullptr) return fail(GTS_EINVAL, "model must not be NULL");
   if (bin_capacity < 1 || bin_capacity > kMaxPathLen)
     return fail(GTS_EINVAL, "bin_capacity %d outside [1, %d]", bin_capacity, kMaxPathLen);

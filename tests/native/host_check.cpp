@@ -4,9 +4,10 @@
 // current directory and, for every packing heuristic, two bin capacities and
 // both dtypes, prepares the model twice (size query, then the blob) and
 // compares the blob byte for byte with the three-call route
-// extract -> pack -> layout.  Then three threads with different thread caps
+// extract -> pack -> layout.  Then six threads with different thread caps
 // (gts_set_host_threads) prepare the BFD model at the same time, several
-// times each, and every blob must equal the one-at-a-time blob.  Exit status
+// times each, sharing the worker pool, and every blob must equal the
+// one-at-a-time blob.  Exit status
 // 0 only if every case matches.
 #include <cstdio>
 #include <cstdlib>
@@ -78,11 +79,11 @@ int main() {
     std::vector<char> want((size_t)m.bytes);
     std::vector<double> want_bias((size_t)G);
     gts_prepare_model(&e, 64, GTS_PACK_BFD, dt, &m, want.data(), m.bytes, want_bias.data());
-    int wrong[3] = {0, 0, 0};
+    int wrong[6] = {0, 0, 0, 0, 0, 0};
     std::vector<std::thread> th;
-    for (int k = 0; k < 3; ++k)
+    for (int k = 0; k < 6; ++k)
       th.emplace_back([&, k] {
-        gts_set_host_threads(k == 0 ? 4 : k == 1 ? 2 : 0);
+        gts_set_host_threads(k == 0 ? 4 : k == 1 ? 2 : k == 2 ? 1 : 0);
         for (int r = 0; r < 4; ++r) {
           gts_model mk;
           std::vector<char> blob((size_t)m.bytes);
@@ -93,7 +94,9 @@ int main() {
         }
       });
     for (auto& t : th) t.join();
-    const bool same = wrong[0] + wrong[1] + wrong[2] == 0;
+    int nwrong = 0;
+    for (int k = 0; k < 6; ++k) nwrong += wrong[k];
+    const bool same = nwrong == 0;
     std::printf("concurrent dtype %d %s\n", dt, same ? "same" : "DIFFERENT");
     if (!same) ++bad;
   }
