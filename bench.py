@@ -11,8 +11,9 @@ for the batch (the paths none of its rows reaches dropped, gts_prune_model;
 packing and each path's place (gts_plan_model), the plan and the ensemble
 are uploaded, and the GPU extracts, merges and lays out the paths and sums
 the bias (gts_build_model_device); --build host prepares the whole blob on
-the host (gts_prepare_model) and uploads it.  The rows X are resident in HBM
-before timing starts.  `value` is rows explained per second over the timed
+the host (gts_prepare_model) and uploads it.  Three steps' host work runs at
+once on the library's worker pool, which serves the oldest first.  The rows X
+are resident in HBM before timing starts.  `value` is rows explained per second over the timed
 steps.
 
 The same JSON line carries:
@@ -31,9 +32,10 @@ The same JSON line carries:
   kernel        kernel-only rows/s over back-to-back launches;
   configs       every workload of the suite (tiny, covtype-shaped, deep fp32
                 and fp64, wide multiclass, interactions): host preparation,
-                kernel time and rows/s, live pairs, modelled rate and
-                fraction, the pruning pass and the kernel on the pruned model,
-                and the CPU oracle's rate on a row prefix;
+                device extraction, the plan and the device build where the
+                model admits a plan, kernel time and rows/s, live pairs,
+                modelled rate and fraction, the pruning pass and the kernel on
+                the pruned model, and the CPU oracle's rate on a row prefix;
   cpu_baseline  the fp64 CPU oracle (Algorithm 1, OpenMP over rows) on a row
                 prefix of the headline batch, on the host's cores, and on one
                 thread.
@@ -622,6 +624,48 @@ def time_device_extract(torch, gts, ens, reps=5):
     return 1e3 * float(np.median(dev)), 1e3 * float(np.median(host))
 
 
+def time_device_build(torch, gts, ens, dtype, reps=10):
+    """A device build as the step loop runs it: gts_plan_model on the host
+    into pinned memory (wall clock), the plan's upload, and
+    gts_build_model_device on the GPU (HIP events around it on the current
+    stream); None when the model admits no plan."""
+    import ctypes
+    try:
+        desc, plan, _ = gts.plan_model(ens, dtype)
+    except gts.GtsError:
+        return None
+    L = gts.lib()
+    s, keep = gts._ensemble_struct(ens)
+    pinned = torch.empty(int(plan.bytes), dtype=torch.uint8).pin_memory()
+    d_plan = torch.empty(int(plan.bytes), dtype=torch.uint8, device="cuda")
+    dens = gts.DeviceEnsemble(ens)
+    out = torch.empty(int(desc.bytes), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(max(1, gts.build_workspace_bytes(plan)), dtype=torch.uint8, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    host, up, dev = [], [], []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        st = L.gts_plan_model(ctypes.byref(s), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype],
+                              ctypes.byref(desc), ctypes.byref(plan),
+                              ctypes.c_void_p(pinned.data_ptr()), pinned.numel())
+        t1 = time.perf_counter()
+        if st != gts.GTS_OK:
+            raise RuntimeError(f"gts_plan_model: {L.gts_last_error().decode()}")
+        d_plan.copy_(pinned, non_blocking=True)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        e0.record()
+        gts.build_model_device(dens, desc, plan, d_plan, dtype, out=out, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        host.append(t1 - t0)
+        up.append(t2 - t1)
+        dev.append(e0.elapsed_time(e1))
+    return {"plan_ms_host": 1e3 * float(np.median(host)),
+            "plan_upload_ms": 1e3 * float(np.median(up)),
+            "build_ms_device": float(np.median(dev)), "plan_bytes": int(plan.bytes)}
+
+
 def cpu_threads() -> int:
     threads = len(os.sched_getaffinity(0))
     env = os.environ.get("OMP_NUM_THREADS")
@@ -690,6 +734,7 @@ def suite_entry(torch, gts, synth, oracle, workload, dtype, interactions, reps, 
         "launch": gts.launch_config(model, rows, interactions),
         "host_prepare_ms": host_ms, "upload_ms": upload_ms, "model_bytes": blob_bytes,
         "extract_ms_device": dev_extract_ms, "extract_ms_host": host_extract_ms,
+        "device_build": time_device_build(torch, gts, ens, dtype),
         "kernel_ms_median": med, "kernel_ms_mean": float(k.mean()),
         "kernel_ms_std": float(k.std()), "kernel_runs": len(k),
         "kernel_rows_per_s": rows / (med * 1e-3),
