@@ -584,18 +584,36 @@ def pruned_counts(gts, pm):
     return nb, int(np.count_nonzero(feat < 0)), ne
 
 
-def time_prepare(gts, ens, dtype, reps=5):
+def warm_host(fn, seconds=0.2):
+    """Calls fn back to back for a while: host cores that have idled (the
+    suite's other parts, model generation) take a while to wake and clock up,
+    and a few timed calls right after would catch that instead of the
+    preparation itself."""
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        fn()
+
+
+def time_prepare(gts, ens, dtype, reps=20):
     """Host preparation (one gts_prepare_model call) into pinned memory, and
     the upload from there into a device buffer, as the step loop does them."""
+    import ctypes
     import torch
     desc, blob, _ = gts.prepare_blob(ens, dtype)
     pinned = torch.empty(len(blob), dtype=torch.uint8).pin_memory()
     dev = torch.empty(len(blob), dtype=torch.uint8, device="cuda")
-    view = pinned.numpy()
+    L = gts.lib()
+    s, keep = gts._ensemble_struct(ens)
+    bias = np.zeros(ens.num_groups, np.float64)
+    args = (ctypes.byref(s), 64, gts.PACK_ALGS["bfd"], gts.DTYPES[dtype], ctypes.byref(desc),
+            ctypes.c_void_p(pinned.data_ptr()), pinned.numel(),
+            bias.ctypes.data_as(ctypes.c_void_p))
+    warm_host(lambda: L.gts_prepare_model(*args))
     host, up = [], []
     for _ in range(reps):
         t0 = time.perf_counter()
-        desc, blob, bias = gts.prepare_blob(ens, dtype, out=view)
+        if L.gts_prepare_model(*args) != gts.GTS_OK:
+            raise RuntimeError(f"gts_prepare_model: {L.gts_last_error().decode()}")
         t1 = time.perf_counter()
         dev.copy_(pinned, non_blocking=True)
         torch.cuda.synchronize()
@@ -605,13 +623,14 @@ def time_prepare(gts, ens, dtype, reps=5):
     return 1e3 * float(np.median(host)), 1e3 * float(np.median(up)), int(len(blob))
 
 
-def time_device_extract(torch, gts, ens, reps=5):
+def time_device_extract(torch, gts, ens, reps=10):
     """gts_extract_paths_device (paths and bias on the GPU from device-resident
     node arrays), wall clock per call including its two count read-backs;
     gts_extract_paths on the host for comparison."""
     dens = gts.DeviceEnsemble(ens)
     gts.extract_paths_device(dens)
     torch.cuda.synchronize()
+    warm_host(lambda: gts.extract_paths(ens))
     dev, host = [], []
     for _ in range(reps):
         t0 = time.perf_counter()
@@ -642,6 +661,9 @@ def time_device_build(torch, gts, ens, dtype, reps=10):
     out = torch.empty(int(desc.bytes), dtype=torch.uint8, device="cuda")
     ws = torch.empty(max(1, gts.build_workspace_bytes(plan)), dtype=torch.uint8, device="cuda")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    warm_host(lambda: L.gts_plan_model(ctypes.byref(s), 64, gts.PACK_ALGS["bfd"],
+                                       gts.DTYPES[dtype], ctypes.byref(desc), ctypes.byref(plan),
+                                       ctypes.c_void_p(pinned.data_ptr()), pinned.numel()))
     host, up, dev = [], [], []
     for _ in range(reps):
         t0 = time.perf_counter()

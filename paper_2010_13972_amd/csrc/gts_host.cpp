@@ -152,22 +152,30 @@ class Pool {
     Region r;
     r.job = &fn;
     r.want = std::min(n - 1, kMaxWorkers);
+    r.ticket = t_ticket != 0 ? t_ticket : g_tickets.fetch_add(1) + 1;
     {
-      std::lock_guard<std::mutex> lock(mu_);
-      r.ticket = t_ticket != 0 ? t_ticket : g_tickets.fetch_add(1) + 1;
-      while ((int)workers_ < r.want) {
+      std::lock_guard<std::mutex> lock(grow_mu_);
+      while (workers_.load(std::memory_order_relaxed) < r.want) {
         std::thread([this] { loop(); }).detach();
-        ++workers_;
+        workers_.fetch_add(1, std::memory_order_relaxed);
       }
+    }
+    {
+      SpinGuard g(list_);
       auto at = open_.begin();
       while (at != open_.end() && (*at)->ticket <= r.ticket) ++at;
       open_.insert(at, &r);
       version_.fetch_add(1, std::memory_order_release);
+    }
+    {
+      // a worker about to sleep checks the version under sleep_mu_, so it
+      // either sees the new one or is waiting when this notifies
+      std::lock_guard<std::mutex> lock(sleep_mu_);
       if (sleepers_ > 0) cv_.notify_all();
     }
     body();
     {
-      std::lock_guard<std::mutex> lock(mu_);
+      SpinGuard g(list_);
       open_.erase(std::find(open_.begin(), open_.end(), &r));
     }
     // no worker joins a closed region; wait for those inside it
@@ -182,8 +190,19 @@ class Pool {
   struct Region {
     const std::function<void()>* job = nullptr;
     uint64_t ticket = 0;
-    int want = 0;                   // workers that may still join (under mu_)
+    int want = 0;                   // workers that may still join (under list_)
     std::atomic<int> active{0};     // workers that joined and have not left
+  };
+
+  // The region list's lock: held for a few list operations at a time, by
+  // callers opening or closing a region and by workers joining one, so a
+  // waiter spins instead of sleeping in the kernel.
+  struct SpinGuard {
+    std::atomic_flag& f;
+    explicit SpinGuard(std::atomic_flag& flag) : f(flag) {
+      for (int i = 0; f.test_and_set(std::memory_order_acquire); ++i) relax(i);
+    }
+    ~SpinGuard() { f.clear(std::memory_order_release); }
   };
 
   static void relax(int i) {
@@ -210,7 +229,7 @@ class Pool {
       Region* r = nullptr;
       uint64_t seen;
       {
-        std::lock_guard<std::mutex> lock(mu_);
+        SpinGuard g(list_);
         for (Region* x : open_)
           if (x->want > 0) {
             r = x;
@@ -232,20 +251,22 @@ class Pool {
       while (version_.load(std::memory_order_acquire) == seen && i < kPauseRounds + kYieldRounds)
         relax(i++);
       if (version_.load(std::memory_order_acquire) == seen) {
-        std::unique_lock<std::mutex> lock(mu_);
+        std::unique_lock<std::mutex> lock(sleep_mu_);
         ++sleepers_;
-        cv_.wait(lock, [&] { return version_.load(std::memory_order_relaxed) != seen; });
+        cv_.wait(lock, [&] { return version_.load(std::memory_order_acquire) != seen; });
         --sleepers_;
       }
     }
   }
 
-  std::mutex mu_;
+  std::atomic_flag list_ = ATOMIC_FLAG_INIT;
+  std::vector<Region*> open_;         // under list_, ascending ticket
+  std::atomic<uint64_t> version_{0};  // bumped (under list_) when a region opens
+  std::mutex grow_mu_;                // starting workers
+  std::atomic<int> workers_{0};
+  std::mutex sleep_mu_;
   std::condition_variable cv_;
-  std::vector<Region*> open_;        // under mu_, ascending ticket
-  int workers_ = 0;                  // under mu_
-  int sleepers_ = 0;                 // under mu_
-  std::atomic<uint64_t> version_{0}; // bumped (under mu_) when a region opens
+  int sleepers_ = 0;                  // under sleep_mu_
 };
 
 // Per-thread state for walking trees depth first.  The merged elements of the
