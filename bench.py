@@ -983,8 +983,10 @@ def main():
                          "sweep (Fig. 4)")
     ap.add_argument("--sweep-workloads", default="covtype_med,deep,interactions")
     ap.add_argument("--cpu-limit", type=float, default=4.0)
-    ap.add_argument("--streams", type=int, default=1,
-                    help="compute streams the pipelined steps alternate between")
+    ap.add_argument("--streams", type=int, default=2,
+                    help="compute streams the pipelined steps alternate between (default "
+                         "two: a step's build and pruning overlap the previous step's "
+                         "SHAP kernel)")
     ap.add_argument("--prep-threads", type=int, default=0,
                     help="host threads each preparation in flight may use (0: every core)")
     ap.add_argument("--preps", type=int, default=0,
@@ -1136,7 +1138,10 @@ def main():
                      "note": "achieved: op model over the live (row, path) pairs (a pair "
                              "whose zero-cover element misses the row contributes exactly "
                              "0; pruning drops only paths without live pairs) / mean "
-                             "in-step launch time of the kernel; peak is the packed-FP32 "
+                             "in-step launch time of the kernel (with two compute "
+                             "streams it shares the GPU with the next step's build and "
+                             "pruning, so its span is longer than alone: "
+                             "kernel_ms_back_to_back); peak is the packed-FP32 "
                              "vendor figure (non-packed FP32 FMAs measured about 129 "
                              "TFLOP/s); dense_equivalent_tflops counts every pair"},
         "launch": gts.launch_config(model, rows, inter),
