@@ -8,12 +8,13 @@ bins and the device layout of the model, then on the device the model pruned
 for the batch (the paths none of its rows reaches dropped, gts_prune_model;
 --no-prune leaves this out) and the SHAP kernel over the batch.  By default
 (--build auto) the host runs the validating walk that counts the paths, the
-packing and each path's place (gts_plan_model), the plan and the ensemble
-are uploaded, and the GPU extracts, merges and lays out the paths and sums
-the bias (gts_build_model_device); --build host prepares the whole blob on
-the host (gts_prepare_model) and uploads it.  Three steps' host work runs at
-once on the library's worker pool, which serves the oldest first.  The rows X
-are resident in HBM before timing starts.  `value` is rows explained per second over the timed
+packing and each path's place (gts_plan_model), the plan is uploaded, and
+the GPU extracts, merges and lays out the paths and sums the bias
+(gts_build_model_device); --build host prepares the whole blob on the host
+(gts_prepare_model) and uploads it.  Three steps' host work runs at once on
+the library's worker pool, which serves the oldest first.  The inputs, the
+rows X and the ensemble's node arrays, are resident in HBM (the ensemble also
+in host memory, for the plans) before timing starts.  `value` is rows explained per second over the timed
 steps.
 
 The same JSON line carries:
@@ -244,10 +245,12 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                   preps=2, prune=True, device_build=False, prep_threads=None):
     """Whole-path steps, pipelined.  `preps` host threads prepare the models
     of consecutive steps at the same time: step k runs gts_prepare_model on
-    thread k mod preps, into pinned buffer k mod NB (NB = preps + 2).  The
+    thread k mod preps, into pinned buffer k mod NB (NB = preps + nstreams +
+    3: a step's buffers are reused once the kernel of the step NB before it
+    is done, so the host can run that far ahead).  The
     preparations share the library's worker pool, which serves the one that
-    started first (each may use every core unless `prep_threads` caps it
-    through gts_set_host_threads).  The main
+    started first; each may use every core unless `prep_threads` caps it
+    (through gts_set_host_threads).  The main
     thread uploads step k's model on a copy stream into device buffer k mod NB
     once it is prepared and launches the kernel of step k as soon as that
     upload has finished, on compute stream k mod nstreams; the compute
@@ -259,9 +262,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     stream, into that stream's workspace) and runs the kernel on the pruned
     model.  With `device_build`, a preparation is gts_plan_model (the host
     half: the counting walk, the packing, each path's place) into a pinned
-    plan buffer; the ensemble's node arrays (from pinned copies) go up as soon
-    as the step's device buffers are free, the plan once it is made, and the
-    compute stream runs
+    plan buffer, the plan goes up once it is made (the ensemble, an input
+    like X, is resident in HBM and in host memory), and the compute stream
+    runs
     gts_build_model_device (extraction and merging into the blob on the GPU)
     before the pruning and the kernel.  Timed on the host clock; the build,
     the pruning and the kernel are bracketed by HIP events on their stream,
@@ -273,7 +276,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     import threading
     L = gts.lib()
     launch = L.gts_shap_interactions if interactions else L.gts_shap
-    NB = preps + 2
+    NB = preps + nstreams + 3
     computes = [torch.cuda.current_stream()] + [torch.cuda.Stream()
                                                 for _ in range(nstreams - 1)]
     copy = torch.cuda.Stream()
@@ -285,18 +288,29 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
         # one device copy per buffer, the plan buffers and the build workspace
         _, plan0, hp0 = gts.plan_model(ens, dtype)
         _, arrs = gts._ensemble_struct(ens)
-        ens_pin = {k: torch.from_numpy(v).pin_memory() for k, v in arrs.items()}
-        ens_dev = [{k: torch.empty_like(v, device="cuda") for k, v in ens_pin.items()}
-                   for _ in range(NB)]
+        # the node arrays in one buffer (each 256-byte aligned), so a step's
+        # ensemble upload is one copy
+        names = ("off", "group", "left", "right", "feat", "thr", "cover", "value")
+        offs, total = {}, 0
+        for k in names:
+            offs[k] = total
+            total += (arrs[k].nbytes + 255) // 256 * 256
+        ens_host = torch.empty(total, dtype=torch.uint8)
+        for k in names:
+            ens_host[offs[k]:offs[k] + arrs[k].nbytes].copy_(
+                torch.from_numpy(arrs[k].view(np.uint8)))
+        # the ensemble is an input of the path like X: resident in HBM (and
+        # in host memory for the plans) before timing starts, read by every
+        # step's build
+        ens_dev = ens_host.cuda()
 
         def ens_struct(t):
+            base = t.data_ptr()
             return gts._Ensemble(ens.num_features, ens.num_groups, len(arrs["group"]),
-                                 len(arrs["left"]), *(t[k].data_ptr() for k in
-                                                      ("off", "group", "left", "right", "feat",
-                                                       "thr", "cover", "value")))
+                                 len(arrs["left"]), *(base + offs[k] for k in names))
 
-        host_ens = ens_struct(ens_pin)
-        dev_ens = [ens_struct(d) for d in ens_dev]
+        host_ens = ens_struct(ens_host)
+        dev_ens = ens_struct(ens_dev)
         pinned = [torch.empty(int(plan0.bytes), dtype=torch.uint8).pin_memory()
                   for _ in range(NB)]
         dev_plan = [torch.empty(int(plan0.bytes), dtype=torch.uint8, device="cuda")
@@ -323,7 +337,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                       ctypes.byref(descs[i]), ctypes.byref(plans[i]),
                       ctypes.c_void_p(pinned[i].data_ptr()), pinned[i].numel())
                      for i in range(NB)]
-        build_args = [[(ctypes.byref(dev_ens[i]), ctypes.byref(descs[i]), ctypes.byref(plans[i]),
+        build_args = [[(ctypes.byref(dev_ens), ctypes.byref(descs[i]), ctypes.byref(plans[i]),
                         ctypes.c_void_p(dev_plan[i].data_ptr()),
                         ctypes.c_void_p(dev[i].data_ptr()),
                         ctypes.c_void_p(build_ws[j].data_ptr()), build_ws_bytes,
@@ -417,37 +431,19 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
             # that kernel was launched before step k's preparation began.)
             uploaded = collections.deque()
             done = 0
-            ens_sent = [False] * n
-            ens_next = 0
-
-            def send_ensemble(k):
-                with torch.cuda.stream(copy):
-                    for key, t in ens_pin.items():
-                        ens_dev[k % NB][key].copy_(t, non_blocking=True)
-                ens_sent[k] = True
 
             while done < n:
                 busy = False
                 if errors:
                     raise errors[0]
-                # a device build's ensemble upload needs no plan: it goes out
-                # as soon as the step's device buffers are free (the kernel of
-                # step k - NB launched and done), ahead of the plan's upload
-                # on the same copy stream
-                while (device_build and ens_next < n and
-                       (ens_next < NB or launched[ens_next - NB].is_set()) and
-                       consumed[ens_next % NB].query()):
-                    if not ens_sent[ens_next]:
-                        send_ensemble(ens_next)
-                    ens_next += 1
-                    busy = True
-                while ready and consumed[ready[0] % NB].query():
-                    k = ready.popleft()
+                # any prepared step whose buffers are free, not only the
+                # oldest: a step prepared early must not wait behind one
+                # whose buffers a late kernel still holds
+                for k in [k for k in list(ready) if consumed[k % NB].query()]:
+                    ready.remove(k)
                     i = k % NB
                     with torch.cuda.stream(copy):
                         if device_build:
-                            if not ens_sent[k]:
-                                send_ensemble(k)
                             dev_plan[i].copy_(pinned[i], non_blocking=True)
                         else:
                             dev[i].copy_(pinned[i], non_blocking=True)
@@ -1104,7 +1100,7 @@ def main():
                    "output": (f"phi[{rows}, {ens.num_groups}, {ens.num_features + 1}"
                               + (f", {ens.num_features + 1}]" if inter else "]")),
                    "step": ("validating walk with path counts + BFD pack (B=64) + each "
-                            "path's place (host) + upload of the plan and the ensemble + "
+                            "path's place (host) + upload of the plan + "
                             "extract + merge + bias + layout (device) "
                             if device_build else
                             "extract + merge + bias + BFD pack (B=64) + layout (host) + upload ")
