@@ -173,13 +173,21 @@ class Pool {
       std::lock_guard<std::mutex> lock(sleep_mu_);
       if (sleepers_ > 0) cv_.notify_all();
     }
+    // the region leaves the list, and every worker that joined it has left
+    // it, before it goes out of scope, also when body() throws
+    struct Close {
+      Pool& p;
+      Region& r;
+      ~Close() {
+        {
+          SpinGuard g(p.list_);
+          p.open_.erase(std::find(p.open_.begin(), p.open_.end(), &r));
+        }
+        // no worker joins a closed region; wait for those inside it
+        for (int i = 0; r.active.load(std::memory_order_acquire) != 0; ++i) relax(i);
+      }
+    } close{*this, r};
     body();
-    {
-      SpinGuard g(list_);
-      open_.erase(std::find(open_.begin(), open_.end(), &r));
-    }
-    // no worker joins a closed region; wait for those inside it
-    for (int i = 0; r.active.load(std::memory_order_acquire) != 0; ++i) relax(i);
   }
 
  private:
