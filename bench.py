@@ -1110,7 +1110,7 @@ def main():
                            + "worker pool that serves the oldest first; uploads and host "
                            + "work overlap the kernels of earlier steps",
                    "compute_streams": args.streams, "preparations_in_flight": preps,
-                   "model_build": "device" if device_build else "host",
+                   "blob_built_on": "device" if device_build else "host",
                    "pruned_for_the_batch": ({"paths": ppaths, "path_elements": pelems,
                                              "bins": pbins} if prune else None)},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
