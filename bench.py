@@ -242,7 +242,8 @@ def kernel_fn(gts, interactions):
 
 
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1,
-                  preps=2, prune=True, device_build=False, prep_threads=None):
+                  preps=2, prune=True, device_build=False, prep_threads=None,
+                  keep_outputs=False):
     """Whole-path steps, pipelined.  `preps` host threads prepare the models
     of consecutive steps at the same time: step k runs gts_prepare_model on
     thread k mod preps, into pinned buffer k mod NB (NB = preps + nstreams +
@@ -268,7 +269,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     gts_build_model_device (extraction and merging into the blob on the GPU)
     before the pruning and the kernel.  Timed on the host clock; the build,
     the pruning and the kernel are bracketed by HIP events on their stream,
-    each preparation by the host clock of its thread."""
+    each preparation by the host clock of its thread.  With `keep_outputs`
+    (for tests, not for timing) every timed step's output is copied on its
+    stream after its kernel, and the copies are returned last."""
     import collections
     import ctypes
     import gc
@@ -324,6 +327,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     copied = [torch.cuda.Event() for _ in range(NB)]    # upload from pinned[i] done
     consumed = [torch.cuda.Event() for _ in range(NB)]  # kernel reading dev[i] done
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(steps)]
+    kept = [None] * steps
     ens_struct, keep = gts._ensemble_struct(ens)
     descs = [gts.ModelDesc() for _ in range(NB)]
     biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NB)]
@@ -474,6 +478,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                         raise RuntimeError(f"kernel launch: {L.gts_last_error().decode()}")
                     if timed:
                         ev[k][3].record(stream)
+                        if keep_outputs:
+                            with torch.cuda.stream(stream):
+                                kept[k] = outs[j].clone()
                     consumed[i].record(stream)
                     launched[k].set()
                     done += 1
@@ -524,8 +531,9 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     build_ms = np.array([a.elapsed_time(b) for a, b, c, d in ev])
     prune_ms = np.array([b.elapsed_time(c) for a, b, c, d in ev])
     kern = np.array([c.elapsed_time(d) for a, b, c, d in ev])
-    return (wall, kern, prune_ms, build_ms, outs[(steps - 1) % nstreams], ref_model,
-            np.array(host_ms))
+    result = (wall, kern, prune_ms, build_ms, outs[(steps - 1) % nstreams], ref_model,
+              np.array(host_ms))
+    return result + (kept,) if keep_outputs else result
 
 
 def time_kernel(torch, gts, model, Xd, reps, interactions):
