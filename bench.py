@@ -243,7 +243,7 @@ def kernel_fn(gts, interactions):
 
 def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstreams=1,
                   preps=2, prune=True, device_build=False, prep_threads=None,
-                  keep_outputs=False):
+                  keep_outputs=False, split=False):
     """Whole-path steps, pipelined.  `preps` host threads prepare the models
     of consecutive steps at the same time: step k runs gts_prepare_model on
     thread k mod preps, into pinned buffer k mod NB (NB = preps + nstreams +
@@ -269,7 +269,13 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     gts_build_model_device (extraction and merging into the blob on the GPU)
     before the pruning and the kernel.  Timed on the host clock; the build,
     the pruning and the kernel are bracketed by HIP events on their stream,
-    each preparation by the host clock of its thread.  With `keep_outputs`
+    each preparation by the host clock of its thread.  With `split`, every
+    step's build and pruning run on one stream and every SHAP kernel on
+    another (the kernel stream waits, on the GPU, for the step's pruned
+    model; the pruning waits for the kernel that last read its workspace,
+    two alternate), so the build and pruning of a step overlap the kernel
+    of the one before while the kernels run back to back; `nstreams` is
+    then unused.  With `keep_outputs`
     (for tests, not for timing) every timed step's output is copied on its
     stream after its kernel, and the copies are returned last."""
     import collections
@@ -280,8 +286,17 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     L = gts.lib()
     launch = L.gts_shap_interactions if interactions else L.gts_shap
     NB = preps + nstreams + 3
+    if split:
+        nstreams = 2   # workspaces and output buffers, alternating by step
     computes = [torch.cuda.current_stream()] + [torch.cuda.Stream()
                                                 for _ in range(nstreams - 1)]
+    # split: builds and prunings on pstream, kernels on kstream
+    kstream = computes[0]
+    pstream = torch.cuda.Stream() if split else None
+    build_streams = [pstream if split else computes[j] for j in range(nstreams)]
+    kernel_streams = [kstream if split else computes[j] for j in range(nstreams)]
+    pruned_ev = [torch.cuda.Event() for _ in range(nstreams)]   # step's model ready
+    shap_done = [torch.cuda.Event() for _ in range(nstreams)]   # kernel read workspace j
     copy = torch.cuda.Stream()
     desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
     nbytes = int(desc0.bytes)
@@ -327,6 +342,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     copied = [torch.cuda.Event() for _ in range(NB)]    # upload from pinned[i] done
     consumed = [torch.cuda.Event() for _ in range(NB)]  # kernel reading dev[i] done
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(steps)]
+    evp = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]   # pruning done
     kept = [None] * steps
     ens_struct, keep = gts._ensemble_struct(ens)
     descs = [gts.ModelDesc() for _ in range(NB)]
@@ -345,7 +361,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                         ctypes.c_void_p(dev_plan[i].data_ptr()),
                         ctypes.c_void_p(dev[i].data_ptr()),
                         ctypes.c_void_p(build_ws[j].data_ptr()), build_ws_bytes,
-                        ctypes.c_void_p(computes[j].cuda_stream))
+                        ctypes.c_void_p(build_streams[j].cuda_stream))
                        for j in range(nstreams)] for i in range(NB)]
     else:
         prep = L.gts_prepare_model
@@ -354,7 +370,8 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                       biases[i].ctypes.data_as(ctypes.c_void_p)) for i in range(NB)]
     run_args = [[(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
                   ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
-                  ctypes.c_void_p(outs[j].data_ptr()), ctypes.c_void_p(computes[j].cuda_stream))
+                  ctypes.c_void_p(outs[j].data_ptr()),
+                  ctypes.c_void_p(kernel_streams[j].cuda_stream))
                  for j in range(nstreams)] for i in range(NB)]
     # batch pruning: per compute stream a workspace (the pruned blob stays in
     # it until that stream's kernel has read it) and the pruned descriptor
@@ -369,11 +386,11 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     prune_args = [[(ctypes.byref(descs[i]), ctypes.c_void_p(dev[i].data_ptr()),
                     ctypes.c_void_p(Xd.data_ptr()), rows, Xd.stride(0),
                     ctypes.c_void_p(wss[j].data_ptr()), ws_bytes.value, ctypes.byref(pdescs[j]),
-                    ctypes.byref(pptrs[j]), ctypes.c_void_p(computes[j].cuda_stream))
+                    ctypes.byref(pptrs[j]), ctypes.c_void_p(build_streams[j].cuda_stream))
                    for j in range(nstreams)] for i in range(NB)] if prune else None
     pruned_args = [(ctypes.byref(pdescs[j]), pptrs[j], ctypes.c_void_p(Xd.data_ptr()), rows,
                     Xd.stride(0), ctypes.c_void_p(outs[j].data_ptr()),
-                    ctypes.c_void_p(computes[j].cuda_stream)) for j in range(nstreams)]
+                    ctypes.c_void_p(kernel_streams[j].cuda_stream)) for j in range(nstreams)]
     cores = min(16, len(os.sched_getaffinity(0)))
     share = 0 if prep_threads is None else prep_threads
 
@@ -457,20 +474,28 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                 while uploaded and copied[uploaded[0] % NB].query():
                     k = uploaded.popleft()
                     i, j = k % NB, k % nstreams
-                    stream = computes[j]
+                    bstream, stream = build_streams[j], kernel_streams[j]
                     if timed:
-                        ev[k][0].record(stream)
+                        ev[k][0].record(bstream)
                     if device_build:
                         st = L.gts_build_model_device(*build_args[i][j])
                         if st != gts.GTS_OK:
                             raise RuntimeError(f"gts_build_model_device: "
                                                f"{L.gts_last_error().decode()}")
                     if timed:
-                        ev[k][1].record(stream)
+                        ev[k][1].record(bstream)
                     if prune:
+                        if split:
+                            # workspace j: free once the kernel two steps back has read it
+                            pstream.wait_event(shap_done[j])
                         st = L.gts_prune_model(*prune_args[i][j])
                         if st != gts.GTS_OK:
                             raise RuntimeError(f"gts_prune_model: {L.gts_last_error().decode()}")
+                    if split:
+                        pruned_ev[j].record(pstream)
+                        if timed:
+                            evp[k].record(pstream)
+                        kstream.wait_event(pruned_ev[j])
                     if timed:
                         ev[k][2].record(stream)
                     st = launch(*(pruned_args[j] if prune else run_args[i][j]))
@@ -481,6 +506,8 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
                         if keep_outputs:
                             with torch.cuda.stream(stream):
                                 kept[k] = outs[j].clone()
+                    if split:
+                        shap_done[j].record(kstream)
                     consumed[i].record(stream)
                     launched[k].set()
                     done += 1
@@ -529,7 +556,8 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
         for t in threads:
             t.join()
     build_ms = np.array([a.elapsed_time(b) for a, b, c, d in ev])
-    prune_ms = np.array([b.elapsed_time(c) for a, b, c, d in ev])
+    prune_ms = (np.array([b.elapsed_time(e) for (a, b, c, d), e in zip(ev, evp)]) if split
+                else np.array([b.elapsed_time(c) for a, b, c, d in ev]))
     kern = np.array([c.elapsed_time(d) for a, b, c, d in ev])
     result = (wall, kern, prune_ms, build_ms, outs[(steps - 1) % nstreams], ref_model,
               np.array(host_ms))
@@ -991,6 +1019,9 @@ def main():
                     help="compute streams the pipelined steps alternate between (default "
                          "two: a step's build and pruning overlap the previous step's "
                          "SHAP kernel)")
+    ap.add_argument("--split-streams", action="store_true",
+                    help="builds and prunings on one stream, every SHAP kernel on another "
+                         "(instead of whole steps alternating between compute streams)")
     ap.add_argument("--prep-threads", type=int, default=0,
                     help="host threads each preparation in flight may use (0: every core)")
     ap.add_argument("--preps", type=int, default=0,
@@ -1075,7 +1106,7 @@ def main():
     preps = args.preps or (3 if ens.num_nodes >= (1 << 17) else 1)
     wall, kern, prune_ms, build_ms, out, model, step_host = time_pipeline(
         torch, gts, ens, Xd, dtype, args.steps, args.warmup, inter, args.streams, preps, prune,
-        device_build, args.prep_threads)
+        device_build, args.prep_threads, split=args.split_streams)
     # the steps' last output against the Python binding's call on the same
     # model (up to the order of the tile additions)
     ref = kernel_fn(gts, inter)(model, Xd)

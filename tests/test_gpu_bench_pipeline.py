@@ -25,20 +25,22 @@ def torch():
     return torch
 
 
-# (where the blob is built, compute streams, preparations in flight)
-CASES = [("device", 2, 3), ("device", 1, 2), ("host", 2, 3)]
+# (where the blob is built, compute streams (0: builds and prunings on one
+# stream, kernels on another), preparations in flight)
+CASES = [("device", 2, 3), ("device", 1, 2), ("host", 2, 3), ("device", 0, 3), ("host", 0, 2)]
 
 
 @pytest.mark.parametrize("build,streams,preps", CASES,
-                         ids=[f"{b}-{s}streams-{p}preps" for b, s, p in CASES])
+                         ids=[f"{b}-{s or 'split'}streams-{p}preps" for b, s, p in CASES])
 def test_every_step_matches_the_binding(torch, build, streams, preps):
     w = synth.random_workload(11, num_trees=80, max_depth=10, M=8, num_groups=2, n_bg=200,
                               rows=3000)
     Xd = torch.from_numpy(w.X).cuda()
     say("pipeline", build, streams, preps)
     steps = 12
-    res = bench.time_pipeline(torch, gts, w.ensemble, Xd, "f32", steps, 2, False, streams,
-                              preps, True, build == "device", None, keep_outputs=True)
+    res = bench.time_pipeline(torch, gts, w.ensemble, Xd, "f32", steps, 2, False, max(1, streams),
+                              preps, True, build == "device", None, keep_outputs=True,
+                              split=streams == 0)
     kept, model = res[-1], res[5]
     ref = gts.shap(model, Xd)
     torch.cuda.synchronize()
