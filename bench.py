@@ -298,13 +298,13 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     pruned_ev = [torch.cuda.Event() for _ in range(nstreams)]   # step's model ready
     shap_done = [torch.cuda.Event() for _ in range(nstreams)]   # kernel read workspace j
     copy = torch.cuda.Stream()
-    desc0, blob, bias0 = gts.prepare_blob(ens, dtype)
+    desc0 = gts.prepare_blob(ens, dtype)[0]
     nbytes = int(desc0.bytes)
     dev = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(NB)]
     if device_build:
         # the ensemble as the host walks it (pinned, so its upload is a DMA),
         # one device copy per buffer, the plan buffers and the build workspace
-        _, plan0, hp0 = gts.plan_model(ens, dtype)
+        plan0 = gts.plan_model(ens, dtype)[1]
         _, arrs = gts._ensemble_struct(ens)
         # the node arrays in one buffer (each 256-byte aligned), so a step's
         # ensemble upload is one copy
@@ -344,7 +344,7 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(steps)]
     evp = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]   # pruning done
     kept = [None] * steps
-    ens_struct, keep = gts._ensemble_struct(ens)
+    ens_struct, keep = gts._ensemble_struct(ens)   # keep: the arrays ens_struct points at
     descs = [gts.ModelDesc() for _ in range(NB)]
     biases = [np.zeros(ens.num_groups, np.float64) for _ in range(NB)]
     rows, M, G = Xd.shape[0], ens.num_features, ens.num_groups
@@ -391,7 +391,6 @@ def time_pipeline(torch, gts, ens, Xd, dtype, steps, warmup, interactions, nstre
     pruned_args = [(ctypes.byref(pdescs[j]), pptrs[j], ctypes.c_void_p(Xd.data_ptr()), rows,
                     Xd.stride(0), ctypes.c_void_p(outs[j].data_ptr()),
                     ctypes.c_void_p(kernel_streams[j].cuda_stream)) for j in range(nstreams)]
-    cores = min(16, len(os.sched_getaffinity(0)))
     share = 0 if prep_threads is None else prep_threads
 
     # persistent preparation threads (their per-thread working memory stays
