@@ -1852,7 +1852,13 @@ gts_status prepare_model(const gts_ensemble* ens, int32_t bin_capacity, int32_t 
         return fail(GTS_EBUFSIZE, "plan capacity %lld < %lld bytes", (long long)po->capacity,
                     (long long)pl.bytes);
       char* hp = po->host_plan;
-      std::memset(hp, 0, (size_t)pl.bytes);
+      // every entry of the five arrays is written below: clear only the
+      // alignment gaps after each one
+      for (int k = 0; k < 5; ++k) {
+        const int64_t end = pl.off[k] + sizes[k];
+        const int64_t next = k < 4 ? pl.off[k + 1] : pl.bytes;
+        std::memset(hp + end, 0, (size_t)(next - end));
+      }
       uint64_t* path_dirs = reinterpret_cast<uint64_t*>(hp + pl.off[0]);
       int32_t* path_dest = reinterpret_cast<int32_t*>(hp + pl.off[1]);
       int32_t* tree_paths = reinterpret_cast<int32_t*>(hp + pl.off[2]);
